@@ -1,0 +1,158 @@
+"""CPU oracle for the PRESTO draft-to-verify round -- TEST INFRASTRUCTURE.
+
+Only the test suite, ``__graft_entry__.smoke()`` and the CPU-baseline leg of
+``bench.py`` may import this package.  It never serves the product path and
+shares no code with the HIP library (``paper_2607_22634_amd``).
+
+Each function wraps one entry point of ``liboracle.so`` (oracle.c), taking
+and returning NumPy arrays.  Storage dtype "bf16" means uint16 bit patterns.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+
+from . import build as _build
+
+_LIB = None
+
+BEST_FIRST = 0
+BEST_FIRST_ALG2 = 1
+
+
+def lib():
+    global _LIB
+    if _LIB is None:
+        if not os.path.exists(_build.LIB):
+            _build.build()
+        _LIB = ctypes.CDLL(_build.LIB)
+        _LIB.oracle_set_threads.argtypes = [ctypes.c_int]
+        _LIB.oracle_get_threads.restype = ctypes.c_int
+    return _LIB
+
+
+def _p(a):
+    return ctypes.c_void_p(0 if a is None else a.ctypes.data)
+
+
+def _dt(dtype: str) -> int:
+    return {"bf16": 0, "f32": 1}[dtype]
+
+
+def _check(a: np.ndarray, dtype: str):
+    want = np.uint16 if dtype == "bf16" else np.float32
+    if a.dtype != want or not a.flags.c_contiguous:
+        raise TypeError(f"expected contiguous {want.__name__} array for {dtype}")
+
+
+def set_threads(n: int) -> None:
+    lib().oracle_set_threads(int(n))
+
+
+def get_threads() -> int:
+    return int(lib().oracle_get_threads())
+
+
+def topk(logits: np.ndarray, k: int, dtype: str):
+    """Per row of logits [rows, V]: top-k ids, log q of those ids, log-sum-exp."""
+    _check(logits, dtype)
+    rows, V = logits.shape
+    ids = np.empty((rows, k), np.int32)
+    lp = np.empty((rows, k), np.float32)
+    lse = np.empty(rows, np.float32)
+    f = lib().oracle_topk
+    f.restype = ctypes.c_int
+    nan_rows = f(ctypes.c_int(_dt(dtype)), _p(logits), ctypes.c_int64(rows), ctypes.c_int32(V),
+                 ctypes.c_int64(V), ctypes.c_int32(k), _p(ids), _p(lp), _p(lse))
+    return ids, lp, lse, int(nan_rows)
+
+
+def build_tree(ids, logprob, rho, lam, root_token, depth: int, k: int, budget: int,
+               branch: int | None = None, mode: int = BEST_FIRST) -> dict:
+    """Best-first tree per sequence; ids/logprob [b, D, k], rho [b, D, k, k, k] or None."""
+    branch = k if branch is None else branch
+    ids = np.ascontiguousarray(ids, np.int32)
+    logprob = np.ascontiguousarray(logprob, np.float32)
+    lam = np.ascontiguousarray(lam, np.float32)
+    root_token = np.ascontiguousarray(root_token, np.int32)
+    rho = None if rho is None else np.ascontiguousarray(rho, np.float32)
+    b = root_token.shape[0]
+    N = budget + 1
+    W = (N + 63) // 64
+    out = {
+        "n_nodes": np.empty(b, np.int32), "parent": np.empty((b, N), np.int32),
+        "token": np.empty((b, N), np.int32), "depth": np.empty((b, N), np.int32),
+        "rank": np.empty((b, N), np.int32), "score": np.empty((b, N), np.float32),
+        "anc": np.empty((b, N, W), np.uint64),
+    }
+    f = lib().oracle_build_tree
+    f.restype = ctypes.c_int
+    rc = f(ctypes.c_int(mode), ctypes.c_int32(b), ctypes.c_int32(depth), ctypes.c_int32(k),
+           ctypes.c_int32(branch), ctypes.c_int32(budget), _p(ids), _p(logprob), _p(rho), _p(lam),
+           _p(root_token), _p(out["n_nodes"]), _p(out["parent"]), _p(out["token"]),
+           _p(out["depth"]), _p(out["rank"]), _p(out["score"]), _p(out["anc"]))
+    if rc != 0:
+        raise ValueError("oracle_build_tree rejected its arguments")
+    return out
+
+
+def _attn_args(dtype, q, k_cache, v_cache, ctx_offsets, k_tree, v_tree, anc, n_nodes, hkv):
+    for a in (q, k_cache, v_cache, k_tree, v_tree):
+        _check(a, dtype)
+    b, N, hq, d = q.shape
+    return b, N, hq, d, [np.ascontiguousarray(ctx_offsets, np.int32),
+                         np.ascontiguousarray(anc, np.uint64),
+                         np.ascontiguousarray(n_nodes, np.int32)]
+
+
+def tree_attention(dtype, q, k_cache, v_cache, ctx_offsets, k_tree, v_tree, anc, n_nodes,
+                   scale: float | None = None):
+    """Tree-masked attention output [b, N, Hq, d] in the storage dtype."""
+    hkv = k_cache.shape[1]
+    b, N, hq, d, (offs, anc, nn) = _attn_args(dtype, q, k_cache, v_cache, ctx_offsets, k_tree,
+                                              v_tree, anc, n_nodes, hkv)
+    scale = 1.0 / np.sqrt(d) if scale is None else scale
+    out = np.empty_like(q)
+    lib().oracle_tree_attention(
+        ctypes.c_int(_dt(dtype)), ctypes.c_int32(b), ctypes.c_int32(N), ctypes.c_int32(hq),
+        ctypes.c_int32(hkv), ctypes.c_int32(d), ctypes.c_double(scale), _p(q), _p(k_cache),
+        _p(v_cache), _p(offs), _p(k_tree), _p(v_tree), _p(anc), _p(nn), _p(out))
+    return out
+
+
+def tree_attention_rows(dtype, q, k_cache, v_cache, ctx_offsets, k_tree, v_tree, anc, n_nodes,
+                        rows, scale: float | None = None):
+    """fp64 attention output for the listed (b, n, h) rows only: [len(rows), d]."""
+    hkv = k_cache.shape[1]
+    b, N, hq, d, (offs, anc, nn) = _attn_args(dtype, q, k_cache, v_cache, ctx_offsets, k_tree,
+                                              v_tree, anc, n_nodes, hkv)
+    scale = 1.0 / np.sqrt(d) if scale is None else scale
+    rows = np.ascontiguousarray(rows, np.int32).reshape(-1, 3)
+    out = np.empty((rows.shape[0], d), np.float64)
+    lib().oracle_tree_attention_rows(
+        ctypes.c_int(_dt(dtype)), ctypes.c_int32(b), ctypes.c_int32(N), ctypes.c_int32(hq),
+        ctypes.c_int32(hkv), ctypes.c_int32(d), ctypes.c_double(scale), _p(q), _p(k_cache),
+        _p(v_cache), _p(offs), _p(k_tree), _p(v_tree), _p(anc), _p(nn),
+        ctypes.c_int64(rows.shape[0]), _p(rows), _p(out))
+    return out
+
+
+def accept(dtype, target_logits, parent, token, n_nodes, depth: int) -> dict:
+    """Greedy verification of the tree: accept_len [b], path [b, D+1], bonus [b], argmax [b, N]."""
+    _check(target_logits, dtype)
+    b, N, V = target_logits.shape
+    parent = np.ascontiguousarray(parent, np.int32)
+    token = np.ascontiguousarray(token, np.int32)
+    n_nodes = np.ascontiguousarray(n_nodes, np.int32)
+    out = {"accept_len": np.empty(b, np.int32), "path": np.empty((b, depth + 1), np.int32),
+           "bonus": np.empty(b, np.int32), "target_argmax": np.empty((b, N), np.int32)}
+    f = lib().oracle_accept
+    f.restype = ctypes.c_int
+    nan_rows = f(ctypes.c_int(_dt(dtype)), _p(target_logits), ctypes.c_int32(V), ctypes.c_int64(V),
+                 ctypes.c_int32(b), ctypes.c_int32(N), ctypes.c_int32(depth), _p(parent), _p(token),
+                 _p(n_nodes), _p(out["accept_len"]), _p(out["path"]), _p(out["bonus"]),
+                 _p(out["target_argmax"]))
+    out["nan_rows"] = int(nan_rows)
+    return out
