@@ -1,0 +1,259 @@
+#!/usr/bin/env python3
+"""Tree-verify rounds/s of the PRESTO draft-to-verify hot path on one MI355X.
+
+One step = one whole round on one batch of synthetic inputs already resident
+in HBM: presto_topk -> presto_build_tree -> presto_tree_attention (every
+layer of the workload) -> presto_accept, enqueued on one stream with no host
+synchronisation inside.  Inputs are replicated in device memory and the steps
+cycle through the replicas, so that every step reads data that has been
+pushed out of the 256 MB last-level cache by the steps in between (the
+numbers are DRAM numbers, not cache numbers).
+
+Printed: one JSON line with rounds/s, per-stage times and achieved
+bandwidth, the roofline of the dominant kernel and the CPU oracle timed on
+the host's cores on a bounded sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "tree-verify rounds/sec at Qwen3-8B shapes; HBM GB/s of tree-attn + top-k"
+HBM_PEAK_GBS = 8000.0
+MFMA_BF16_TFLOPS = 2500.0
+MALL_BYTES = 256 << 20
+
+
+def algorithmic_work(w, ctx, n_nodes, depth_of_nodes):
+    """Bytes/flops the method must move or compute (padding and masks excluded)."""
+    e = 2 if w.dtype == "bf16" else 4
+    rows = w.batch * w.depth
+    topk_bytes = rows * w.vocab * e + rows * (8 * w.k + 4)
+    argmax_bytes = int(n_nodes.sum()) * w.vocab * e
+    attn_bytes = sum(w.hkv * (int(c) + int(n)) * w.head_dim * 2 * e + int(n) * w.hq * w.head_dim * 2 * e
+                     for c, n in zip(ctx, n_nodes))
+    attn_flops = 0
+    for s in range(w.batch):
+        d = depth_of_nodes[s, : int(n_nodes[s])].astype(np.int64)
+        attn_flops += int((w.hq * 4 * w.head_dim * (int(ctx[s]) + d + 1)).sum())
+    return {"topk_bytes": topk_bytes, "argmax_bytes": argmax_bytes,
+            "attn_bytes_per_layer": attn_bytes, "attn_flops_per_layer": attn_flops}
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", type=int, default=2, help="synthetic workload 1..5")
+    ap.add_argument("--replicas", type=int, default=0, help="input copies cycled (0 = auto)")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py runs on exactly one GPU: the round is independent per sequence and this "
+              "build measures one GPU's share; use --gpus 1", file=sys.stderr)
+        return 2
+
+    import torch
+
+    import paper_2607_22634_amd as P
+    import synthetic as sy
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    w = sy.workload(args.workload)
+    t_gen = time.time()
+    rin = sy.round_inputs(w)
+
+    def dv(a, dtype=None):
+        if dtype == "bf16" or a.dtype == np.uint16:
+            return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).to(dev)
+        return torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+
+    drafter = dv(rin["drafter_logits"], w.dtype)
+    rho, lam, root = dv(rin["rho"]), dv(rin["lam"]), dv(rin["root_token"])
+    ctx = rin["ctx"]
+    max_ctx = int(ctx.max())
+    layers = []
+    for layer in range(w.layers):
+        att = sy.attention_inputs(w, layer, ctx)
+        layers.append({k: dv(v, w.dtype if v.dtype == np.uint16 else None) for k, v in att.items()})
+
+    # the tree (deterministic) fixes the target rows the verifier produces
+    ids, lp, _ = P.presto_topk(drafter, w.k)
+    tree = P.presto_build_tree(ids, lp, rho, lam, root, w.depth, w.k, w.budget)
+    torch.cuda.synchronize()
+    th = {k: v.cpu().numpy() for k, v in tree.items()}
+    target = dv(sy.target_logits(w, rin["field"], th["parent"], th["rank"], th["n_nodes"]), w.dtype)
+    gen_s = time.time() - t_gen
+
+    work = algorithmic_work(w, ctx, th["n_nodes"], th["depth"])
+    step_bytes = (work["topk_bytes"] + work["argmax_bytes"] + w.layers * work["attn_bytes_per_layer"])
+    reps = args.replicas or max(1, min(16, -(-2 * MALL_BYTES // max(step_bytes, 1))))
+
+    # replicas of every input the round reads; outputs and workspaces preallocated
+    def clone(t):
+        return t.clone()
+
+    R = []
+    for r in range(reps):
+        R.append({
+            "drafter": drafter if r == 0 else clone(drafter),
+            "target": target if r == 0 else clone(target),
+            "layers": layers if r == 0 else [{k: clone(v) for k, v in L.items()} for L in layers],
+        })
+    i32 = dict(dtype=torch.int32, device=dev)
+    rows = w.batch * w.depth
+    topk_out = (torch.empty(rows, w.k, **i32), torch.empty(rows, w.k, dtype=torch.float32, device=dev),
+                torch.empty(rows, dtype=torch.float32, device=dev))
+    topk_ws = torch.empty(max(1, P.lib().presto_topk_workspace(rows, w.vocab, w.k)), dtype=torch.uint8,
+                          device=dev)
+    N = w.n_max
+    tree_out = {k: torch.empty_like(v) for k, v in tree.items()}
+    attn_out = [torch.empty_like(L["q"]) for L in layers]
+    desc = P.AttnDesc(w.batch, N, w.hq, w.hkv, w.head_dim, max_ctx, w.scale,
+                      P.PRESTO_DT_BF16 if w.dtype == "bf16" else P.PRESTO_DT_F32)
+    import ctypes
+    attn_ws_n = P.lib().presto_tree_attention_workspace(ctypes.byref(desc))
+    attn_ws = torch.empty(max(1, attn_ws_n), dtype=torch.uint8, device=dev) if attn_ws_n else None
+    acc_out = {"accept_len": torch.empty(w.batch, **i32), "path": torch.empty(w.batch, w.depth + 1, **i32),
+               "bonus": torch.empty(w.batch, **i32), "target_argmax": torch.empty(w.batch, N, **i32)}
+    acc_ws = torch.empty(P.lib().presto_accept_workspace(w.batch, N, w.vocab), dtype=torch.uint8,
+                         device=dev)
+    flags = torch.zeros(1, **i32)
+
+    stream = torch.cuda.current_stream()
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
+
+    def step(r, e=None):
+        d = R[r]
+        if e: e[0].record(stream)
+        P.presto_topk(d["drafter"], w.k, ids=topk_out[0], logprob=topk_out[1], lse=topk_out[2],
+                      flags=flags, workspace=topk_ws)
+        if e: e[1].record(stream)
+        P.presto_build_tree(topk_out[0], topk_out[1], rho, lam, root, w.depth, w.k, w.budget,
+                            out=tree_out)
+        if e: e[2].record(stream)
+        for li, L in enumerate(d["layers"]):
+            P.presto_tree_attention(L["q"], L["k_cache"], L["v_cache"], L["ctx_offsets"],
+                                    L["k_tree"], L["v_tree"], tree_out["anc"], tree_out["n_nodes"],
+                                    max_ctx, w.scale, out=attn_out[li], workspace=attn_ws)
+        if e: e[3].record(stream)
+        P.presto_accept(d["target"], tree_out["parent"], tree_out["token"], tree_out["n_nodes"],
+                        w.depth, out=acc_out, flags=flags, workspace=acc_ws)
+        if e: e[4].record(stream)
+
+    for i in range(args.warmup):
+        step(i % reps)
+    torch.cuda.synchronize()
+    t_start = torch.cuda.Event(enable_timing=True)
+    t_end = torch.cuda.Event(enable_timing=True)
+    t_start.record(stream)
+    for i in range(args.steps):
+        step((args.warmup + i) % reps, ev[i])
+    t_end.record(stream)
+    torch.cuda.synchronize()
+    total_ms = t_start.elapsed_time(t_end)
+    ms_per_step = total_ms / args.steps
+    stage_ms = np.array([[ev[i][j].elapsed_time(ev[i][j + 1]) for j in range(4)]
+                         for i in range(args.steps)]).mean(axis=0)
+    assert int(flags.item()) == 0, "device flagged NaN inputs"
+
+    names = ["topk", "build_tree", "tree_attention", "accept"]
+    stages = {}
+    for j, nme in enumerate(names):
+        us = float(stage_ms[j] * 1e3)
+        entry = {"us": round(us, 2)}
+        if nme == "topk":
+            entry["GB/s"] = round(work["topk_bytes"] / (us * 1e3), 1)
+        elif nme == "tree_attention":
+            entry["GB/s"] = round(w.layers * work["attn_bytes_per_layer"] / (us * 1e3), 1)
+            entry["TFLOP/s"] = round(w.layers * work["attn_flops_per_layer"] / (us * 1e6), 2)
+        elif nme == "accept":
+            entry["GB/s"] = round(work["argmax_bytes"] / (us * 1e3), 1)
+        stages[nme] = entry
+
+    # roofline of the dominant kernel among the bandwidth/compute-bound stages
+    dom = max(["topk", "tree_attention", "accept"], key=lambda s: stages[s]["us"])
+    us = stages[dom]["us"]
+    if dom == "tree_attention":
+        t_hbm = w.layers * work["attn_bytes_per_layer"] / (HBM_PEAK_GBS * 1e3)
+        t_mfma = w.layers * work["attn_flops_per_layer"] / (MFMA_BF16_TFLOPS * 1e6)
+        if t_mfma > t_hbm:
+            roof = {"bound": "mfma", "achieved": stages[dom]["TFLOP/s"], "peak": MFMA_BF16_TFLOPS,
+                    "unit": "TFLOP/s"}
+        else:
+            roof = {"bound": "hbm", "achieved": stages[dom]["GB/s"], "peak": HBM_PEAK_GBS,
+                    "unit": "GB/s"}
+    else:
+        roof = {"bound": "hbm", "achieved": stages[dom]["GB/s"], "peak": HBM_PEAK_GBS, "unit": "GB/s"}
+    roof["kernel"] = dom
+    roof["frac"] = round(roof["achieved"] / roof["peak"], 4)
+    roof["traffic"] = None
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(w, rin, layers, th, target, args.cpu_seconds)
+
+    line = {
+        "metric": METRIC, "value": round(1e3 / ms_per_step, 2), "unit": "rounds/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 5),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": w.dtype,
+        "data": "synthetic",
+        "config": {"workload": f"{w.name}: batch {w.batch}, block {w.depth}, vocab {w.vocab}, "
+                               f"top-{w.k}, budget {w.budget}, GQA {w.hq}q/{w.hkv}kv d{w.head_dim}, "
+                               f"ctx {w.ctx[0]}-{w.ctx[1]}, {w.layers} layer(s)",
+                   "global_batch": w.batch, "replicas": reps},
+        "sequence_rounds_per_s": round(w.batch * 1e3 / ms_per_step, 2),
+        "stages": stages, "roofline": roof, "cpu_baseline": cpu,
+        "accept_len": acc_out["accept_len"].cpu().tolist(),
+        "gen_seconds": round(gen_s, 1),
+    }
+    print(json.dumps(line), flush=True)
+    return 0
+
+
+def cpu_baseline(w, rin, layers, th, target, seconds):
+    """The oracle, as it stands, on whole rounds of the same workload for ~`seconds`."""
+    import oracle
+
+    threads = len(os.sched_getaffinity(0))
+    oracle.set_threads(threads)
+
+    def host(t):
+        import torch
+        t = t.detach().cpu()
+        return t.view(torch.int16).numpy().view(np.uint16) if t.dtype == torch.bfloat16 else t.numpy()
+
+    att = [{k: host(v) for k, v in L.items()} for L in layers]
+    T = host(target)
+    D, k = w.depth, w.k
+    n = 0
+    t0 = time.time()
+    while True:
+        ids, lp, _, _ = oracle.topk(rin["drafter_logits"], k, w.dtype)
+        tr = oracle.build_tree(ids.reshape(w.batch, D, k), lp.reshape(w.batch, D, k), rin["rho"],
+                               rin["lam"], rin["root_token"], D, k, w.budget)
+        for L in att:
+            oracle.tree_attention(w.dtype, L["q"], L["k_cache"], L["v_cache"], L["ctx_offsets"],
+                                  L["k_tree"], L["v_tree"], tr["anc"], tr["n_nodes"], w.scale)
+        oracle.accept(w.dtype, T, tr["parent"], tr["token"], tr["n_nodes"], D)
+        n += 1
+        if time.time() - t0 >= seconds:
+            break
+    el = time.time() - t0
+    return {"value": round(n / el, 4), "unit": "rounds/s", "cores": oracle.get_threads(),
+            "kind": "oracle", "sample": f"{n} whole round(s) of the same workload ({el:.1f} s)"}
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -1,0 +1,223 @@
+/*
+ * presto.h -- C ABI of libpresto, the MI355X (gfx950) hot path of one
+ * PRESTO draft-to-verify round ("PRESTO: Prefix-Aligned Tree Drafting for
+ * Diffusion Speculative Decoding").
+ *
+ * A round is four calls, enqueued in order on one HIP stream:
+ *
+ *   presto_topk            per-position log-softmax normaliser and top-k
+ *                          candidates of the drafter's block marginals
+ *   presto_build_tree      prefix-aligned scoring and best-first tree
+ *                          construction under a node budget, flattened
+ *                          with its ancestor (tree-attention) mask
+ *   presto_tree_attention  tree-masked verification attention of one
+ *                          target layer over [cached prefix ; tree nodes]
+ *   presto_accept          target argmax per node and the longest
+ *                          accepted root-to-node path plus bonus token
+ *
+ * Conventions shared by every entry point:
+ *
+ * - Every tensor argument is a DEVICE pointer owned by the caller, row
+ *   major with a contiguous innermost dimension.  Strides are in elements.
+ *   The library allocates no device memory: scratch space comes from a
+ *   caller-provided device workspace of at least *_workspace() bytes
+ *   (a null workspace is allowed when that size is 0).
+ * - Every call is asynchronous on `stream` (0 = the null stream).  All
+ *   argument checks happen on the host before anything is launched; on an
+ *   error return nothing was enqueued.
+ * - Storage dtype PRESTO_DT_BF16 means bfloat16 values (raw 16-bit
+ *   patterns), PRESTO_DT_F32 means IEEE float32.
+ * - Data errors found on the device never fault: the kernels OR bits into
+ *   the optional caller word `flags` (device int32, may be NULL), which the
+ *   caller reads after synchronising.  A call never clears `flags`.
+ * - The only host state is a thread-local last-error string.
+ * - Results are deterministic: the same inputs give bit-identical outputs.
+ */
+#ifndef PRESTO_H
+#define PRESTO_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    PRESTO_OK = 0,
+    PRESTO_ERR_INVALID_ARG = -1, /* rejected on the host; nothing launched          */
+    PRESTO_ERR_UNSUPPORTED = -2, /* valid request this build does not implement     */
+    PRESTO_ERR_WORKSPACE = -3,   /* workspace missing or smaller than *_workspace() */
+    PRESTO_ERR_HIP = -4          /* HIP runtime error; see presto_last_error()      */
+} presto_status;
+
+typedef enum { PRESTO_DT_BF16 = 0, PRESTO_DT_F32 = 1 } presto_dtype;
+
+typedef enum {
+    PRESTO_TREE_BEST_FIRST = 0,      /* commit on pop: exactly the B best prefixes by S        */
+    PRESTO_TREE_BEST_FIRST_ALG2 = 1, /* Alg. 2 as printed: add children on expand, then TopB  */
+    PRESTO_TREE_BEAM = 2             /* Alg. 1 beam search with global retention              */
+} presto_tree_mode;
+
+/* Bits ORed into the optional `flags` word. */
+enum {
+    PRESTO_FLAG_NAN_DRAFTER = 1, /* a drafter logit row held a NaN (or +inf)   */
+    PRESTO_FLAG_NAN_TARGET = 2   /* a live target logit row held a NaN         */
+};
+
+/* ------------------------------------------------------------------------ */
+/* Stage 1: log-softmax normaliser and top-k candidates per drafter position.
+ *
+ * Defined by the diffusion marginal q_d = softmax(z_d) of each block
+ * position d (Sec. 3, Eq. 6) and the per-position top-k candidate
+ * extraction of Sec. 5.1 / Appendix C stage II.
+ *
+ * logits     [rows, row_stride] of dtype dt; row r = (sequence, position),
+ *            only the first `vocab` entries of a row are read.
+ * ids        [rows, k] int32 out: the k largest logits of the row, larger
+ *            value first, lower id first among equal values (-0.0 == +0.0).
+ * logprob    [rows, k] fp32 out: log q(id) = z_id - LSE.
+ * lse        [rows] fp32 out, may be NULL: LSE = log sum_v exp(z_v), fp32.
+ *            A row of only -inf gives LSE = -inf and logprob = -inf.
+ * flags      optional: PRESTO_FLAG_NAN_DRAFTER when a row holds NaN or
+ *            +inf; that row's outputs are then unspecified.
+ * Limits: 1 <= k <= 16, k <= vocab, row_stride >= vocab, rows >= 0
+ * (rows == 0 is a no-op).
+ */
+size_t presto_topk_workspace(int64_t rows, int32_t vocab, int32_t k);
+presto_status presto_topk(presto_dtype dt, const void *logits, int64_t rows, int32_t vocab,
+                          int64_t row_stride, int32_t k, int32_t *ids, float *logprob, float *lse,
+                          int32_t *flags, void *ws, size_t ws_bytes, hipStream_t stream);
+
+/* ------------------------------------------------------------------------ */
+/* Stage 2: prefix-aligned scoring and best-first tree construction.
+ *
+ * Token score (Sec. 4.1, Eq. 9): s = fl(log q_d(t) + fl(lambda_d * log rho_d)),
+ * path score S(root) = 0, S(child) = fl(S(parent) + s), fp32, no fused
+ * multiply-add.  rho is a trigram over the two preceding tokens, given as
+ * the lattice log_rho[b, d, r2, r1, r] over candidate ranks, where r1 is the
+ * rank of the parent token and r2 of the grandparent; rank slot 0 stands
+ * for a token outside the block (the root and the committed context).
+ * A child at depth d+1 reads drafter row d (d = 0 .. depth-1).
+ *
+ * Expanding a node yields its top-`branch` candidates by s (larger s first,
+ * lower rank on ties) if its depth is below `depth`, else nothing.
+ * Nodes are ranked by the total order: larger S first, then the rank path
+ * compared lexicographically with a proper prefix before its extensions.
+ *
+ * PRESTO_TREE_BEST_FIRST (Sec. 4.2, Alg. 2 with commit on pop): the tree
+ *   is exactly the `budget` best non-root prefixes of the candidate tree
+ *   (the closed form of Sec. 4.2 via Eq. 3), or the whole candidate tree
+ *   when it has fewer nodes.
+ * PRESTO_TREE_BEST_FIRST_ALG2: Alg. 2 as printed: every pop adds all its
+ *   children to T; stop once T holds `budget` non-root nodes; keep TopB(T).
+ * PRESTO_TREE_BEAM: reserved (returns PRESTO_ERR_UNSUPPORTED).
+ *
+ * The budget counts draft (non-root) nodes: the output has N = budget + 1
+ * rows, row 0 being the root (the last committed token, root_token[b]).
+ */
+typedef struct {
+    int32_t batch;
+    int32_t depth;  /* block length D = maximal tree depth, 1 .. 32           */
+    int32_t k;      /* candidates per position, 1 .. 16                        */
+    int32_t branch; /* children per expansion, 1 .. k                          */
+    int32_t budget; /* B, draft nodes excluding the root, 1 .. 511            */
+    int32_t mode;   /* presto_tree_mode                                        */
+} presto_tree_desc;
+
+/* ids, logprob [batch, depth, k] from presto_topk (logprob <= 0);
+ * log_rho [batch, depth, k, k, k] fp32, finite and <= 0, or NULL for s = log q;
+ * lambda [depth] fp32, finite and >= 0 (device);  root_token [batch] int32.
+ * Outputs, N = budget + 1 rows per sequence, rows in the total order above
+ * (every parent precedes its children):
+ *   n_nodes [batch]             live rows, 1 .. N
+ *   parent, token, depth_out, rank [batch, N] int32   (root: -1, root_token, 0, -1)
+ *   score   [batch, N] fp32     S of the node
+ *   anc     [batch, N, ceil(N/64)] uint64   bit m of row n set iff node m is n
+ *                                           or an ancestor of n
+ * Rows n >= n_nodes: parent/token/depth/rank = -1, score = -inf, anc = 0.
+ */
+size_t presto_build_tree_workspace(const presto_tree_desc *desc);
+presto_status presto_build_tree(const presto_tree_desc *desc, const int32_t *ids,
+                                const float *logprob, const float *log_rho, const float *lambda,
+                                const int32_t *root_token, int32_t *n_nodes, int32_t *parent,
+                                int32_t *token, int32_t *depth_out, int32_t *rank, float *score,
+                                uint64_t *anc, void *ws, size_t ws_bytes, hipStream_t stream);
+
+/* ------------------------------------------------------------------------ */
+/* Stage 3: tree-masked verification attention, one layer.
+ *
+ * Appendix C stage I: each draft token attends to the committed prefix
+ * (its exact KV cache) and to its ancestors in the draft tree (and itself).
+ * For sequence b, node n < n_nodes[b], query head h, KV head g = h / (hq/hkv):
+ *   O[b,n,h] = softmax_j(scale * q[b,n,h] . k_j) v_j
+ * over j in {cache positions of b} U {tree nodes m : anc bit m of row n}.
+ * Rows n >= n_nodes[b] are written as zeros.
+ *
+ * q        [batch, n_max, hq, head_dim]
+ * k_cache, v_cache [sum_b ctx_b, hkv, head_dim], packed: sequence b owns
+ *          positions ctx_offsets[b] .. ctx_offsets[b+1]-1
+ * ctx_offsets [batch + 1] int32 device, non-decreasing, ctx_offsets[0] = 0,
+ *          every ctx_b <= max_ctx (ctx_b = 0 is allowed)
+ * k_tree, v_tree [batch, n_max, hkv, head_dim]: K/V of the tree nodes
+ * anc      [batch, n_max, ceil(n_max/64)] from presto_build_tree
+ * n_nodes  [batch] int32 device, 1 .. n_max
+ * out      [batch, n_max, hq, head_dim], dtype dt
+ * Arithmetic: bf16 inputs use bf16 matrix cores with fp32 accumulation and
+ * fp32 softmax; fp32 inputs use fp32 throughout.
+ * Limits: head_dim in {64, 128}; hq % hkv == 0; n_max <= 1024.
+ */
+typedef struct {
+    int32_t batch, n_max, hq, hkv, head_dim, max_ctx;
+    float scale; /* usually 1/sqrt(head_dim) */
+    presto_dtype dt;
+} presto_attn_desc;
+
+size_t presto_tree_attention_workspace(const presto_attn_desc *desc);
+presto_status presto_tree_attention(const presto_attn_desc *desc, const void *q,
+                                    const void *k_cache, const void *v_cache,
+                                    const int32_t *ctx_offsets, const void *k_tree,
+                                    const void *v_tree, const uint64_t *anc,
+                                    const int32_t *n_nodes, void *out, void *ws, size_t ws_bytes,
+                                    hipStream_t stream);
+
+/* ------------------------------------------------------------------------ */
+/* Stage 4: greedy verification of the tree (Eq. 1 at temperature 0) and the
+ * bonus token (Appendix C stage I: the position after the last accepted
+ * token takes the model's own prediction).
+ *
+ * target_logits [batch * n_max, row_stride], dtype dt: row (b, n) is the
+ *          target's next-token logits after node n; rows n >= n_nodes[b]
+ *          are not read.
+ * a[n] = lowest id attaining the row maximum.  From the root, repeatedly
+ * move to the child whose token equals a[current]; stop when none does.
+ * accept_len [batch] int32 out: accepted draft tokens, 0 .. depth
+ * path       [batch, depth + 1] int32 out: node rows root .. last accepted,
+ *            then -1
+ * bonus      [batch] int32 out: a[last accepted node]
+ * target_argmax [batch, n_max] int32 out, may be NULL: a[n], -1 for
+ *            padding rows
+ * flags      optional: PRESTO_FLAG_NAN_TARGET when a live row holds a NaN;
+ *            that row's argmax is then unspecified.
+ * parent, token, n_nodes as produced by presto_build_tree (sibling tokens
+ * distinct).  Limits: n_max <= 1024, depth >= 1.
+ */
+size_t presto_accept_workspace(int32_t batch, int32_t n_max, int32_t vocab);
+presto_status presto_accept(presto_dtype dt, const void *target_logits, int32_t vocab,
+                            int64_t row_stride, int32_t batch, int32_t n_max, int32_t depth,
+                            const int32_t *parent, const int32_t *token, const int32_t *n_nodes,
+                            int32_t *accept_len, int32_t *path, int32_t *bonus,
+                            int32_t *target_argmax, int32_t *flags, void *ws, size_t ws_bytes,
+                            hipStream_t stream);
+
+/* ------------------------------------------------------------------------ */
+const char *presto_status_string(presto_status s);
+const char *presto_last_error(void); /* thread-local text of the last failure ("" if none) */
+const char *presto_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* PRESTO_H */

@@ -1,0 +1,232 @@
+"""ctypes binding of libpresto (include/presto.h).
+
+Argument marshalling only: every step of a round runs in the HIP kernels of
+libpresto.so.  Tensors are PyTorch device tensors (memory and streams only);
+the binding checks their dtype/shape/contiguity, allocates outputs and the
+workspace with torch when the caller does not pass them, and enqueues the
+call on the current (or given) stream.  There is no fallback: a missing
+library raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libpresto.so")
+
+PRESTO_OK = 0
+PRESTO_ERR_INVALID_ARG = -1
+PRESTO_ERR_UNSUPPORTED = -2
+PRESTO_ERR_WORKSPACE = -3
+PRESTO_ERR_HIP = -4
+
+PRESTO_DT_BF16 = 0
+PRESTO_DT_F32 = 1
+
+PRESTO_TREE_BEST_FIRST = 0
+PRESTO_TREE_BEST_FIRST_ALG2 = 1
+PRESTO_TREE_BEAM = 2
+
+PRESTO_FLAG_NAN_DRAFTER = 1
+PRESTO_FLAG_NAN_TARGET = 2
+
+EXPORTS = (
+    "presto_topk_workspace", "presto_topk", "presto_build_tree_workspace", "presto_build_tree",
+    "presto_tree_attention_workspace", "presto_tree_attention", "presto_accept_workspace",
+    "presto_accept", "presto_status_string", "presto_last_error", "presto_version",
+)
+
+
+class PrestoError(RuntimeError):
+    def __init__(self, status: int, where: str, detail: str):
+        super().__init__(f"{where}: status {status}: {detail}")
+        self.status = status
+
+
+class TreeDesc(ctypes.Structure):
+    _fields_ = [("batch", ctypes.c_int32), ("depth", ctypes.c_int32), ("k", ctypes.c_int32),
+                ("branch", ctypes.c_int32), ("budget", ctypes.c_int32), ("mode", ctypes.c_int32)]
+
+
+class AttnDesc(ctypes.Structure):
+    _fields_ = [("batch", ctypes.c_int32), ("n_max", ctypes.c_int32), ("hq", ctypes.c_int32),
+                ("hkv", ctypes.c_int32), ("head_dim", ctypes.c_int32), ("max_ctx", ctypes.c_int32),
+                ("scale", ctypes.c_float), ("dt", ctypes.c_int32)]
+
+
+_VP, _I32, _I64, _SZ = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
+_LIB = None
+
+
+def lib() -> ctypes.CDLL:
+    """Load libpresto.so (raises if it has not been built)."""
+    global _LIB
+    if _LIB is None:
+        if not os.path.exists(LIB_PATH):
+            raise ImportError(f"{LIB_PATH} is missing: build it with paper_2607_22634_amd.build")
+        L = ctypes.CDLL(LIB_PATH)
+        L.presto_topk_workspace.argtypes = [_I64, _I32, _I32]
+        L.presto_topk_workspace.restype = _SZ
+        L.presto_topk.argtypes = [_I32, _VP, _I64, _I32, _I64, _I32, _VP, _VP, _VP, _VP, _VP, _SZ, _VP]
+        L.presto_topk.restype = _I32
+        L.presto_build_tree_workspace.argtypes = [ctypes.POINTER(TreeDesc)]
+        L.presto_build_tree_workspace.restype = _SZ
+        L.presto_build_tree.argtypes = [ctypes.POINTER(TreeDesc)] + [_VP] * 13 + [_SZ, _VP]
+        L.presto_build_tree.restype = _I32
+        L.presto_tree_attention_workspace.argtypes = [ctypes.POINTER(AttnDesc)]
+        L.presto_tree_attention_workspace.restype = _SZ
+        L.presto_tree_attention.argtypes = [ctypes.POINTER(AttnDesc)] + [_VP] * 10 + [_SZ, _VP]
+        L.presto_tree_attention.restype = _I32
+        L.presto_accept_workspace.argtypes = [_I32, _I32, _I32]
+        L.presto_accept_workspace.restype = _SZ
+        L.presto_accept.argtypes = [_I32, _VP, _I32, _I64, _I32, _I32, _I32] + [_VP] * 9 + [_SZ, _VP]
+        L.presto_accept.restype = _I32
+        L.presto_status_string.argtypes = [_I32]
+        L.presto_status_string.restype = ctypes.c_char_p
+        L.presto_last_error.restype = ctypes.c_char_p
+        L.presto_version.restype = ctypes.c_char_p
+        _LIB = L
+    return _LIB
+
+
+def _check(status: int, where: str) -> None:
+    if status != PRESTO_OK:
+        raise PrestoError(status, where, lib().presto_last_error().decode())
+
+
+def _ptr(t) -> int | None:
+    return None if t is None else t.data_ptr()
+
+
+def _stream(stream) -> int | None:
+    s = torch.cuda.current_stream() if stream is None else stream
+    return s.cuda_stream
+
+
+def _dt(t: torch.Tensor) -> int:
+    if t.dtype == torch.bfloat16:
+        return PRESTO_DT_BF16
+    if t.dtype == torch.float32:
+        return PRESTO_DT_F32
+    raise TypeError(f"unsupported dtype {t.dtype}")
+
+
+def _dev(*ts):
+    for t in ts:
+        if t is not None and (not t.is_cuda or not t.is_contiguous()):
+            raise ValueError("tensors must be contiguous device tensors")
+
+
+def _rows(t: torch.Tensor) -> None:
+    """Row-strided matrices: any row stride, contiguous innermost dimension."""
+    if not t.is_cuda or t.stride(-1) != 1 or (t.dim() == 3 and t.stride(0) != t.shape[1] * t.stride(1)):
+        raise ValueError("logits must be a device tensor with a contiguous innermost dimension")
+
+
+def _workspace(nbytes: int, device, ws):
+    if nbytes == 0:
+        return None, 0
+    if ws is not None:
+        return ws, ws.numel() * ws.element_size()
+    t = torch.empty(nbytes, dtype=torch.uint8, device=device)
+    return t, nbytes
+
+
+def version() -> str:
+    return lib().presto_version().decode()
+
+
+def presto_topk(logits: torch.Tensor, k: int, *, ids=None, logprob=None, lse=None, flags=None,
+                workspace=None, stream=None):
+    """Top-k ids, log q and LSE of every row of logits [rows, V] (bf16 or fp32)."""
+    _rows(logits)
+    rows, V = logits.shape
+    dev = logits.device
+    ids = torch.empty(rows, k, dtype=torch.int32, device=dev) if ids is None else ids
+    logprob = torch.empty(rows, k, dtype=torch.float32, device=dev) if logprob is None else logprob
+    lse = torch.empty(rows, dtype=torch.float32, device=dev) if lse is None else lse
+    _dev(ids, logprob, lse, flags)
+    need = lib().presto_topk_workspace(rows, V, k)
+    ws, nb = _workspace(need, dev, workspace)
+    _check(lib().presto_topk(_dt(logits), _ptr(logits), rows, V, logits.stride(0), k, _ptr(ids),
+                             _ptr(logprob), _ptr(lse), _ptr(flags), _ptr(ws), nb, _stream(stream)),
+           "presto_topk")
+    return ids, logprob, lse
+
+
+def presto_build_tree(ids: torch.Tensor, logprob: torch.Tensor, log_rho, lam: torch.Tensor,
+                      root_token: torch.Tensor, depth: int, k: int, budget: int,
+                      branch: int | None = None, mode: int = PRESTO_TREE_BEST_FIRST, *, out=None,
+                      workspace=None, stream=None) -> dict:
+    """Best-first draft tree per sequence: ids/logprob [b*D, k] or [b, D, k]."""
+    branch = k if branch is None else branch
+    b = root_token.shape[0]
+    N = budget + 1
+    W = (N + 63) // 64
+    dev = root_token.device
+    _dev(ids, logprob, log_rho, lam, root_token)
+    if out is None:
+        i32 = dict(dtype=torch.int32, device=dev)
+        out = {
+            "n_nodes": torch.empty(b, **i32), "parent": torch.empty(b, N, **i32),
+            "token": torch.empty(b, N, **i32), "depth": torch.empty(b, N, **i32),
+            "rank": torch.empty(b, N, **i32),
+            "score": torch.empty(b, N, dtype=torch.float32, device=dev),
+            "anc": torch.empty(b, N, W, dtype=torch.int64, device=dev),
+        }
+    desc = TreeDesc(b, depth, k, branch, budget, mode)
+    need = lib().presto_build_tree_workspace(ctypes.byref(desc))
+    ws, nb = _workspace(need, dev, workspace)
+    _check(lib().presto_build_tree(
+        ctypes.byref(desc), _ptr(ids), _ptr(logprob), _ptr(log_rho), _ptr(lam), _ptr(root_token),
+        _ptr(out["n_nodes"]), _ptr(out["parent"]), _ptr(out["token"]), _ptr(out["depth"]),
+        _ptr(out["rank"]), _ptr(out["score"]), _ptr(out["anc"]), _ptr(ws), nb, _stream(stream)),
+        "presto_build_tree")
+    return out
+
+
+def presto_tree_attention(q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.Tensor,
+                          ctx_offsets: torch.Tensor, k_tree: torch.Tensor, v_tree: torch.Tensor,
+                          anc: torch.Tensor, n_nodes: torch.Tensor, max_ctx: int,
+                          scale: float | None = None, *, out=None, workspace=None, stream=None):
+    """Tree-masked attention of q [b, N, Hq, d] over [cache ; ancestors]."""
+    b, N, hq, d = q.shape
+    hkv = k_tree.shape[2]
+    scale = d ** -0.5 if scale is None else scale
+    _dev(q, k_cache, v_cache, ctx_offsets, k_tree, v_tree, anc, n_nodes)
+    out = torch.empty_like(q) if out is None else out
+    _dev(out)
+    desc = AttnDesc(b, N, hq, hkv, d, int(max_ctx), float(scale), _dt(q))
+    need = lib().presto_tree_attention_workspace(ctypes.byref(desc))
+    ws, nb = _workspace(need, q.device, workspace)
+    _check(lib().presto_tree_attention(
+        ctypes.byref(desc), _ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(ctx_offsets), _ptr(k_tree),
+        _ptr(v_tree), _ptr(anc), _ptr(n_nodes), _ptr(out), _ptr(ws), nb, _stream(stream)),
+        "presto_tree_attention")
+    return out
+
+
+def presto_accept(target_logits: torch.Tensor, parent: torch.Tensor, token: torch.Tensor,
+                  n_nodes: torch.Tensor, depth: int, *, out=None, flags=None, workspace=None,
+                  stream=None) -> dict:
+    """Greedy acceptance: target_logits [b, N, V] (or [b*N, V]) against the tree."""
+    b, N = parent.shape
+    V = target_logits.shape[-1]
+    dev = parent.device
+    _rows(target_logits)
+    _dev(parent, token, n_nodes, flags)
+    if out is None:
+        i32 = dict(dtype=torch.int32, device=dev)
+        out = {"accept_len": torch.empty(b, **i32), "path": torch.empty(b, depth + 1, **i32),
+               "bonus": torch.empty(b, **i32), "target_argmax": torch.empty(b, N, **i32)}
+    need = lib().presto_accept_workspace(b, N, V)
+    ws, nb = _workspace(need, dev, workspace)
+    _check(lib().presto_accept(
+        _dt(target_logits), _ptr(target_logits), V, target_logits.stride(-2), b, N, depth,
+        _ptr(parent), _ptr(token), _ptr(n_nodes), _ptr(out["accept_len"]), _ptr(out["path"]),
+        _ptr(out["bonus"]), _ptr(out.get("target_argmax")), _ptr(flags), _ptr(ws), nb,
+        _stream(stream)), "presto_accept")
+    return out

@@ -1,0 +1,196 @@
+// Stage 4: greedy verification of the tree and the bonus token.
+//
+// Kernel 1 streams every live node's target logit row from HBM once and
+// leaves, per wave-sized chunk, the chunk maximum and the lowest id holding
+// it (packed into one orderable 64-bit key).  Rows of padding nodes are
+// skipped without being read.  Kernel 2 (one workgroup per sequence)
+// reduces the chunk keys to the target's greedy prediction a[n] of every
+// node, stages the tree in LDS and walks it from the root: move to the
+// child whose token equals a[current] until no child does.
+#include <math.h>
+
+#include "common.hpp"
+
+namespace presto {
+
+constexpr int kArgmaxWavesPerBlock = 4;
+constexpr int kWalkThreads = 256;
+constexpr int kMaxNodes = 1024;
+
+template <bool BF16, int NLOAD>
+__global__ __launch_bounds__(kArgmaxWavesPerBlock * kWave) void argmax_partial_kernel(
+    const void* __restrict__ logits, int32_t batch, int32_t n_max, int32_t vocab,
+    int64_t row_stride, const int32_t* __restrict__ n_nodes, int32_t chunks, bool aligned,
+    uint64_t* __restrict__ part, int32_t* __restrict__ flags) {
+    constexpr int P = BF16 ? 8 : 4;
+    constexpr int E = NLOAD * P;
+    constexpr int64_t CH = (int64_t)kWave * E;
+    const int wave = threadIdx.x / kWave, lane = lane_id();
+    const int64_t gw = (int64_t)blockIdx.x * kArgmaxWavesPerBlock + wave;
+    const int64_t rows = (int64_t)batch * n_max;
+    if (gw >= rows * chunks) return;
+    const int64_t row = gw / chunks;
+    const int32_t chunk = (int32_t)(gw % chunks);
+    const int b = (int)(row / n_max), n = (int)(row % n_max);
+    if (n >= min(max(n_nodes[b], 1), n_max)) return;  // padding node: never read, never used
+    const int64_t c0 = (int64_t)chunk * CH;
+    const char* rowp = static_cast<const char*>(logits) + row * row_stride * (BF16 ? 2 : 4);
+    const bool full = aligned && (c0 + CH <= vocab);
+
+    float v[E];
+    if (full) {
+        const uint4* src = reinterpret_cast<const uint4*>(rowp + c0 * (BF16 ? 2 : 4));
+        uint4 raw[NLOAD];
+#pragma unroll
+        for (int i = 0; i < NLOAD; ++i) raw[i] = load_stream16(&src[i * kWave + lane]);
+#pragma unroll
+        for (int i = 0; i < NLOAD; ++i) {
+            const uint32_t w[4] = {raw[i].x, raw[i].y, raw[i].z, raw[i].w};
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                if constexpr (BF16) {
+                    v[i * P + 2 * j] = bf16lo(w[j]);
+                    v[i * P + 2 * j + 1] = bf16hi(w[j]);
+                } else {
+                    v[i * P + j] = __uint_as_float(w[j]);
+                }
+            }
+        }
+    } else {
+#pragma unroll
+        for (int e = 0; e < E; ++e) {
+            const int64_t idx = c0 + (int64_t)((e / P) * kWave + lane) * P + (e % P);
+            float x = -INFINITY;
+            if (idx < vocab)
+                x = BF16 ? bf16_to_f(reinterpret_cast<const uint16_t*>(rowp)[idx])
+                         : reinterpret_cast<const float*>(rowp)[idx];
+            v[e] = x;
+        }
+    }
+    float lm = -INFINITY, sum = 0.f;
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+        lm = fmaxf(lm, v[e]);
+        sum += v[e];
+    }
+    const float M = wave_max(lm);
+    // lowest vocabulary id of the lane holding the chunk maximum
+    uint32_t best = 0xffffffffu;
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+        const int64_t idx = c0 + (int64_t)((e / P) * kWave + lane) * P + (e % P);
+        const bool hit = (v[e] == M) && (full || idx < vocab);
+        best = (hit && (uint32_t)idx < best) ? (uint32_t)idx : best;
+    }
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+        const uint32_t w = __shfl_xor(best, o, kWave);
+        best = w < best ? w : best;
+    }
+    const float tot = wave_sum(sum);
+    if (lane == 0) {
+        part[gw] = vocab_key(M, best);
+        if (!(tot == tot)) raise_flag(flags, PRESTO_FLAG_NAN_TARGET);
+    }
+}
+
+__global__ __launch_bounds__(kWalkThreads) void accept_walk_kernel(
+    int32_t n_max, int32_t depth, int32_t chunks, const uint64_t* __restrict__ part,
+    const int32_t* __restrict__ parent, const int32_t* __restrict__ token,
+    const int32_t* __restrict__ n_nodes, int32_t* __restrict__ accept_len,
+    int32_t* __restrict__ path, int32_t* __restrict__ bonus, int32_t* __restrict__ target_argmax) {
+    __shared__ int32_t s_a[kMaxNodes];
+    __shared__ int32_t s_par[kMaxNodes];
+    __shared__ int32_t s_tok[kMaxNodes];
+    const int b = blockIdx.x;
+    const int nn = min(max(n_nodes[b], 1), n_max);
+    for (int n = threadIdx.x; n < n_max; n += kWalkThreads) {
+        int32_t a = -1;
+        if (n < nn) {
+            const uint64_t* p = part + ((int64_t)b * n_max + n) * chunks;
+            uint64_t best = 0ull;
+            for (int c = 0; c < chunks; ++c) best = p[c] > best ? p[c] : best;
+            a = (int32_t)key_id(best);
+        }
+        s_a[n] = a;
+        s_par[n] = parent[(int64_t)b * n_max + n];
+        s_tok[n] = token[(int64_t)b * n_max + n];
+        if (target_argmax) target_argmax[(int64_t)b * n_max + n] = a;
+    }
+    __syncthreads();
+    if (threadIdx.x >= kWave) return;
+    const int lane = threadIdx.x;
+    int32_t* pth = path + (int64_t)b * (depth + 1);
+    int cur = 0, L = 0;
+    for (;;) {
+        const int32_t want = s_a[cur];
+        int next = -1;
+        for (int base = 1; base < nn && next < 0; base += kWave) {
+            const int c = base + lane;
+            const bool hit = c < nn && s_par[c] == cur && s_tok[c] == want;
+            const uint64_t m = __ballot(hit);
+            if (m) next = base + (int)__ffsll((unsigned long long)m) - 1;
+        }
+        if (next < 0 || L >= depth) break;
+        cur = next;
+        ++L;
+        if (lane == 0) pth[L] = cur;
+    }
+    for (int i = L + 1 + lane; i <= depth; i += kWave) pth[i] = -1;
+    if (lane == 0) {
+        pth[0] = 0;
+        accept_len[b] = L;
+        bonus[b] = s_a[cur];
+    }
+}
+
+}  // namespace presto
+
+namespace presto_host {
+
+using namespace presto;
+
+static int argmax_nload(int64_t rows, int32_t vocab, bool bf16) {
+    const int64_t ch8 = (int64_t)kWave * 8 * (bf16 ? 8 : 4);
+    return rows * ((vocab + ch8 - 1) / ch8) >= 4 * 256 * 4 ? 8 : 4;
+}
+
+size_t accept_workspace_bytes(int32_t batch, int32_t n_max, int32_t vocab) {
+    const int64_t chunks = (vocab + (int64_t)kWave * 16 - 1) / ((int64_t)kWave * 16);
+    return (size_t)batch * n_max * chunks * sizeof(uint64_t) + 256;
+}
+
+presto_status launch_accept(bool bf16, const void* logits, int32_t vocab, int64_t row_stride,
+                            int32_t batch, int32_t n_max, int32_t depth, const int32_t* parent,
+                            const int32_t* token, const int32_t* n_nodes, int32_t* accept_len,
+                            int32_t* path, int32_t* bonus, int32_t* target_argmax, int32_t* flags,
+                            void* ws, hipStream_t stream) {
+    const int64_t rows = (int64_t)batch * n_max;
+    const int nload = argmax_nload(rows, vocab, bf16);
+    const int64_t ch = (int64_t)kWave * nload * (bf16 ? 8 : 4);
+    const int64_t chunks = (vocab + ch - 1) / ch;
+    const size_t esz = bf16 ? 2 : 4;
+    const bool aligned = ((uintptr_t)logits % 16 == 0) && ((row_stride * (int64_t)esz) % 16 == 0);
+    uint64_t* part = static_cast<uint64_t*>(ws);
+    const int64_t waves = rows * chunks;
+    const dim3 block(kArgmaxWavesPerBlock * kWave);
+    const dim3 grid((unsigned)((waves + kArgmaxWavesPerBlock - 1) / kArgmaxWavesPerBlock));
+#define PRESTO_ARGMAX(BF, NL)                                                                  \
+    argmax_partial_kernel<BF, NL><<<grid, block, 0, stream>>>(logits, batch, n_max, vocab,      \
+                                                              row_stride, n_nodes,             \
+                                                              (int32_t)chunks, aligned, part, flags)
+    if (bf16) {
+        if (nload == 8) PRESTO_ARGMAX(true, 8); else PRESTO_ARGMAX(true, 4);
+    } else {
+        if (nload == 8) PRESTO_ARGMAX(false, 8); else PRESTO_ARGMAX(false, 4);
+    }
+#undef PRESTO_ARGMAX
+    presto_status st = check_launch("argmax_partial_kernel");
+    if (st != PRESTO_OK) return st;
+    accept_walk_kernel<<<batch, kWalkThreads, 0, stream>>>(n_max, depth, (int32_t)chunks, part,
+                                                           parent, token, n_nodes, accept_len,
+                                                           path, bonus, target_argmax);
+    return check_launch("accept_walk_kernel");
+}
+
+}  // namespace presto_host

@@ -1,0 +1,222 @@
+// Host side of libpresto: argument validation, workspace sizing, error
+// reporting and dispatch to the stage launchers.  Nothing here touches the
+// GPU before every check has passed.
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include "common.hpp"
+
+namespace presto_host {
+
+size_t topk_workspace_bytes(int64_t rows, int32_t vocab, int32_t k);
+presto_status launch_topk(bool bf16, const void* logits, int64_t rows, int32_t vocab,
+                          int64_t row_stride, int32_t k, int32_t* ids, float* logprob, float* lse,
+                          int32_t* flags, void* ws, hipStream_t stream);
+bool tree_build_fits(int D, int k, int branch, int N);
+presto_status launch_build_tree(const presto_tree_desc* desc, const int32_t* ids,
+                                const float* logprob, const float* log_rho, const float* lambda,
+                                const int32_t* root_token, int32_t* n_nodes, int32_t* parent,
+                                int32_t* token, int32_t* depth, int32_t* rank, float* score,
+                                uint64_t* anc, hipStream_t stream);
+size_t attn_workspace_bytes(const presto_attn_desc* d);
+presto_status launch_tree_attention(const presto_attn_desc* d, const void* q, const void* k_cache,
+                                    const void* v_cache, const int32_t* ctx_offsets,
+                                    const void* k_tree, const void* v_tree, const uint64_t* anc,
+                                    const int32_t* n_nodes, void* out, void* ws,
+                                    hipStream_t stream);
+size_t accept_workspace_bytes(int32_t batch, int32_t n_max, int32_t vocab);
+presto_status launch_accept(bool bf16, const void* logits, int32_t vocab, int64_t row_stride,
+                            int32_t batch, int32_t n_max, int32_t depth, const int32_t* parent,
+                            const int32_t* token, const int32_t* n_nodes, int32_t* accept_len,
+                            int32_t* path, int32_t* bonus, int32_t* target_argmax, int32_t* flags,
+                            void* ws, hipStream_t stream);
+
+static thread_local char g_err[512] = "";
+
+presto_status set_error(presto_status s, const char* fmt, ...) {
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(g_err, sizeof(g_err), fmt, ap);
+    va_end(ap);
+    return s;
+}
+
+presto_status check_launch(const char* what) {
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return set_error(PRESTO_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+    return PRESTO_OK;
+}
+
+}  // namespace presto_host
+
+using namespace presto_host;
+
+#define REQUIRE(cond, ...)                                        \
+    do {                                                          \
+        if (!(cond)) return set_error(PRESTO_ERR_INVALID_ARG, __VA_ARGS__); \
+    } while (0)
+
+static bool valid_dtype(presto_dtype dt) { return dt == PRESTO_DT_BF16 || dt == PRESTO_DT_F32; }
+
+static presto_status check_ws(void* ws, size_t have, size_t need) {
+    if (need > 0 && (ws == nullptr || have < need))
+        return set_error(PRESTO_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", need,
+                         ws ? have : (size_t)0);
+    return PRESTO_OK;
+}
+
+extern "C" {
+
+size_t presto_topk_workspace(int64_t rows, int32_t vocab, int32_t k) {
+    if (rows <= 0 || vocab <= 0 || k <= 0) return 0;
+    return topk_workspace_bytes(rows, vocab, k);
+}
+
+presto_status presto_topk(presto_dtype dt, const void* logits, int64_t rows, int32_t vocab,
+                          int64_t row_stride, int32_t k, int32_t* ids, float* logprob, float* lse,
+                          int32_t* flags, void* ws, size_t ws_bytes, hipStream_t stream) {
+    g_err[0] = 0;
+    REQUIRE(valid_dtype(dt), "presto_topk: unknown dtype %d", (int)dt);
+    REQUIRE(rows >= 0, "presto_topk: rows < 0");
+    REQUIRE(vocab >= 1, "presto_topk: vocab < 1");
+    REQUIRE(k >= 1 && k <= vocab, "presto_topk: k=%d outside 1..vocab", k);
+    REQUIRE(row_stride >= vocab, "presto_topk: row_stride < vocab");
+    if (k > 16) return set_error(PRESTO_ERR_UNSUPPORTED, "presto_topk: k=%d > 16", k);
+    if (rows == 0) return PRESTO_OK;
+    REQUIRE(logits && ids && logprob, "presto_topk: null pointer");
+    REQUIRE(rows * (int64_t)((vocab + 1023) / 1024) < (int64_t)1 << 31,
+            "presto_topk: too many rows");
+    presto_status st = check_ws(ws, ws_bytes, presto_topk_workspace(rows, vocab, k));
+    if (st != PRESTO_OK) return st;
+    return launch_topk(dt == PRESTO_DT_BF16, logits, rows, vocab, row_stride, k, ids, logprob, lse,
+                       flags, ws, stream);
+}
+
+size_t presto_build_tree_workspace(const presto_tree_desc* desc) {
+    (void)desc;
+    return 0;
+}
+
+presto_status presto_build_tree(const presto_tree_desc* desc, const int32_t* ids,
+                                const float* logprob, const float* log_rho, const float* lambda,
+                                const int32_t* root_token, int32_t* n_nodes, int32_t* parent,
+                                int32_t* token, int32_t* depth_out, int32_t* rank, float* score,
+                                uint64_t* anc, void* ws, size_t ws_bytes, hipStream_t stream) {
+    g_err[0] = 0;
+    (void)ws;
+    (void)ws_bytes;
+    REQUIRE(desc, "presto_build_tree: null descriptor");
+    const presto_tree_desc d = *desc;
+    REQUIRE(d.batch >= 0, "presto_build_tree: batch < 0");
+    REQUIRE(d.depth >= 1 && d.depth <= 32, "presto_build_tree: depth=%d outside 1..32", d.depth);
+    REQUIRE(d.k >= 1 && d.k <= 16, "presto_build_tree: k=%d outside 1..16", d.k);
+    REQUIRE(d.branch >= 1 && d.branch <= d.k, "presto_build_tree: branch=%d outside 1..k",
+            d.branch);
+    REQUIRE(d.budget >= 1 && d.budget <= 511, "presto_build_tree: budget=%d outside 1..511",
+            d.budget);
+    int wbits = 1;
+    while ((1 << wbits) < d.k + 1) ++wbits;
+    REQUIRE(d.depth * wbits <= 128, "presto_build_tree: depth*ceil(log2(k+1)) > 128");
+    if (d.mode == PRESTO_TREE_BEST_FIRST_ALG2 || d.mode == PRESTO_TREE_BEAM)
+        return set_error(PRESTO_ERR_UNSUPPORTED, "presto_build_tree: mode %d not built", d.mode);
+    REQUIRE(d.mode == PRESTO_TREE_BEST_FIRST, "presto_build_tree: unknown mode %d", d.mode);
+    if (!tree_build_fits(d.depth, d.k, d.branch, d.budget + 1))
+        return set_error(PRESTO_ERR_UNSUPPORTED, "presto_build_tree: tables exceed 64 KiB of LDS");
+    if (d.batch == 0) return PRESTO_OK;
+    REQUIRE(ids && logprob && lambda && root_token && n_nodes && parent && token && depth_out &&
+                rank && score && anc,
+            "presto_build_tree: null pointer");
+    return launch_build_tree(&d, ids, logprob, log_rho, lambda, root_token, n_nodes, parent, token,
+                             depth_out, rank, score, anc, stream);
+}
+
+size_t presto_tree_attention_workspace(const presto_attn_desc* desc) {
+    if (!desc || desc->batch <= 0 || desc->n_max <= 0 || desc->hkv <= 0 || desc->hq <= 0 ||
+        desc->hq % desc->hkv != 0 || desc->max_ctx < 0)
+        return 0;
+    return attn_workspace_bytes(desc);
+}
+
+presto_status presto_tree_attention(const presto_attn_desc* desc, const void* q,
+                                    const void* k_cache, const void* v_cache,
+                                    const int32_t* ctx_offsets, const void* k_tree,
+                                    const void* v_tree, const uint64_t* anc,
+                                    const int32_t* n_nodes, void* out, void* ws, size_t ws_bytes,
+                                    hipStream_t stream) {
+    g_err[0] = 0;
+    REQUIRE(desc, "presto_tree_attention: null descriptor");
+    const presto_attn_desc d = *desc;
+    REQUIRE(valid_dtype(d.dt), "presto_tree_attention: unknown dtype %d", (int)d.dt);
+    REQUIRE(d.batch >= 0, "presto_tree_attention: batch < 0");
+    REQUIRE(d.n_max >= 1 && d.n_max <= 1024, "presto_tree_attention: n_max outside 1..1024");
+    REQUIRE(d.hq >= 1 && d.hkv >= 1 && d.hq % d.hkv == 0,
+            "presto_tree_attention: hq must be a positive multiple of hkv");
+    REQUIRE(d.head_dim == 64 || d.head_dim == 128, "presto_tree_attention: head_dim %d",
+            d.head_dim);
+    REQUIRE(d.max_ctx >= 0, "presto_tree_attention: max_ctx < 0");
+    REQUIRE(isfinite(d.scale), "presto_tree_attention: scale not finite");
+    REQUIRE((int64_t)d.max_ctx + d.n_max < ((int64_t)1 << 30), "presto_tree_attention: too long");
+    if (d.batch == 0) return PRESTO_OK;
+    REQUIRE(q && k_tree && v_tree && ctx_offsets && anc && n_nodes && out,
+            "presto_tree_attention: null pointer");
+    REQUIRE(d.max_ctx == 0 || (k_cache && v_cache), "presto_tree_attention: null cache");
+    if (d.dt == PRESTO_DT_BF16) {
+        const uintptr_t al = (uintptr_t)q | (uintptr_t)k_tree | (uintptr_t)v_tree |
+                             (uintptr_t)out | (uintptr_t)(k_cache ? k_cache : q) |
+                             (uintptr_t)(v_cache ? v_cache : q);
+        REQUIRE(al % 16 == 0, "presto_tree_attention: bf16 tensors must be 16-byte aligned");
+    }
+    presto_status st = check_ws(ws, ws_bytes, presto_tree_attention_workspace(&d));
+    if (st != PRESTO_OK) return st;
+    return launch_tree_attention(&d, q, k_cache, v_cache, ctx_offsets, k_tree, v_tree, anc, n_nodes,
+                                 out, ws, stream);
+}
+
+size_t presto_accept_workspace(int32_t batch, int32_t n_max, int32_t vocab) {
+    if (batch <= 0 || n_max <= 0 || vocab <= 0) return 0;
+    return accept_workspace_bytes(batch, n_max, vocab);
+}
+
+presto_status presto_accept(presto_dtype dt, const void* target_logits, int32_t vocab,
+                            int64_t row_stride, int32_t batch, int32_t n_max, int32_t depth,
+                            const int32_t* parent, const int32_t* token, const int32_t* n_nodes,
+                            int32_t* accept_len, int32_t* path, int32_t* bonus,
+                            int32_t* target_argmax, int32_t* flags, void* ws, size_t ws_bytes,
+                            hipStream_t stream) {
+    g_err[0] = 0;
+    REQUIRE(valid_dtype(dt), "presto_accept: unknown dtype %d", (int)dt);
+    REQUIRE(vocab >= 1, "presto_accept: vocab < 1");
+    REQUIRE(row_stride >= vocab, "presto_accept: row_stride < vocab");
+    REQUIRE(batch >= 0, "presto_accept: batch < 0");
+    REQUIRE(n_max >= 1 && n_max <= 1024, "presto_accept: n_max outside 1..1024");
+    REQUIRE(depth >= 1, "presto_accept: depth < 1");
+    if (batch == 0) return PRESTO_OK;
+    REQUIRE(target_logits && parent && token && n_nodes && accept_len && path && bonus,
+            "presto_accept: null pointer");
+    REQUIRE((int64_t)batch * n_max * ((vocab + 1023) / 1024) < ((int64_t)1 << 31),
+            "presto_accept: too many rows");
+    presto_status st = check_ws(ws, ws_bytes, presto_accept_workspace(batch, n_max, vocab));
+    if (st != PRESTO_OK) return st;
+    return launch_accept(dt == PRESTO_DT_BF16, target_logits, vocab, row_stride, batch, n_max, depth,
+                         parent, token, n_nodes, accept_len, path, bonus, target_argmax, flags, ws,
+                         stream);
+}
+
+const char* presto_status_string(presto_status s) {
+    switch (s) {
+        case PRESTO_OK: return "ok";
+        case PRESTO_ERR_INVALID_ARG: return "invalid argument";
+        case PRESTO_ERR_UNSUPPORTED: return "unsupported";
+        case PRESTO_ERR_WORKSPACE: return "workspace too small";
+        case PRESTO_ERR_HIP: return "HIP error";
+    }
+    return "unknown status";
+}
+
+const char* presto_last_error(void) { return g_err; }
+
+const char* presto_version(void) { return "presto-mi355x 0.1 (gfx950)"; }
+
+}  // extern "C"

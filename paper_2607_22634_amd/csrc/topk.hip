@@ -1,0 +1,279 @@
+// Stage 1: log-softmax normaliser and top-k candidates per drafter position.
+//
+// The vocabulary row of each position is streamed from HBM once.  A row is
+// cut into wave-sized chunks; every wave holds its chunk in registers and
+// produces, with no LDS barrier and no block-level synchronisation:
+//   * the chunk maximum m and sum exp(z - m)           (for the row's LSE)
+//   * the chunk's k best (value desc, id asc) entries  (as 64-bit keys)
+// The k-th largest lane maximum is a lower bound on the chunk's k-th value,
+// so only entries at or above it are candidates (normally k to 2k of them);
+// they are compacted through a small per-wave LDS list and ranked there.
+// A chunk with more than kCandCap candidates (massive ties) falls back to
+// k rounds of exact wave-wide selection.  A second kernel merges the chunk
+// partials of each row (one wave per row).
+#include <math.h>
+
+#include "common.hpp"
+
+namespace presto {
+
+constexpr int kCandCap = 64;
+constexpr int kTopkWavesPerBlock = 4;
+
+template <bool BF16>
+struct VecTraits;
+template <>
+struct VecTraits<true> {
+    static constexpr int kPerVec = 8;
+};
+template <>
+struct VecTraits<false> {
+    static constexpr int kPerVec = 4;
+};
+
+// Element e of a lane's register block: load i = e / kPerVec, j = e % kPerVec;
+// vocabulary index c0 + (i * 64 + lane) * kPerVec + j.
+template <bool BF16, int NLOAD>
+__device__ __forceinline__ void load_chunk(const void* __restrict__ row, int64_t c0, int32_t vocab,
+                                           bool vec_ok, float (&v)[NLOAD * VecTraits<BF16>::kPerVec]) {
+    constexpr int P = VecTraits<BF16>::kPerVec;
+    const int lane = lane_id();
+    if (vec_ok) {
+        const uint4* src = reinterpret_cast<const uint4*>(
+            static_cast<const char*>(row) + c0 * (BF16 ? 2 : 4));
+        uint4 raw[NLOAD];
+#pragma unroll
+        for (int i = 0; i < NLOAD; ++i) raw[i] = load_stream16(&src[i * kWave + lane]);
+#pragma unroll
+        for (int i = 0; i < NLOAD; ++i) {
+            const uint32_t w[4] = {raw[i].x, raw[i].y, raw[i].z, raw[i].w};
+            if constexpr (BF16) {
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    v[i * P + 2 * j] = bf16lo(w[j]);
+                    v[i * P + 2 * j + 1] = bf16hi(w[j]);
+                }
+            } else {
+#pragma unroll
+                for (int j = 0; j < 4; ++j) v[i * P + j] = __uint_as_float(w[j]);
+            }
+        }
+    } else {
+#pragma unroll
+        for (int i = 0; i < NLOAD; ++i) {
+#pragma unroll
+            for (int j = 0; j < P; ++j) {
+                const int64_t idx = c0 + (int64_t)(i * kWave + lane) * P + j;
+                float x = -INFINITY;
+                if (idx < vocab) {
+                    if constexpr (BF16)
+                        x = bf16_to_f(static_cast<const uint16_t*>(row)[idx]);
+                    else
+                        x = static_cast<const float*>(row)[idx];
+                }
+                v[i * P + j] = x;
+            }
+        }
+    }
+}
+
+// Descending bitonic sort of one float per lane across the wave.
+__device__ __forceinline__ float wave_sort_desc(float x) {
+    const int lane = lane_id();
+#pragma unroll
+    for (int size = 2; size <= kWave; size <<= 1) {
+#pragma unroll
+        for (int stride = size >> 1; stride > 0; stride >>= 1) {
+            const float y = __shfl_xor(x, stride, kWave);
+            const bool keep_max = ((lane & size) == 0) == ((lane & stride) == 0);
+            x = keep_max ? fmaxf(x, y) : fminf(x, y);
+        }
+    }
+    return x;
+}
+
+template <bool BF16, int NLOAD>
+__global__ __launch_bounds__(kTopkWavesPerBlock * kWave) void topk_partial_kernel(
+    const void* __restrict__ logits, int64_t rows, int32_t vocab, int64_t row_stride, int32_t k,
+    int32_t chunks, bool aligned, float2* __restrict__ part_ms, uint64_t* __restrict__ part_keys,
+    int32_t* __restrict__ flags) {
+    constexpr int P = VecTraits<BF16>::kPerVec;
+    constexpr int E = NLOAD * P;
+    constexpr int64_t CH = (int64_t)kWave * E;
+    __shared__ uint64_t cand[kTopkWavesPerBlock][kCandCap];
+    __shared__ uint32_t cand_n[kTopkWavesPerBlock];
+
+    const int wave = threadIdx.x / kWave, lane = lane_id();
+    const int64_t gw = (int64_t)blockIdx.x * kTopkWavesPerBlock + wave;
+    if (gw >= rows * chunks) return;
+    const int64_t row = gw / chunks;
+    const int32_t chunk = (int32_t)(gw % chunks);
+    const int64_t c0 = (int64_t)chunk * CH;
+    const char* rowp = static_cast<const char*>(logits) + row * row_stride * (BF16 ? 2 : 4);
+    const bool full = aligned && (c0 + CH <= vocab);
+
+    float v[E];
+    load_chunk<BF16, NLOAD>(rowp, c0, vocab, full, v);
+
+    // lane and wave maxima
+    float lm = -INFINITY;
+#pragma unroll
+    for (int e = 0; e < E; ++e) lm = fmaxf(lm, v[e]);
+    const float M = wave_max(lm);
+
+    // sum exp(z - M) over the chunk
+    float s = 0.f;
+    if (M != -INFINITY) {
+#pragma unroll
+        for (int e = 0; e < E; ++e) s += __expf(v[e] - M);
+    }
+    const float S = wave_sum(s);
+
+    // threshold: k-th largest lane maximum
+    const float sorted = wave_sort_desc(lm);
+    const float thr = __shfl(sorted, k - 1, kWave);
+
+    if (lane == 0) cand_n[wave] = 0u;
+    __builtin_amdgcn_wave_barrier();
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+        const int64_t idx = c0 + (int64_t)((e / P) * kWave + lane) * P + (e % P);
+        if (v[e] >= thr && (full || idx < vocab)) {
+            const uint32_t pos = atomicAdd(&cand_n[wave], 1u);
+            if (pos < kCandCap) cand[wave][pos] = vocab_key(v[e], (uint32_t)idx);
+        }
+    }
+    __builtin_amdgcn_wave_barrier();
+    const uint32_t total = __builtin_amdgcn_readfirstlane(cand_n[wave]);
+    uint64_t* out = part_keys + gw * k;
+
+    if (total <= (uint32_t)kCandCap) {
+        const uint64_t mine = lane < (int)total ? cand[wave][lane] : 0ull;
+        int rank = 0;
+        for (uint32_t j = 0; j < total; ++j) rank += cand[wave][j] > mine ? 1 : 0;
+        if (lane < (int)total && rank < k) out[rank] = mine;
+        if (lane >= (int)total && lane < k) out[lane] = 0ull;
+    } else {
+        // exact selection: k rounds of "largest key below the last one"
+        uint64_t last = ~0ull;
+        for (int j = 0; j < k; ++j) {
+            uint64_t best = 0ull;
+#pragma unroll
+            for (int e = 0; e < E; ++e) {
+                const int64_t idx = c0 + (int64_t)((e / P) * kWave + lane) * P + (e % P);
+                if (full || idx < vocab) {
+                    const uint64_t key = vocab_key(v[e], (uint32_t)idx);
+                    if (key < last && key > best) best = key;
+                }
+            }
+            last = wave_max_u64(best);
+            if (lane == 0) out[j] = last;
+        }
+    }
+    if (lane == 0) {
+        part_ms[gw] = make_float2(M, S);
+        if (!(S == S)) raise_flag(flags, PRESTO_FLAG_NAN_DRAFTER);
+    }
+}
+
+__global__ __launch_bounds__(kTopkWavesPerBlock * kWave) void topk_merge_kernel(
+    int64_t rows, int32_t chunks, int32_t k, const float2* __restrict__ part_ms,
+    const uint64_t* __restrict__ part_keys, int32_t* __restrict__ ids, float* __restrict__ logprob,
+    float* __restrict__ lse) {
+    const int wave = threadIdx.x / kWave, lane = lane_id();
+    const int64_t row = (int64_t)blockIdx.x * kTopkWavesPerBlock + wave;
+    if (row >= rows) return;
+    const float2* ms = part_ms + row * chunks;
+
+    float m = -INFINITY;
+    for (int c = lane; c < chunks; c += kWave) m = fmaxf(m, ms[c].x);
+    const float M = wave_max(m);
+    float s = 0.f;
+    if (M != -INFINITY)
+        for (int c = lane; c < chunks; c += kWave) {
+            const float2 p = ms[c];
+            s += p.x == -INFINITY ? 0.f : p.y * __expf(p.x - M);
+        }
+    const float S = wave_sum(s);
+    const float L = (M == -INFINITY) ? -INFINITY : M + __logf(S);
+
+    const uint64_t* keys = part_keys + row * chunks * k;
+    const int nk = chunks * k;
+    uint64_t last = ~0ull, mine = 0ull;
+    for (int j = 0; j < k; ++j) {
+        uint64_t best = 0ull;
+        for (int i = lane; i < nk; i += kWave) {
+            const uint64_t key = keys[i];
+            if (key < last && key > best) best = key;
+        }
+        last = wave_max_u64(best);
+        if (lane == j) mine = last;
+    }
+    if (lane < k) {
+        ids[row * k + lane] = (int32_t)key_id(mine);
+        logprob[row * k + lane] = (L == -INFINITY) ? -INFINITY : key_value(mine) - L;
+    }
+    if (lse && lane == 0) lse[row] = L;
+}
+
+}  // namespace presto
+
+namespace presto_host {
+
+using namespace presto;
+
+static int topk_nload(bool bf16, int64_t rows, int32_t vocab) {
+    const int64_t ch8 = (int64_t)kWave * 8 * (bf16 ? 8 : 4);
+    const int64_t waves8 = rows * ((vocab + ch8 - 1) / ch8);
+    return waves8 >= 4 * 256 * 4 ? 8 : 4;
+}
+
+static int64_t topk_chunks(bool bf16, int64_t rows, int32_t vocab) {
+    const int64_t ch = (int64_t)kWave * topk_nload(bf16, rows, vocab) * (bf16 ? 8 : 4);
+    return (vocab + ch - 1) / ch;
+}
+
+size_t topk_workspace_bytes(int64_t rows, int32_t vocab, int32_t k) {
+    // sized for the finest chunking any dtype may pick
+    const int64_t chunks = (vocab + (int64_t)kWave * 16 - 1) / ((int64_t)kWave * 16);
+    const size_t per = (size_t)chunks * (sizeof(float2) + sizeof(uint64_t) * (size_t)k);
+    return (size_t)rows * per + 256;
+}
+
+presto_status launch_topk(bool bf16, const void* logits, int64_t rows, int32_t vocab,
+                          int64_t row_stride, int32_t k, int32_t* ids, float* logprob, float* lse,
+                          int32_t* flags, void* ws, hipStream_t stream) {
+    const int nload = topk_nload(bf16, rows, vocab);
+    const int64_t chunks = topk_chunks(bf16, rows, vocab);
+    const size_t esz = bf16 ? 2 : 4;
+    const bool aligned = ((uintptr_t)logits % 16 == 0) && ((row_stride * (int64_t)esz) % 16 == 0);
+    float2* ms = static_cast<float2*>(ws);
+    uint64_t* keys = reinterpret_cast<uint64_t*>(
+        (reinterpret_cast<uintptr_t>(ms + rows * chunks) + 15) & ~uintptr_t(15));
+    const int64_t waves = rows * chunks;
+    const dim3 block(kTopkWavesPerBlock * kWave);
+    const dim3 grid((unsigned)((waves + kTopkWavesPerBlock - 1) / kTopkWavesPerBlock));
+    if (bf16) {
+        if (nload == 8)
+            topk_partial_kernel<true, 8><<<grid, block, 0, stream>>>(
+                logits, rows, vocab, row_stride, k, (int32_t)chunks, aligned, ms, keys, flags);
+        else
+            topk_partial_kernel<true, 4><<<grid, block, 0, stream>>>(
+                logits, rows, vocab, row_stride, k, (int32_t)chunks, aligned, ms, keys, flags);
+    } else {
+        if (nload == 8)
+            topk_partial_kernel<false, 8><<<grid, block, 0, stream>>>(
+                logits, rows, vocab, row_stride, k, (int32_t)chunks, aligned, ms, keys, flags);
+        else
+            topk_partial_kernel<false, 4><<<grid, block, 0, stream>>>(
+                logits, rows, vocab, row_stride, k, (int32_t)chunks, aligned, ms, keys, flags);
+    }
+    presto_status st = check_launch("topk_partial_kernel");
+    if (st != PRESTO_OK) return st;
+    const dim3 mgrid((unsigned)((rows + kTopkWavesPerBlock - 1) / kTopkWavesPerBlock));
+    topk_merge_kernel<<<mgrid, block, 0, stream>>>(rows, (int32_t)chunks, k, ms, keys, ids,
+                                                    logprob, lse);
+    return check_launch("topk_merge_kernel");
+}
+
+}  // namespace presto_host

@@ -1,0 +1,113 @@
+"""Host-only checks of the C ABI (no GPU): the library loads, exports every
+entry point declared in include/presto.h, sizes workspaces, and rejects bad
+arguments before launching anything."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2607_22634_amd as P
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared():
+    text = open(os.path.join(ROOT, "include", "presto.h")).read()
+    return sorted(set(re.findall(r"\b(presto_[a-z_]+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_symbol():
+    lib = P.lib()
+    names = _declared()
+    assert set(names) == set(P.EXPORTS)
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def test_status_strings_and_version():
+    lib = P.lib()
+    assert lib.presto_status_string(0) == b"ok"
+    assert lib.presto_status_string(-3) == b"workspace too small"
+    assert b"gfx950" in lib.presto_version()
+
+
+def test_workspace_sizes_are_deterministic_and_monotone():
+    lib = P.lib()
+    a = lib.presto_topk_workspace(16, 151936, 4)
+    assert a > 0 and a == lib.presto_topk_workspace(16, 151936, 4)
+    assert lib.presto_topk_workspace(32, 151936, 4) > a
+    assert lib.presto_topk_workspace(0, 151936, 4) == 0
+    assert lib.presto_accept_workspace(1, 65, 151936) > 0
+    d = P.AttnDesc(4, 257, 32, 8, 128, 32768, 0.088, P.PRESTO_DT_BF16)
+    assert lib.presto_tree_attention_workspace(ctypes.byref(d)) > 0
+    d1 = P.AttnDesc(32, 129, 32, 8, 128, 2048, 0.088, P.PRESTO_DT_BF16)
+    assert lib.presto_tree_attention_workspace(ctypes.byref(d1)) == 0  # fills the chip unsplit
+
+
+def _err(status):
+    return status, P.lib().presto_last_error().decode()
+
+
+def test_topk_rejects_bad_arguments():
+    lib = P.lib()
+    st, msg = _err(lib.presto_topk(0, None, 4, 1024, 1024, 0, None, None, None, None, None, 0, None))
+    assert st == P.PRESTO_ERR_INVALID_ARG and "k=0" in msg
+    st, _ = _err(lib.presto_topk(0, None, 4, 1024, 1000, 2, None, None, None, None, None, 0, None))
+    assert st == P.PRESTO_ERR_INVALID_ARG
+    st, _ = _err(lib.presto_topk(7, None, 4, 1024, 1024, 2, None, None, None, None, None, 0, None))
+    assert st == P.PRESTO_ERR_INVALID_ARG
+    st, _ = _err(lib.presto_topk(0, None, 4, 1024, 1024, 17, None, None, None, None, None, 0, None))
+    assert st == P.PRESTO_ERR_UNSUPPORTED
+    st, _ = _err(lib.presto_topk(0, None, 4, 1024, 1024, 2, None, None, None, None, None, 0, None))
+    assert st == P.PRESTO_ERR_INVALID_ARG  # null pointers
+    # zero rows is a no-op, even without pointers
+    assert lib.presto_topk(0, None, 0, 1024, 1024, 2, None, None, None, None, None, 0, None) == 0
+
+
+def test_topk_rejects_small_workspace():
+    lib = P.lib()
+    fake = ctypes.c_void_p(0x1000)  # never dereferenced: the check fails first
+    st, msg = _err(lib.presto_topk(0, fake, 4, 1024, 1024, 2, fake, fake, None, None, fake, 8, None))
+    assert st == P.PRESTO_ERR_WORKSPACE and "workspace" in msg
+
+
+@pytest.mark.parametrize("field,value", [("depth", 0), ("depth", 33), ("k", 0), ("k", 17),
+                                         ("branch", 5), ("budget", 0), ("budget", 512),
+                                         ("mode", 9)])
+def test_build_tree_rejects_bad_descriptor(field, value):
+    d = P.TreeDesc(1, 4, 4, 4, 8, 0)
+    setattr(d, field, value)
+    st, _ = _err(P.lib().presto_build_tree(ctypes.byref(d), *([None] * 13), 0, None))
+    assert st == P.PRESTO_ERR_INVALID_ARG
+
+
+def test_build_tree_unbuilt_modes_are_unsupported():
+    d = P.TreeDesc(1, 4, 4, 4, 8, P.PRESTO_TREE_BEAM)
+    st, _ = _err(P.lib().presto_build_tree(ctypes.byref(d), *([None] * 13), 0, None))
+    assert st == P.PRESTO_ERR_UNSUPPORTED
+
+
+def test_build_tree_path_key_limit():
+    d = P.TreeDesc(1, 32, 16, 16, 8, 0)  # 32 * 5 bits > 128
+    st, msg = _err(P.lib().presto_build_tree(ctypes.byref(d), *([None] * 13), 0, None))
+    assert st == P.PRESTO_ERR_INVALID_ARG and "128" in msg
+
+
+@pytest.mark.parametrize("field,value", [("head_dim", 96), ("hkv", 3), ("n_max", 0),
+                                         ("n_max", 1025), ("max_ctx", -1), ("dt", 5)])
+def test_attention_rejects_bad_descriptor(field, value):
+    d = P.AttnDesc(1, 9, 2, 1, 64, 128, 0.125, P.PRESTO_DT_F32)
+    setattr(d, field, value)
+    st, _ = _err(P.lib().presto_tree_attention(ctypes.byref(d), *([None] * 10), 0, None))
+    assert st == P.PRESTO_ERR_INVALID_ARG
+
+
+def test_accept_rejects_bad_arguments():
+    lib = P.lib()
+    args = [None] * 9
+    assert lib.presto_accept(0, None, 1024, 1000, 1, 9, 4, *args, 0, None) == P.PRESTO_ERR_INVALID_ARG
+    assert lib.presto_accept(0, None, 1024, 1024, 1, 0, 4, *args, 0, None) == P.PRESTO_ERR_INVALID_ARG
+    assert lib.presto_accept(0, None, 1024, 1024, 1, 9, 0, *args, 0, None) == P.PRESTO_ERR_INVALID_ARG
+    assert lib.presto_accept(0, None, 1024, 1024, 1, 9, 4, *args, 0, None) == P.PRESTO_ERR_INVALID_ARG
+    assert lib.presto_accept(0, None, 1024, 1024, 0, 9, 4, *args, 0, None) == P.PRESTO_OK

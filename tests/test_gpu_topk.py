@@ -1,0 +1,96 @@
+"""GPU parity of presto_topk against the oracle (ids bit-exact, log q within
+1e-5 * max(1, |ref|)), at the five workloads' full sizes and on edge cases."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2607_22634_amd as P
+import synthetic as sy
+from gpu_util import round_data, to_dev, to_host
+
+pytestmark = pytest.mark.gpu
+
+
+def _compare(logits_store, dtype, k, ids, lp, lse):
+    rid, rlp, rlse, _ = oracle.topk(logits_store, k, dtype)
+    np.testing.assert_array_equal(to_host(ids), rid)
+    lp = to_host(lp)
+    fin = np.isfinite(rlp)
+    assert (np.isneginf(lp) == np.isneginf(rlp)).all()
+    err = np.abs(lp[fin] - rlp[fin]) / np.maximum(1.0, np.abs(rlp[fin]))
+    assert err.max(initial=0) <= 1e-5, err.max()
+    lse = to_host(lse)
+    fl = np.isfinite(rlse)
+    np.testing.assert_allclose(lse[fl], rlse[fl], rtol=1e-6, atol=1e-6)
+
+
+@pytest.mark.parametrize("cfg", [1, 2, 3, 4, 5])
+def test_topk_matches_oracle_on_workload(cfg):
+    w, rin = round_data(cfg)
+    logits = rin["drafter_logits"]
+    print(f"topk cfg={cfg} rows={logits.shape[0]} k={w.k}", flush=True)
+    flags = torch.zeros(1, dtype=torch.int32, device="cuda")
+    ids, lp, lse = P.presto_topk(to_dev(logits, w.dtype), w.k, flags=flags)
+    torch.cuda.synchronize()
+    assert int(flags.item()) == 0
+    _compare(logits, w.dtype, w.k, ids, lp, lse)
+
+
+EDGE = [
+    ("f32", 1000, 1), ("bf16", 1000, 3), ("bf16", 4099, 16), ("f32", 37, 16),
+    ("bf16", 151936, 8), ("f32", 151936, 2), ("bf16", 16, 16), ("bf16", 2048, 5),
+]
+
+
+@pytest.mark.parametrize("dtype,V,k", EDGE)
+def test_topk_edge_rows(dtype, V, k):
+    rng = np.random.default_rng([V, k, 11])
+    rows = 9
+    x = (rng.standard_normal((rows, V)) * 4).astype(np.float32)
+    x[1, :] = 1.5                                   # one giant tie: exact fallback path
+    x[2, :] = np.round(x[2])                        # heavy ties
+    x[3, ::2] = -np.inf                             # masked vocabulary
+    x[4, :] = -np.inf                               # fully masked row
+    x[5, : min(V, 40)] = 0.0
+    x[5, 1:min(V, 40):2] = -0.0                     # signed zeros tie
+    x[6, rng.choice(V, min(V, 3), replace=False)] = x[6].max() + 8
+    x[7, -1] = x[7].max() + 1                       # best entry in the ragged tail
+    x[8, :] = -1e30
+    store = sy.cast(x, dtype)
+    ids, lp, lse = P.presto_topk(to_dev(store, dtype), k)
+    torch.cuda.synchronize()
+    _compare(store, dtype, k, ids, lp, lse)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_topk_unaligned_row_stride(dtype):
+    rng = np.random.default_rng(5)
+    V, stride, rows, k = 3001, 3005, 6, 4
+    big = (rng.standard_normal((rows, stride)) * 4).astype(np.float32)
+    store = sy.cast(big, dtype)
+    t = to_dev(store, dtype)[:, :V]
+    ids, lp, lse = P.presto_topk(t, k)
+    torch.cuda.synchronize()
+    _compare(np.ascontiguousarray(store[:, :V]), dtype, k, ids, lp, lse)
+
+
+def test_topk_nan_sets_flag_only_for_nan():
+    x = np.random.default_rng(1).standard_normal((4, 5000)).astype(np.float32)
+    flags = torch.zeros(1, dtype=torch.int32, device="cuda")
+    P.presto_topk(to_dev(x), 4, flags=flags)
+    torch.cuda.synchronize()
+    assert int(flags.item()) == 0
+    x[2, 77] = np.nan
+    P.presto_topk(to_dev(x), 4, flags=flags)
+    torch.cuda.synchronize()
+    assert int(flags.item()) & P.PRESTO_FLAG_NAN_DRAFTER
+
+
+def test_topk_is_deterministic():
+    w, rin = round_data(2)
+    t = to_dev(rin["drafter_logits"], w.dtype)
+    a = [to_host(x) for x in P.presto_topk(t, w.k)]
+    b = [to_host(x) for x in P.presto_topk(t, w.k)]
+    for u, v in zip(a, b):
+        np.testing.assert_array_equal(u, v)

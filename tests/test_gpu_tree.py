@@ -1,0 +1,85 @@
+"""GPU parity of presto_build_tree: fed the same candidate tables, the GPU
+tree equals the oracle's bit for bit (topology, tokens, depths, ranks,
+fp32 scores, ancestor masks, node counts)."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2607_22634_amd as P
+import synthetic as sy
+from gpu_util import round_data, to_dev, to_host, tree_to_host
+
+pytestmark = pytest.mark.gpu
+
+KEYS = ("n_nodes", "parent", "token", "depth", "rank", "score", "anc")
+
+
+def _gpu_and_oracle(ids, lp, rho, lam, root, D, k, B, branch=None):
+    g = P.presto_build_tree(to_dev(ids), to_dev(lp), None if rho is None else to_dev(rho),
+                            to_dev(lam), to_dev(root), D, k, B, branch=branch)
+    torch.cuda.synchronize()
+    g = tree_to_host(g)
+    o = oracle.build_tree(ids, lp, rho, lam, root, D, k, B, branch=branch)
+    return g, o
+
+
+def _assert_same(g, o):
+    for key in KEYS:
+        if key == "score":
+            np.testing.assert_array_equal(g[key].view(np.uint32), o[key].view(np.uint32), err_msg=key)
+        else:
+            np.testing.assert_array_equal(g[key], o[key], err_msg=key)
+
+
+@pytest.mark.parametrize("cfg,lam", [(1, None), (2, None), (3, None), (4, None), (5, None), (5, 0.2)])
+def test_tree_matches_oracle_on_workload(cfg, lam):
+    over = {} if lam is None else {"lam": lam}
+    w, rin = round_data(cfg, **over)
+    print(f"tree cfg={cfg} batch={w.batch} B={w.budget} k={w.k}", flush=True)
+    ids, lp, _ = P.presto_topk(to_dev(rin["drafter_logits"], w.dtype), w.k)
+    ids = to_host(ids).reshape(w.batch, w.depth, w.k)
+    lp = to_host(lp).reshape(w.batch, w.depth, w.k)
+    g, o = _gpu_and_oracle(ids, lp, rin["rho"], rin["lam"], rin["root_token"], w.depth, w.k,
+                           w.budget)
+    _assert_same(g, o)
+    assert (g["n_nodes"] == w.budget + 1).all()
+
+
+def _random_batch(seed, b, D, k, quant):
+    rng = np.random.default_rng(seed)
+    lp = -rng.exponential(1.5, size=(b, D, k))
+    R = -rng.exponential(2.0, size=(b, D, k, k, k))
+    if quant:
+        lp = np.round(lp * 4) / 4
+        R = np.round(R * 2) / 2
+    R[rng.random(R.shape) < 0.3] = np.log(np.float32(1e-4))
+    lp = -np.sort(-lp, axis=2)
+    ids = np.stack([[rng.choice(5000, k, replace=False) for _ in range(D)] for _ in range(b)])
+    root = rng.integers(0, 5000, size=b)
+    return (ids.astype(np.int32), lp.astype(np.float32), R.astype(np.float32),
+            root.astype(np.int32))
+
+
+@pytest.mark.parametrize("D,k,branch,B", [(1, 1, 1, 1), (3, 2, 2, 4), (4, 3, 2, 40), (5, 3, 3, 200),
+                                          (6, 2, 1, 9), (16, 8, 8, 256), (32, 4, 3, 128),
+                                          (8, 16, 16, 255), (2, 16, 5, 63), (12, 5, 5, 130),
+                                          (10, 4, 4, 511)])
+@pytest.mark.parametrize("quant", [False, True])
+def test_tree_matches_oracle_random(D, k, branch, B, quant):
+    ids, lp, R, root = _random_batch([D, k, B, int(quant)], 24, D, k, quant)
+    for lam_v, rho in ((0.2, R), (0.0, R), (1.0, None)):
+        lam = np.full(D, lam_v, np.float32)
+        g, o = _gpu_and_oracle(ids, lp, rho, lam, root, D, k, B, branch=branch)
+        _assert_same(g, o)
+
+
+def test_tree_is_deterministic():
+    ids, lp, R, root = _random_batch(3, 8, 16, 8, True)
+    lam = np.full(16, 0.2, np.float32)
+    a = tree_to_host(P.presto_build_tree(to_dev(ids), to_dev(lp), to_dev(R), to_dev(lam),
+                                         to_dev(root), 16, 8, 256))
+    b = tree_to_host(P.presto_build_tree(to_dev(ids), to_dev(lp), to_dev(R), to_dev(lam),
+                                         to_dev(root), 16, 8, 256))
+    for key in KEYS:
+        np.testing.assert_array_equal(a[key], b[key])
