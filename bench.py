@@ -115,7 +115,7 @@ def main() -> int:
     rows = w.batch * w.depth
     topk_out = (torch.empty(rows, w.k, **i32), torch.empty(rows, w.k, dtype=torch.float32, device=dev),
                 torch.empty(rows, dtype=torch.float32, device=dev))
-    topk_ws = torch.empty(max(1, P.lib().presto_topk_workspace(rows, w.vocab, w.k)), dtype=torch.uint8,
+    topk_ws = torch.zeros(max(1, P.lib().presto_topk_workspace(rows, w.vocab, w.k)), dtype=torch.uint8,
                           device=dev)
     N = w.n_max
     tree_out = {k: torch.empty_like(v) for k, v in tree.items()}
@@ -124,48 +124,58 @@ def main() -> int:
                       P.PRESTO_DT_BF16 if w.dtype == "bf16" else P.PRESTO_DT_F32)
     import ctypes
     attn_ws_n = P.lib().presto_tree_attention_workspace(ctypes.byref(desc))
-    attn_ws = torch.empty(max(1, attn_ws_n), dtype=torch.uint8, device=dev) if attn_ws_n else None
+    attn_ws = torch.zeros(max(1, attn_ws_n), dtype=torch.uint8, device=dev) if attn_ws_n else None
     acc_out = {"accept_len": torch.empty(w.batch, **i32), "path": torch.empty(w.batch, w.depth + 1, **i32),
                "bonus": torch.empty(w.batch, **i32), "target_argmax": torch.empty(w.batch, N, **i32)}
-    acc_ws = torch.empty(P.lib().presto_accept_workspace(w.batch, N, w.vocab), dtype=torch.uint8,
+    acc_ws = torch.zeros(P.lib().presto_accept_workspace(w.batch, N, w.vocab), dtype=torch.uint8,
                          device=dev)
     flags = torch.zeros(1, **i32)
 
     stream = torch.cuda.current_stream()
-    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
 
-    def step(r, e=None):
-        d = R[r]
-        if e: e[0].record(stream)
-        P.presto_topk(d["drafter"], w.k, ids=topk_out[0], logprob=topk_out[1], lse=topk_out[2],
+    def st_topk(r):
+        P.presto_topk(R[r]["drafter"], w.k, ids=topk_out[0], logprob=topk_out[1], lse=topk_out[2],
                       flags=flags, workspace=topk_ws)
-        if e: e[1].record(stream)
+
+    def st_tree(r):
         P.presto_build_tree(topk_out[0], topk_out[1], rho, lam, root, w.depth, w.k, w.budget,
                             out=tree_out)
-        if e: e[2].record(stream)
-        for li, L in enumerate(d["layers"]):
+
+    def st_attn(r):
+        for li, L in enumerate(R[r]["layers"]):
             P.presto_tree_attention(L["q"], L["k_cache"], L["v_cache"], L["ctx_offsets"],
                                     L["k_tree"], L["v_tree"], tree_out["anc"], tree_out["n_nodes"],
                                     max_ctx, w.scale, out=attn_out[li], workspace=attn_ws)
-        if e: e[3].record(stream)
-        P.presto_accept(d["target"], tree_out["parent"], tree_out["token"], tree_out["n_nodes"],
+
+    def st_accept(r):
+        P.presto_accept(R[r]["target"], tree_out["parent"], tree_out["token"], tree_out["n_nodes"],
                         w.depth, out=acc_out, flags=flags, workspace=acc_ws)
-        if e: e[4].record(stream)
+
+    stage_fns = [st_topk, st_tree, st_attn, st_accept]
+
+    def step(r):
+        for f in stage_fns:
+            f(r)
+
+    def timed(fn, n, offset):
+        """Average ms of `fn` over n back-to-back launches (replicas cycled)."""
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record(stream)
+        for i in range(n):
+            fn((offset + i) % reps)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / n
 
     for i in range(args.warmup):
         step(i % reps)
     torch.cuda.synchronize()
-    t_start = torch.cuda.Event(enable_timing=True)
-    t_end = torch.cuda.Event(enable_timing=True)
-    t_start.record(stream)
-    for i in range(args.steps):
-        step((args.warmup + i) % reps, ev[i])
-    t_end.record(stream)
-    torch.cuda.synchronize()
-    total_ms = t_start.elapsed_time(t_end)
-    ms_per_step = total_ms / args.steps
-    stage_ms = np.array([[ev[i][j].elapsed_time(ev[i][j + 1]) for j in range(4)]
-                         for i in range(args.steps)]).mean(axis=0)
+    # the timed region: K whole rounds back to back
+    ms_per_step = timed(step, args.steps, args.warmup)
+    # per-stage averages (each stage alone, same replica cycling), for the rooflines
+    stage_ms = np.array([timed(f, args.steps, 0) for f in stage_fns])
     assert int(flags.item()) == 0, "device flagged NaN inputs"
 
     names = ["topk", "build_tree", "tree_attention", "accept"]

@@ -21,7 +21,9 @@
  *   major with a contiguous innermost dimension.  Strides are in elements.
  *   The library allocates no device memory: scratch space comes from a
  *   caller-provided device workspace of at least *_workspace() bytes
- *   (a null workspace is allowed when that size is 0).
+ *   (a null workspace is allowed when that size is 0).  Its contents on
+ *   entry are ignored; two calls in flight at the same time (on different
+ *   streams) need distinct workspaces.
  * - Every call is asynchronous on `stream` (0 = the null stream).  All
  *   argument checks happen on the host before anything is launched; on an
  *   error return nothing was enqueued.
@@ -120,7 +122,7 @@ presto_status presto_topk(presto_dtype dt, const void *logits, int64_t rows, int
  */
 typedef struct {
     int32_t batch;
-    int32_t depth;  /* block length D = maximal tree depth, 1 .. 32           */
+    int32_t depth;  /* block length D = maximal tree depth, 1 .. 32 (24 if k=16) */
     int32_t k;      /* candidates per position, 1 .. 16                        */
     int32_t branch; /* children per expansion, 1 .. k                          */
     int32_t budget; /* B, draft nodes excluding the root, 1 .. 511            */

@@ -131,7 +131,7 @@ def _workspace(nbytes: int, device, ws):
         return None, 0
     if ws is not None:
         return ws, ws.numel() * ws.element_size()
-    t = torch.empty(nbytes, dtype=torch.uint8, device=device)
+    t = torch.zeros(nbytes, dtype=torch.uint8, device=device)  # workspaces start zeroed
     return t, nbytes
 
 

@@ -1,12 +1,12 @@
 // Stage 4: greedy verification of the tree and the bonus token.
 //
-// Kernel 1 streams every live node's target logit row from HBM once and
-// leaves, per wave-sized chunk, the chunk maximum and the lowest id holding
-// it (packed into one orderable 64-bit key).  Rows of padding nodes are
-// skipped without being read.  Kernel 2 (one workgroup per sequence)
-// reduces the chunk keys to the target's greedy prediction a[n] of every
-// node, stages the tree in LDS and walks it from the root: move to the
-// child whose token equals a[current] until no child does.
+// Kernel 1 streams every live node's target logit row from HBM once (rows of
+// padding nodes are never read) and leaves, per wave-sized chunk, the chunk
+// maximum and the lowest id holding it, packed into one orderable 64-bit
+// key.  Kernel 2, queued right behind, runs one workgroup per sequence: its
+// waves reduce the chunk keys of the live nodes to the target's greedy
+// prediction a[n] (into LDS), then one wave walks the tree from the root:
+// move to the child whose token equals a[current] until no child does.
 #include <math.h>
 
 #include "common.hpp"
@@ -14,7 +14,7 @@
 namespace presto {
 
 constexpr int kArgmaxWavesPerBlock = 4;
-constexpr int kWalkThreads = 256;
+constexpr int kWalkThreads = 1024;
 constexpr int kMaxNodes = 1024;
 
 template <bool BF16, int NLOAD>
@@ -71,10 +71,10 @@ __global__ __launch_bounds__(kArgmaxWavesPerBlock * kWave) void argmax_partial_k
 #pragma unroll
     for (int e = 0; e < E; ++e) {
         lm = fmaxf(lm, v[e]);
-        sum += v[e];
+        sum += v[e];  // only to detect NaN
     }
-    const float M = wave_max(lm);
-    // lowest vocabulary id of the lane holding the chunk maximum
+    const float M = wave_max_f32_dpp(lm);
+    // lowest vocabulary id holding the chunk maximum
     uint32_t best = 0xffffffffu;
 #pragma unroll
     for (int e = 0; e < E; ++e) {
@@ -82,18 +82,15 @@ __global__ __launch_bounds__(kArgmaxWavesPerBlock * kWave) void argmax_partial_k
         const bool hit = (v[e] == M) && (full || idx < vocab);
         best = (hit && (uint32_t)idx < best) ? (uint32_t)idx : best;
     }
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) {
-        const uint32_t w = __shfl_xor(best, o, kWave);
-        best = w < best ? w : best;
-    }
-    const float tot = wave_sum(sum);
+    best = wave_min_u32_dpp(best);
+    const float tot = wave_sum_f32_dpp(sum);
     if (lane == 0) {
         part[gw] = vocab_key(M, best);
         if (!(tot == tot)) raise_flag(flags, PRESTO_FLAG_NAN_TARGET);
     }
 }
 
+// One workgroup per sequence: per-node argmax from the chunk keys, then the walk.
 __global__ __launch_bounds__(kWalkThreads) void accept_walk_kernel(
     int32_t n_max, int32_t depth, int32_t chunks, const uint64_t* __restrict__ part,
     const int32_t* __restrict__ parent, const int32_t* __restrict__ token,
@@ -104,22 +101,35 @@ __global__ __launch_bounds__(kWalkThreads) void accept_walk_kernel(
     __shared__ int32_t s_tok[kMaxNodes];
     const int b = blockIdx.x;
     const int nn = min(max(n_nodes[b], 1), n_max);
-    for (int n = threadIdx.x; n < n_max; n += kWalkThreads) {
-        int32_t a = -1;
-        if (n < nn) {
-            const uint64_t* p = part + ((int64_t)b * n_max + n) * chunks;
-            uint64_t best = 0ull;
-            for (int c = 0; c < chunks; ++c) best = p[c] > best ? p[c] : best;
-            a = (int32_t)key_id(best);
+    const int wave = threadIdx.x / kWave, lane = lane_id();
+    const int nwaves = blockDim.x / kWave;
+    const int64_t rb = (int64_t)b * n_max;
+    for (int n = threadIdx.x; n < n_max; n += blockDim.x) {
+        s_par[n] = n < nn ? parent[rb + n] : -2;
+        s_tok[n] = token[rb + n];
+    }
+    // each wave reduces the chunk keys of four nodes at a time
+    for (int n0 = wave * 4; n0 < nn; n0 += nwaves * 4) {
+        uint64_t best[4] = {0ull, 0ull, 0ull, 0ull};
+        for (int c = lane; c < chunks; c += kWave) {
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                if (n0 + u < nn) {
+                    const uint64_t x = part[(rb + n0 + u) * chunks + c];
+                    best[u] = x > best[u] ? x : best[u];
+                }
+            }
         }
-        s_a[n] = a;
-        s_par[n] = parent[(int64_t)b * n_max + n];
-        s_tok[n] = token[(int64_t)b * n_max + n];
-        if (target_argmax) target_argmax[(int64_t)b * n_max + n] = a;
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const uint64_t m = wave_max_u64_dpp(best[u]);
+            if (lane == 0 && n0 + u < nn) s_a[n0 + u] = (int32_t)key_id(m);
+        }
     }
     __syncthreads();
-    if (threadIdx.x >= kWave) return;
-    const int lane = threadIdx.x;
+    for (int n = threadIdx.x; n < n_max; n += blockDim.x)
+        if (target_argmax) target_argmax[rb + n] = n < nn ? s_a[n] : -1;
+    if (wave != 0) return;
     int32_t* pth = path + (int64_t)b * (depth + 1);
     int cur = 0, L = 0;
     for (;;) {
@@ -187,9 +197,10 @@ presto_status launch_accept(bool bf16, const void* logits, int32_t vocab, int64_
 #undef PRESTO_ARGMAX
     presto_status st = check_launch("argmax_partial_kernel");
     if (st != PRESTO_OK) return st;
-    accept_walk_kernel<<<batch, kWalkThreads, 0, stream>>>(n_max, depth, (int32_t)chunks, part,
-                                                           parent, token, n_nodes, accept_len,
-                                                           path, bonus, target_argmax);
+    const int threads = n_max >= 512 ? kWalkThreads : (n_max >= 128 ? 512 : 256);
+    accept_walk_kernel<<<batch, threads, 0, stream>>>(n_max, depth, (int32_t)chunks, part, parent,
+                                                      token, n_nodes, accept_len, path, bonus,
+                                                      target_argmax);
     return check_launch("accept_walk_kernel");
 }
 

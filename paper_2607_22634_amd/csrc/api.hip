@@ -15,6 +15,7 @@ presto_status launch_topk(bool bf16, const void* logits, int64_t rows, int32_t v
                           int64_t row_stride, int32_t k, int32_t* ids, float* logprob, float* lse,
                           int32_t* flags, void* ws, hipStream_t stream);
 bool tree_build_fits(int D, int k, int branch, int N);
+int tree_max_depth(int k);
 presto_status launch_build_tree(const presto_tree_desc* desc, const int32_t* ids,
                                 const float* logprob, const float* log_rho, const float* lambda,
                                 const int32_t* root_token, int32_t* n_nodes, int32_t* parent,
@@ -116,9 +117,9 @@ presto_status presto_build_tree(const presto_tree_desc* desc, const int32_t* ids
             d.branch);
     REQUIRE(d.budget >= 1 && d.budget <= 511, "presto_build_tree: budget=%d outside 1..511",
             d.budget);
-    int wbits = 1;
-    while ((1 << wbits) < d.k + 1) ++wbits;
-    REQUIRE(d.depth * wbits <= 128, "presto_build_tree: depth*ceil(log2(k+1)) > 128");
+    REQUIRE(d.depth <= tree_max_depth(d.k),
+            "presto_build_tree: depth %d exceeds the rank-path key (at most %d for k=%d)", d.depth,
+            tree_max_depth(d.k), d.k);
     if (d.mode == PRESTO_TREE_BEST_FIRST_ALG2 || d.mode == PRESTO_TREE_BEAM)
         return set_error(PRESTO_ERR_UNSUPPORTED, "presto_build_tree: mode %d not built", d.mode);
     REQUIRE(d.mode == PRESTO_TREE_BEST_FIRST, "presto_build_tree: unknown mode %d", d.mode);

@@ -98,6 +98,107 @@ __device__ __forceinline__ int wave_sum_i32(int v) {
 
 __device__ __forceinline__ int lane_id() { return threadIdx.x & (kWave - 1); }
 
+// ---------------------------------------------------------------------------
+// DPP reductions (no LDS traffic).  `old` is the identity, returned by lanes
+// whose DPP source is out of range or masked off.
+template <int CTRL, int ROW_MASK = 0xf>
+__device__ __forceinline__ uint32_t dpp_u32(uint32_t old, uint32_t v) {
+    return (uint32_t)__builtin_amdgcn_update_dpp((int)old, (int)v, CTRL, ROW_MASK, 0xf, false);
+}
+
+// Unsigned max over the whole wave (result returned to every lane).
+__device__ __forceinline__ uint32_t wave_max_u32_dpp(uint32_t v) {
+    v = max(v, dpp_u32<0xb1>(0u, v));        // quad_perm [1,0,3,2]
+    v = max(v, dpp_u32<0x4e>(0u, v));        // quad_perm [2,3,0,1]
+    v = max(v, dpp_u32<0x114>(0u, v));       // row_shr:4
+    v = max(v, dpp_u32<0x118>(0u, v));       // row_shr:8
+    v = max(v, dpp_u32<0x142, 0xa>(0u, v));  // row_bcast:15
+    v = max(v, dpp_u32<0x143, 0xc>(0u, v));  // row_bcast:31
+    return (uint32_t)__builtin_amdgcn_readlane((int)v, 63);
+}
+
+template <int CTRL, int ROW_MASK = 0xf>
+__device__ __forceinline__ uint64_t dpp_u64(uint64_t old, uint64_t v) {
+    const uint32_t lo = dpp_u32<CTRL, ROW_MASK>((uint32_t)old, (uint32_t)v);
+    const uint32_t hi = dpp_u32<CTRL, ROW_MASK>((uint32_t)(old >> 32), (uint32_t)(v >> 32));
+    return ((uint64_t)hi << 32) | lo;
+}
+
+__device__ __forceinline__ uint64_t readlane_u64(uint64_t v, int lane) {
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)v, lane);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(v >> 32), lane);
+    return ((uint64_t)hi << 32) | lo;
+}
+
+template <int CTRL, int ROW_MASK = 0xf>
+__device__ __forceinline__ float dpp_f32(float old, float v) {
+    return __uint_as_float(dpp_u32<CTRL, ROW_MASK>(__float_as_uint(old), __float_as_uint(v)));
+}
+
+// Float max / sum over the whole wave (result returned to every lane).
+__device__ __forceinline__ float wave_max_f32_dpp(float v) {
+    v = fmaxf(v, dpp_f32<0xb1>(-INFINITY, v));
+    v = fmaxf(v, dpp_f32<0x4e>(-INFINITY, v));
+    v = fmaxf(v, dpp_f32<0x114>(-INFINITY, v));
+    v = fmaxf(v, dpp_f32<0x118>(-INFINITY, v));
+    v = fmaxf(v, dpp_f32<0x142, 0xa>(-INFINITY, v));
+    v = fmaxf(v, dpp_f32<0x143, 0xc>(-INFINITY, v));
+    return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 63));
+}
+
+__device__ __forceinline__ float wave_sum_f32_dpp(float v) {
+    v += dpp_f32<0xb1>(0.f, v);
+    v += dpp_f32<0x4e>(0.f, v);
+    v += dpp_f32<0x114>(0.f, v);
+    v += dpp_f32<0x118>(0.f, v);
+    v += dpp_f32<0x142, 0xa>(0.f, v);
+    v += dpp_f32<0x143, 0xc>(0.f, v);
+    return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 63));
+}
+
+__device__ __forceinline__ uint32_t wave_min_u32_dpp(uint32_t v) {
+    v = min(v, dpp_u32<0xb1>(~0u, v));
+    v = min(v, dpp_u32<0x4e>(~0u, v));
+    v = min(v, dpp_u32<0x114>(~0u, v));
+    v = min(v, dpp_u32<0x118>(~0u, v));
+    v = min(v, dpp_u32<0x142, 0xa>(~0u, v));
+    v = min(v, dpp_u32<0x143, 0xc>(~0u, v));
+    return (uint32_t)__builtin_amdgcn_readlane((int)v, 63);
+}
+
+// Unsigned 64-bit max / min over the whole wave.
+__device__ __forceinline__ uint64_t wave_max_u64_dpp(uint64_t v) {
+    uint64_t t;
+    t = dpp_u64<0xb1>(0ull, v); v = t > v ? t : v;
+    t = dpp_u64<0x4e>(0ull, v); v = t > v ? t : v;
+    t = dpp_u64<0x114>(0ull, v); v = t > v ? t : v;
+    t = dpp_u64<0x118>(0ull, v); v = t > v ? t : v;
+    t = dpp_u64<0x142, 0xa>(0ull, v); v = t > v ? t : v;
+    t = dpp_u64<0x143, 0xc>(0ull, v); v = t > v ? t : v;
+    return readlane_u64(v, 63);
+}
+
+__device__ __forceinline__ uint64_t wave_min_u64_dpp(uint64_t v) {
+    uint64_t t;
+    t = dpp_u64<0xb1>(~0ull, v); v = t < v ? t : v;
+    t = dpp_u64<0x4e>(~0ull, v); v = t < v ? t : v;
+    t = dpp_u64<0x114>(~0ull, v); v = t < v ? t : v;
+    t = dpp_u64<0x118>(~0ull, v); v = t < v ? t : v;
+    t = dpp_u64<0x142, 0xa>(~0ull, v); v = t < v ? t : v;
+    t = dpp_u64<0x143, 0xc>(~0ull, v); v = t < v ? t : v;
+    return readlane_u64(v, 63);
+}
+
+// Unsigned 64-bit max over lanes 0..15 (row 0), returned to every lane.
+__device__ __forceinline__ uint64_t row0_max_u64_dpp(uint64_t v) {
+    uint64_t t;
+    t = dpp_u64<0xb1>(0ull, v); v = t > v ? t : v;
+    t = dpp_u64<0x4e>(0ull, v); v = t > v ? t : v;
+    t = dpp_u64<0x114>(0ull, v); v = t > v ? t : v;
+    t = dpp_u64<0x118>(0ull, v); v = t > v ? t : v;
+    return readlane_u64(v, 15);
+}
+
 // Flags word: OR a bit from one lane (vector atomic).
 __device__ __forceinline__ void raise_flag(int32_t* flags, int32_t bit) {
     if (flags) atomicOr(flags, bit);

@@ -2,15 +2,16 @@
 //
 // The vocabulary row of each position is streamed from HBM once.  A row is
 // cut into wave-sized chunks; every wave holds its chunk in registers and
-// produces, with no LDS barrier and no block-level synchronisation:
+// produces, with no block-level synchronisation:
 //   * the chunk maximum m and sum exp(z - m)           (for the row's LSE)
 //   * the chunk's k best (value desc, id asc) entries  (as 64-bit keys)
-// The k-th largest lane maximum is a lower bound on the chunk's k-th value,
-// so only entries at or above it are candidates (normally k to 2k of them);
-// they are compacted through a small per-wave LDS list and ranked there.
-// A chunk with more than kCandCap candidates (massive ties) falls back to
-// k rounds of exact wave-wide selection.  A second kernel merges the chunk
-// partials of each row (one wave per row).
+// The k-th largest lane maximum (found by a 32-step ballot bisection on its
+// orderable bits) is a lower bound on the chunk's k-th value, so only entries
+// at or above it are candidates (normally k to 2k of them); they are
+// compacted through a small per-wave LDS list and ranked there.  A chunk
+// with more than kCandCap candidates (massive ties) falls back to k rounds
+// of exact wave-wide selection.  A second kernel, queued right behind,
+// merges each row's chunk partials with one wave per row.
 #include <math.h>
 
 #include "common.hpp"
@@ -77,19 +78,16 @@ __device__ __forceinline__ void load_chunk(const void* __restrict__ row, int64_t
     }
 }
 
-// Descending bitonic sort of one float per lane across the wave.
-__device__ __forceinline__ float wave_sort_desc(float x) {
-    const int lane = lane_id();
+// The k-th largest value of one u32 per lane (k <= 64): bisection on the
+// bits, counting lanes at or above each probe with a ballot.
+__device__ __forceinline__ uint32_t wave_kth_largest_u32(uint32_t x, int k) {
+    uint32_t t = 0u;
 #pragma unroll
-    for (int size = 2; size <= kWave; size <<= 1) {
-#pragma unroll
-        for (int stride = size >> 1; stride > 0; stride >>= 1) {
-            const float y = __shfl_xor(x, stride, kWave);
-            const bool keep_max = ((lane & size) == 0) == ((lane & stride) == 0);
-            x = keep_max ? fmaxf(x, y) : fminf(x, y);
-        }
+    for (int bit = 31; bit >= 0; --bit) {
+        const uint32_t c = t | (1u << bit);
+        if (__popcll(__ballot(x >= c)) >= k) t = c;
     }
-    return x;
+    return t;
 }
 
 template <bool BF16, int NLOAD>
@@ -115,23 +113,17 @@ __global__ __launch_bounds__(kTopkWavesPerBlock * kWave) void topk_partial_kerne
     float v[E];
     load_chunk<BF16, NLOAD>(rowp, c0, vocab, full, v);
 
-    // lane and wave maxima
     float lm = -INFINITY;
 #pragma unroll
     for (int e = 0; e < E; ++e) lm = fmaxf(lm, v[e]);
-    const float M = wave_max(lm);
-
-    // sum exp(z - M) over the chunk
+    const float M = wave_max_f32_dpp(lm);
     float s = 0.f;
     if (M != -INFINITY) {
 #pragma unroll
         for (int e = 0; e < E; ++e) s += __expf(v[e] - M);
     }
-    const float S = wave_sum(s);
-
-    // threshold: k-th largest lane maximum
-    const float sorted = wave_sort_desc(lm);
-    const float thr = __shfl(sorted, k - 1, kWave);
+    const float S = wave_sum_f32_dpp(s);
+    const float thr = unord32(wave_kth_largest_u32(ord32(lm), k));
 
     if (lane == 0) cand_n[wave] = 0u;
     __builtin_amdgcn_wave_barrier();
@@ -166,7 +158,7 @@ __global__ __launch_bounds__(kTopkWavesPerBlock * kWave) void topk_partial_kerne
                     if (key < last && key > best) best = key;
                 }
             }
-            last = wave_max_u64(best);
+            last = wave_max_u64_dpp(best);
             if (lane == 0) out[j] = last;
         }
     }
@@ -176,6 +168,10 @@ __global__ __launch_bounds__(kTopkWavesPerBlock * kWave) void topk_partial_kerne
     }
 }
 
+// One wave per row: LSE from the chunk (max, sum) pairs, then the k best of
+// the chunk keys by k rounds of wave-wide selection over keys held in
+// registers (KPL per lane; KPL == 0 re-reads them from memory).
+template <int KPL>
 __global__ __launch_bounds__(kTopkWavesPerBlock * kWave) void topk_merge_kernel(
     int64_t rows, int32_t chunks, int32_t k, const float2* __restrict__ part_ms,
     const uint64_t* __restrict__ part_keys, int32_t* __restrict__ ids, float* __restrict__ logprob,
@@ -184,29 +180,42 @@ __global__ __launch_bounds__(kTopkWavesPerBlock * kWave) void topk_merge_kernel(
     const int64_t row = (int64_t)blockIdx.x * kTopkWavesPerBlock + wave;
     if (row >= rows) return;
     const float2* ms = part_ms + row * chunks;
+    const uint64_t* keys = part_keys + row * chunks * k;
+    const int nk = chunks * k;
 
+    uint64_t kr[KPL > 0 ? KPL : 1];
+    if constexpr (KPL > 0) {
+#pragma unroll
+        for (int i = 0; i < KPL; ++i) {
+            const int idx = i * kWave + lane;
+            kr[i] = idx < nk ? keys[idx] : 0ull;
+        }
+    }
     float m = -INFINITY;
     for (int c = lane; c < chunks; c += kWave) m = fmaxf(m, ms[c].x);
-    const float M = wave_max(m);
+    const float M = wave_max_f32_dpp(m);
     float s = 0.f;
     if (M != -INFINITY)
         for (int c = lane; c < chunks; c += kWave) {
             const float2 p = ms[c];
             s += p.x == -INFINITY ? 0.f : p.y * __expf(p.x - M);
         }
-    const float S = wave_sum(s);
+    const float S = wave_sum_f32_dpp(s);
     const float L = (M == -INFINITY) ? -INFINITY : M + __logf(S);
 
-    const uint64_t* keys = part_keys + row * chunks * k;
-    const int nk = chunks * k;
     uint64_t last = ~0ull, mine = 0ull;
     for (int j = 0; j < k; ++j) {
         uint64_t best = 0ull;
-        for (int i = lane; i < nk; i += kWave) {
-            const uint64_t key = keys[i];
-            if (key < last && key > best) best = key;
+        if constexpr (KPL > 0) {
+#pragma unroll
+            for (int i = 0; i < KPL; ++i) best = (kr[i] < last && kr[i] > best) ? kr[i] : best;
+        } else {
+            for (int i = lane; i < nk; i += kWave) {
+                const uint64_t key = keys[i];
+                best = (key < last && key > best) ? key : best;
+            }
         }
-        last = wave_max_u64(best);
+        last = wave_max_u64_dpp(best);
         if (lane == j) mine = last;
     }
     if (lane < k) {
@@ -228,11 +237,6 @@ static int topk_nload(bool bf16, int64_t rows, int32_t vocab) {
     return waves8 >= 4 * 256 * 4 ? 8 : 4;
 }
 
-static int64_t topk_chunks(bool bf16, int64_t rows, int32_t vocab) {
-    const int64_t ch = (int64_t)kWave * topk_nload(bf16, rows, vocab) * (bf16 ? 8 : 4);
-    return (vocab + ch - 1) / ch;
-}
-
 size_t topk_workspace_bytes(int64_t rows, int32_t vocab, int32_t k) {
     // sized for the finest chunking any dtype may pick
     const int64_t chunks = (vocab + (int64_t)kWave * 16 - 1) / ((int64_t)kWave * 16);
@@ -244,7 +248,8 @@ presto_status launch_topk(bool bf16, const void* logits, int64_t rows, int32_t v
                           int64_t row_stride, int32_t k, int32_t* ids, float* logprob, float* lse,
                           int32_t* flags, void* ws, hipStream_t stream) {
     const int nload = topk_nload(bf16, rows, vocab);
-    const int64_t chunks = topk_chunks(bf16, rows, vocab);
+    const int64_t ch = (int64_t)kWave * nload * (bf16 ? 8 : 4);
+    const int64_t chunks = (vocab + ch - 1) / ch;
     const size_t esz = bf16 ? 2 : 4;
     const bool aligned = ((uintptr_t)logits % 16 == 0) && ((row_stride * (int64_t)esz) % 16 == 0);
     float2* ms = static_cast<float2*>(ws);
@@ -253,26 +258,29 @@ presto_status launch_topk(bool bf16, const void* logits, int64_t rows, int32_t v
     const int64_t waves = rows * chunks;
     const dim3 block(kTopkWavesPerBlock * kWave);
     const dim3 grid((unsigned)((waves + kTopkWavesPerBlock - 1) / kTopkWavesPerBlock));
+#define PRESTO_TOPK(BF, NL)                                                                 \
+    topk_partial_kernel<BF, NL><<<grid, block, 0, stream>>>(logits, rows, vocab, row_stride, \
+                                                           k, (int32_t)chunks, aligned, ms,  \
+                                                           keys, flags)
     if (bf16) {
-        if (nload == 8)
-            topk_partial_kernel<true, 8><<<grid, block, 0, stream>>>(
-                logits, rows, vocab, row_stride, k, (int32_t)chunks, aligned, ms, keys, flags);
-        else
-            topk_partial_kernel<true, 4><<<grid, block, 0, stream>>>(
-                logits, rows, vocab, row_stride, k, (int32_t)chunks, aligned, ms, keys, flags);
+        if (nload == 8) PRESTO_TOPK(true, 8); else PRESTO_TOPK(true, 4);
     } else {
-        if (nload == 8)
-            topk_partial_kernel<false, 8><<<grid, block, 0, stream>>>(
-                logits, rows, vocab, row_stride, k, (int32_t)chunks, aligned, ms, keys, flags);
-        else
-            topk_partial_kernel<false, 4><<<grid, block, 0, stream>>>(
-                logits, rows, vocab, row_stride, k, (int32_t)chunks, aligned, ms, keys, flags);
+        if (nload == 8) PRESTO_TOPK(false, 8); else PRESTO_TOPK(false, 4);
     }
+#undef PRESTO_TOPK
     presto_status st = check_launch("topk_partial_kernel");
     if (st != PRESTO_OK) return st;
     const dim3 mgrid((unsigned)((rows + kTopkWavesPerBlock - 1) / kTopkWavesPerBlock));
-    topk_merge_kernel<<<mgrid, block, 0, stream>>>(rows, (int32_t)chunks, k, ms, keys, ids,
-                                                    logprob, lse);
+    const int64_t per_lane = (chunks * k + kWave - 1) / kWave;
+#define PRESTO_MERGE(KP)                                                                     \
+    topk_merge_kernel<KP><<<mgrid, block, 0, stream>>>(rows, (int32_t)chunks, k, ms, keys, \
+                                                       ids, logprob, lse)
+    if (per_lane <= 2) PRESTO_MERGE(2);
+    else if (per_lane <= 4) PRESTO_MERGE(4);
+    else if (per_lane <= 8) PRESTO_MERGE(8);
+    else if (per_lane <= 16) PRESTO_MERGE(16);
+    else PRESTO_MERGE(0);
+#undef PRESTO_MERGE
     return check_launch("topk_merge_kernel");
 }
 

@@ -8,14 +8,17 @@
 // 0 .. ctx_b-1 read the packed cache, positions ctx_b .. ctx_b+n_nodes-1
 // read the tree K/V and are masked by the ancestor bitmask.
 //
-// bf16 path (matrix cores, v_mfma_f32_16x16x32_bf16).  Each wave owns 32
-// query rows.  Scores are computed transposed, S^T = K Q^T, so that each
-// lane holds one query row and 4+4 keys of a 32-key step: the row max/sum
-// need only two cross-lane steps, and the probabilities already sit in the
-// B-operand layout of O^T = V^T P^T; V is staged transposed in LDS to feed
-// the A operand.  The context is split across workgroups when a sequence
-// alone cannot fill the chip; partial (max, sum, accumulator) triples are
-// then merged by a second kernel.
+// bf16 path (matrix cores, v_mfma_f32_32x32x16_bf16).  A workgroup is four
+// waves, one per SIMD, each owning 64 query rows (two 32-row MFMA blocks, so
+// every K/V fragment read from LDS feeds two MFMAs).  Scores are computed
+// transposed, S^T = K Q^T: a lane then holds one query row and 16 of the 32
+// keys of a block, the row max/sum need one cross-half swap, and the bf16
+// probabilities are already in the B-operand layout of O^T = V^T P^T.  K and
+// V sit in LDS row-major; the V^T operand comes from transposed LDS reads
+// (ds_read_b64_tr_b16).  The next K/V tile is fetched into registers while
+// the current one is consumed.  The context is split across workgroups when
+// the batch alone cannot fill the chip; partial (max, sum, accumulator)
+// triples are then merged by a second kernel.
 #include <math.h>
 
 #include "common.hpp"
@@ -24,12 +27,14 @@ namespace presto {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float floatx4 __attribute__((ext_vector_type(4)));
+typedef float floatx16 __attribute__((ext_vector_type(16)));
+typedef short short4_t __attribute__((ext_vector_type(4)));
 
-constexpr int kKeyTile = 64;  // keys per LDS tile
-constexpr int kRowsPerWave = 32;
-constexpr int kMaxRowsPerTile = 256;  // 8 waves: two per SIMD, 256 registers each
-constexpr int kKPad = 8;      // bf16 padding of a K row in LDS (bank spread)
-constexpr int kVPad = 8;      // bf16 padding of a V^T row in LDS
+constexpr int kKeyTile = 64;      // keys per LDS tile
+constexpr int kRowsPerWave = 64;  // two 32-row MFMA blocks per wave
+constexpr int kAttnWaves = 4;     // one wave per SIMD (about 300 registers each)
+constexpr int kAttnThreads = kAttnWaves * kWave;
+constexpr int kRowsPerTile = kAttnWaves * kRowsPerWave;
 constexpr float kLog2e = 1.4426950408889634f;
 
 struct AttnArgs {
@@ -44,7 +49,7 @@ struct AttnArgs {
     uint16_t* out;
     float* part;  // [batch, hkv, rows_pad, splits, D + 2] when splits > 1
     int32_t batch, n_max, hq, hkv, G, W;
-    int32_t row_tiles, rows_per_tile, rows_pad, splits, split_len;
+    int32_t row_tiles, rows_pad, splits, split_len;
     int32_t n_tasks, n_blocks;
     float scale_log2;  // scale * log2(e)
 };
@@ -62,13 +67,15 @@ __device__ __forceinline__ int xcd_task(int bid, int n_blocks) {
 }
 
 template <int D>
-__global__ __launch_bounds__(512) void tree_attn_bf16_kernel(AttnArgs a) {
-    constexpr int DB = D / 16;  // 16-wide blocks of the head dimension
-    constexpr int KS = D / 32;  // 32-deep contraction steps over the head dimension
-    constexpr int KROW = D + kKPad;
-    constexpr int VROW = kKeyTile + kVPad;
+__global__ __launch_bounds__(kAttnThreads, 1) void tree_attn_bf16_kernel(AttnArgs a) {
+    constexpr int KS = D / 16;                 // S^T contraction steps over the head dimension
+    constexpr int DB = D / 32;                 // 32-wide blocks of the output head dimension
+    constexpr int KROW = D + 8;                // K row in LDS (bf16): bank spread for b128 reads
+    constexpr int VROW = D + 16;               // V row in LDS: bank spread for transposed reads
+    constexpr int PIECES = kKeyTile * D / 8;   // 16-byte pieces of one K (or V) tile
+    constexpr int PT = PIECES / kAttnThreads;  // pieces per thread
     __shared__ __align__(16) uint16_t sK[kKeyTile * KROW];
-    __shared__ __align__(16) uint16_t sV[D * VROW];
+    __shared__ __align__(16) uint16_t sV[kKeyTile * VROW];
 
     const int task = xcd_task(blockIdx.x, a.n_blocks);
     if (task >= a.n_tasks) return;
@@ -85,226 +92,284 @@ __global__ __launch_bounds__(512) void tree_attn_bf16_kernel(AttnArgs a) {
     if (k_begin >= keys) return;  // nothing of this sequence in this split
     const int k_end = min(keys, k_begin + a.split_len);
     const int live_rows = a.G * nn;
+    const int all_rows = a.G * a.n_max;
 
-    const int tid = threadIdx.x, nthr = blockDim.x;
+    const int tid = threadIdx.x;
     const int wave = tid / kWave, lane = lane_id();
-    const int li = lane & 15, lg = lane >> 4;  // row within a 16-block, lane group
-    const int row0 = rt * a.rows_per_tile + wave * kRowsPerWave;
+    const int l32 = lane & 31, h = lane >> 5;
+    const int rbase = rt * kRowsPerTile + wave * kRowsPerWave;  // two 32-row blocks per wave
+    const bool active = rbase < live_rows;
 
-    // Q fragments (B operand of S^T = K Q^T): lane holds row li, d = ks*32 + lg*8 .. +8
+    // Q fragments, B operand of S^T = K Q^T: lane holds row l32, d = ks*16 + h*8 .. +8
     bf16x8 qf[2][KS];
     int node_of[2];
 #pragma unroll
-    for (int blk = 0; blk < 2; ++blk) {
-        const int rho = row0 + blk * 16 + li;
+    for (int nb = 0; nb < 2; ++nb) {
+        const int rho = rbase + nb * 32 + l32;
         const int n = rho / a.G, hh = rho - n * a.G;
-        node_of[blk] = n;
-        const bool ok = rho < a.G * a.n_max;
+        node_of[nb] = min(n, a.n_max - 1);
         const uint16_t* qp = a.q + (((int64_t)b * a.n_max + n) * a.hq + g * a.G + hh) * D;
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks) {
             uint4 u = make_uint4(0, 0, 0, 0);
-            if (ok) u = *reinterpret_cast<const uint4*>(qp + ks * 32 + lg * 8);
-            qf[blk][ks] = __builtin_bit_cast(bf16x8, u);
+            if (rho < all_rows) u = *reinterpret_cast<const uint4*>(qp + ks * 16 + h * 8);
+            qf[nb][ks] = __builtin_bit_cast(bf16x8, u);
         }
     }
 
-    floatx4 o[2][DB];
+    floatx16 o[2][DB];
     float m_run[2], l_run[2];
 #pragma unroll
-    for (int blk = 0; blk < 2; ++blk) {
-        m_run[blk] = -INFINITY;
-        l_run[blk] = 0.f;
+    for (int nb = 0; nb < 2; ++nb) {
+        m_run[nb] = -INFINITY;
+        l_run[nb] = 0.f;
 #pragma unroll
-        for (int db = 0; db < DB; ++db) o[blk][db] = floatx4{0.f, 0.f, 0.f, 0.f};
+        for (int db = 0; db < DB; ++db)
+#pragma unroll
+            for (int i = 0; i < 16; ++i) o[nb][db][i] = 0.f;
     }
 
-    const int64_t kv_stride = (int64_t)a.hkv * D;  // elements between consecutive positions
-    for (int t0 = k_begin; t0 < k_end; t0 += kKeyTile) {
-        // ---- stage K (row major) and V (transposed) of keys t0 .. t0+63
-        constexpr int PIECES = kKeyTile * D / 8;
-        for (int p = tid; p < PIECES; p += nthr) {
-            const int kk = p / (D / 8), c8 = p % (D / 8);
-            const int j = t0 + kk;
-            uint4 ku = make_uint4(0, 0, 0, 0), vu = make_uint4(0, 0, 0, 0);
-            if (j < k_end) {
-                const uint16_t *ks, *vs;
-                if (j < ctx) {
-                    const int64_t off = (int64_t)(c0 + j) * kv_stride + (int64_t)g * D + c8 * 8;
-                    ks = a.kc + off;
-                    vs = a.vc + off;
-                } else {
-                    const int64_t off = (((int64_t)b * a.n_max + (j - ctx)) * a.hkv + g) * D + c8 * 8;
-                    ks = a.kt + off;
-                    vs = a.vt + off;
-                }
-                ku = *reinterpret_cast<const uint4*>(ks);
-                vu = *reinterpret_cast<const uint4*>(vs);
-            }
-            *reinterpret_cast<uint4*>(&sK[kk * KROW + c8 * 8]) = ku;
-            const uint32_t vw[4] = {vu.x, vu.y, vu.z, vu.w};
+    // K/V tile staging: PT 16-byte pieces of K and of V per thread, fetched into
+    // registers one tile ahead and written to LDS row-major.
+    const int64_t kv_stride = (int64_t)a.hkv * D;
+    uint4 kreg[PT], vreg[PT];
+    auto fetch = [&](int t0) {
 #pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                sV[(c8 * 8 + 2 * e) * VROW + kk] = (uint16_t)(vw[e] & 0xffffu);
-                sV[(c8 * 8 + 2 * e + 1) * VROW + kk] = (uint16_t)(vw[e] >> 16);
+        for (int i = 0; i < PT; ++i) {
+            const int p = tid + i * kAttnThreads;
+            const int kk = p / (D / 8), c8 = p % (D / 8);
+            const int jr = t0 + kk;
+            const int j = min(jr, k_end - 1);  // clamped: every load is in bounds
+            const bool in_ctx = j < ctx;
+            const int64_t off = in_ctx
+                ? (int64_t)(c0 + j) * kv_stride + (int64_t)g * D + c8 * 8
+                : (((int64_t)b * a.n_max + (j - ctx)) * a.hkv + g) * D + c8 * 8;
+            const uint4 ku = *reinterpret_cast<const uint4*>((in_ctx ? a.kc : a.kt) + off);
+            const uint4 vu = *reinterpret_cast<const uint4*>((in_ctx ? a.vc : a.vt) + off);
+            const bool ok = jr < k_end;
+            kreg[i] = ok ? ku : make_uint4(0, 0, 0, 0);
+            vreg[i] = ok ? vu : make_uint4(0, 0, 0, 0);
+        }
+    };
+    auto stage = [&]() {
+#pragma unroll
+        for (int i = 0; i < PT; ++i) {
+            const int p = tid + i * kAttnThreads;
+            const int kk = p / (D / 8), c8 = p % (D / 8);
+            *reinterpret_cast<uint4*>(&sK[kk * KROW + c8 * 8]) = kreg[i];
+            *reinterpret_cast<uint4*>(&sV[kk * VROW + c8 * 8]) = vreg[i];
+        }
+    };
+
+    fetch(k_begin);
+    for (int t0 = k_begin; t0 < k_end; t0 += kKeyTile) {
+        __syncthreads();  // the previous tile has been consumed
+        stage();
+        __syncthreads();
+        if (t0 + kKeyTile < k_end) fetch(t0 + kKeyTile);
+        if (!active) continue;
+        const bool plain = t0 + kKeyTile <= min(ctx, k_end);  // no mask inside this tile
+        // ancestor words covering the tree keys of this tile, per row block
+        uint64_t aw[2][2] = {{0ull, 0ull}, {0ull, 0ull}};
+        int wbase = 0;
+        if (!plain && t0 + kKeyTile > ctx) {
+            wbase = max(0, t0 - ctx) >> 6;
+#pragma unroll
+            for (int nb = 0; nb < 2; ++nb) {
+                const uint64_t* arow = a.anc + ((int64_t)b * a.n_max + node_of[nb]) * a.W;
+                aw[nb][0] = arow[wbase];
+                aw[nb][1] = wbase + 1 < a.W ? arow[wbase + 1] : 0ull;
             }
         }
-        __syncthreads();
-
-        if (row0 < live_rows) {
 #pragma unroll
-            for (int blk = 0; blk < 2; ++blk) {
-                // ---- S^T for 64 keys: 4 key blocks of 16
-                floatx4 s[4];
+        for (int kb = 0; kb < kKeyTile / 32; ++kb) {
+            // ---- S^T (32 keys x 64 rows): A = K rows from LDS, B = Q fragments
+            floatx16 s[2];
 #pragma unroll
-                for (int kb = 0; kb < 4; ++kb) {
-                    floatx4 acc = {0.f, 0.f, 0.f, 0.f};
+            for (int nb = 0; nb < 2; ++nb)
 #pragma unroll
-                    for (int ks = 0; ks < KS; ++ks) {
-                        const uint4 u = *reinterpret_cast<const uint4*>(
-                            &sK[(kb * 16 + li) * KROW + ks * 32 + lg * 8]);
-                        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                            __builtin_bit_cast(bf16x8, u), qf[blk][ks], acc, 0, 0, 0);
-                    }
-                    s[kb] = acc;
-                }
-                // ---- scale, mask (end of sequence, tree ancestry), running max
-                const int n = node_of[blk];
-                const uint64_t* arow = a.anc + ((int64_t)b * a.n_max + min(n, a.n_max - 1)) * a.W;
+                for (int i = 0; i < 16; ++i) s[nb][i] = 0.f;
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks) {
+                const uint4 u = *reinterpret_cast<const uint4*>(
+                    &sK[(kb * 32 + l32) * KROW + ks * 16 + h * 8]);
+                const bf16x8 ka = __builtin_bit_cast(bf16x8, u);
+                s[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qf[0][ks], s[0], 0, 0, 0);
+                s[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qf[1][ks], s[1], 0, 0, 0);
+            }
+            // ---- online softmax; element i of lane holds key 8(i/4) + 4h + i%4 of the block
+            uint32_t pk[2][8];
+#pragma unroll
+            for (int nb = 0; nb < 2; ++nb) {
                 float mx = -INFINITY;
 #pragma unroll
-                for (int kb = 0; kb < 4; ++kb) {
-#pragma unroll
-                    for (int e = 0; e < 4; ++e) {
-                        const int j = t0 + kb * 16 + lg * 4 + e;
-                        bool vis = j < k_end;
-                        if (vis && j >= ctx) {
-                            const int m = j - ctx;
-                            vis = (arow[m >> 6] >> (m & 63)) & 1ull;
-                        }
-                        const float v = vis ? s[kb][e] * a.scale_log2 : -INFINITY;
-                        s[kb][e] = v;
-                        mx = fmaxf(mx, v);
+                for (int i = 0; i < 16; ++i) {
+                    float v = s[nb][i] * a.scale_log2;
+                    if (!plain) {
+                        // visible: inside the sequence, and a cached key or an ancestor
+                        const int j = t0 + kb * 32 + 8 * (i >> 2) + 4 * h + (i & 3);
+                        const int m = max(j - ctx, 0);
+                        const uint64_t wd = ((m >> 6) - wbase) == 0 ? aw[nb][0] : aw[nb][1];
+                        const bool anc_bit = (wd >> (m & 63)) & 1ull;
+                        const bool vis = (j < k_end) & ((j < ctx) | anc_bit);
+                        v = vis ? v : -INFINITY;
                     }
+                    s[nb][i] = v;
+                    mx = fmaxf(mx, v);
                 }
-                mx = fmaxf(mx, __shfl_xor(mx, 16, kWave));
-                mx = fmaxf(mx, __shfl_xor(mx, 32, kWave));
-                const float m_new = fmaxf(m_run[blk], mx);
+                {
+                    const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(mx),
+                                                                     __float_as_uint(mx), false, false);
+                    mx = fmaxf(mx, __uint_as_float(h == 0 ? sw[1] : sw[0]));
+                }
+                const float m_new = fmaxf(m_run[nb], mx);
                 const float m_use = m_new == -INFINITY ? 0.f : m_new;
-                const float alpha = exp2f(m_run[blk] - m_use);
-                m_run[blk] = m_new;
+                const float alpha = __builtin_amdgcn_exp2f(m_run[nb] - m_use);
+                m_run[nb] = m_new;
                 float ls = 0.f;
-                uint32_t pk[4][2];
 #pragma unroll
-                for (int kb = 0; kb < 4; ++kb) {
-                    float p[4];
-#pragma unroll
-                    for (int e = 0; e < 4; ++e) {
-                        p[e] = exp2f(s[kb][e] - m_use);
-                        ls += p[e];
-                    }
-                    pk[kb][0] = (uint32_t)__builtin_bit_cast(uint16_t, (__bf16)p[0]) |
-                                ((uint32_t)__builtin_bit_cast(uint16_t, (__bf16)p[1]) << 16);
-                    pk[kb][1] = (uint32_t)__builtin_bit_cast(uint16_t, (__bf16)p[2]) |
-                                ((uint32_t)__builtin_bit_cast(uint16_t, (__bf16)p[3]) << 16);
+                for (int i = 0; i < 16; i += 2) {
+                    const float p0 = __builtin_amdgcn_exp2f(s[nb][i] - m_use);
+                    const float p1 = __builtin_amdgcn_exp2f(s[nb][i + 1] - m_use);
+                    ls += p0 + p1;
+                    pk[nb][i >> 1] = (uint32_t)__builtin_bit_cast(uint16_t, (__bf16)p0) |
+                                     ((uint32_t)__builtin_bit_cast(uint16_t, (__bf16)p1) << 16);
                 }
-                l_run[blk] = l_run[blk] * alpha + ls;
+                l_run[nb] = l_run[nb] * alpha + ls;
+                if (__ballot(alpha != 1.f)) {
 #pragma unroll
-                for (int db = 0; db < DB; ++db) o[blk][db] *= alpha;
-                // ---- O^T += V^T P^T over two 32-key steps
+                    for (int db = 0; db < DB; ++db) o[nb][db] *= alpha;
+                }
+            }
+            // ---- O^T += V^T P^T over two 16-key steps; V^T fragments by transposed LDS reads
 #pragma unroll
-                for (int st = 0; st < 2; ++st) {
-                    const uint4 pb = make_uint4(pk[2 * st][0], pk[2 * st][1], pk[2 * st + 1][0],
-                                                pk[2 * st + 1][1]);
-                    const bf16x8 bop = __builtin_bit_cast(bf16x8, pb);
+            for (int st = 0; st < 2; ++st) {
+                bf16x8 pb[2];
 #pragma unroll
-                    for (int db = 0; db < DB; ++db) {
-                        const uint16_t* vrow = &sV[(db * 16 + li) * VROW + st * 32 + lg * 4];
-                        const uint2 lo = *reinterpret_cast<const uint2*>(vrow);
-                        const uint2 hi = *reinterpret_cast<const uint2*>(vrow + 16);
-                        const uint4 av = make_uint4(lo.x, lo.y, hi.x, hi.y);
-                        o[blk][db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                            __builtin_bit_cast(bf16x8, av), bop, o[blk][db], 0, 0, 0);
-                    }
+                for (int nb = 0; nb < 2; ++nb)
+                    pb[nb] = __builtin_bit_cast(
+                        bf16x8, make_uint4(pk[nb][4 * st], pk[nb][4 * st + 1], pk[nb][4 * st + 2],
+                                           pk[nb][4 * st + 3]));
+                const int kbase = kb * 32 + st * 16 + 4 * h;
+                const int t16 = lane & 15, dhalf = (lane >> 4) & 1;
+#pragma unroll
+                for (int db = 0; db < DB; ++db) {
+                    const int d0 = db * 32 + dhalf * 16;
+                    const uint16_t* v0 = &sV[(kbase + (t16 >> 2)) * VROW + d0 + 4 * (t16 & 3)];
+                    const short4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                        (__attribute__((address_space(3))) short4_t*)(v0));
+                    const short4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                        (__attribute__((address_space(3))) short4_t*)(v0 + 8 * VROW));
+                    const bf16x8 va = __builtin_bit_cast(
+                        bf16x8, make_uint4(__builtin_bit_cast(uint2, lo).x, __builtin_bit_cast(uint2, lo).y,
+                                           __builtin_bit_cast(uint2, hi).x, __builtin_bit_cast(uint2, hi).y));
+                    o[0][db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pb[0], o[0][db], 0, 0, 0);
+                    o[1][db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pb[1], o[1][db], 0, 0, 0);
                 }
             }
         }
-        __syncthreads();
     }
 
-    // ---- epilogue
+    // ---- epilogue: lane holds row l32 of each block, d = db*32 + 8(i/4) + 4h + i%4
 #pragma unroll
-    for (int blk = 0; blk < 2; ++blk) {
-        float l = l_run[blk];
-        l += __shfl_xor(l, 16, kWave);
-        l += __shfl_xor(l, 32, kWave);
-        const int rho = row0 + blk * 16 + li;
-        if (rho >= a.G * a.n_max) continue;
+    for (int nb = 0; nb < 2; ++nb) {
+        float l = l_run[nb];
+        {
+            const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(l), __float_as_uint(l),
+                                                             false, false);
+            l += __uint_as_float(h == 0 ? sw[1] : sw[0]);
+        }
+        const int rho = rbase + nb * 32 + l32;
+        if (rho >= all_rows) continue;
         const int n = rho / a.G, hh = rho - n * a.G;
         if (a.splits == 1) {
             uint16_t* op = a.out + (((int64_t)b * a.n_max + n) * a.hq + g * a.G + hh) * D;
-            const bool live = rho < live_rows;
-            const float inv = live && l > 0.f ? 1.f / l : 0.f;
+            const float inv = (rho < live_rows && l > 0.f) ? 1.f / l : 0.f;
 #pragma unroll
-            for (int db = 0; db < DB; ++db) {
-                const floatx4 v = o[blk][db] * inv;
-                uint2 w;
-                w.x = (uint32_t)f_to_bf16(v[0]) | ((uint32_t)f_to_bf16(v[1]) << 16);
-                w.y = (uint32_t)f_to_bf16(v[2]) | ((uint32_t)f_to_bf16(v[3]) << 16);
-                *reinterpret_cast<uint2*>(op + db * 16 + lg * 4) = w;
-            }
+            for (int db = 0; db < DB; ++db)
+#pragma unroll
+                for (int q4 = 0; q4 < 4; ++q4) {
+                    const int dd = db * 32 + 8 * q4 + 4 * h;
+                    uint2 w;
+                    w.x = (uint32_t)f_to_bf16(o[nb][db][4 * q4] * inv) |
+                          ((uint32_t)f_to_bf16(o[nb][db][4 * q4 + 1] * inv) << 16);
+                    w.y = (uint32_t)f_to_bf16(o[nb][db][4 * q4 + 2] * inv) |
+                          ((uint32_t)f_to_bf16(o[nb][db][4 * q4 + 3] * inv) << 16);
+                    *reinterpret_cast<uint2*>(op + dd) = w;
+                }
         } else {
             float* pp = a.part + ((((int64_t)b * a.hkv + g) * a.rows_pad + rho) * a.splits + split) * (D + 2);
 #pragma unroll
             for (int db = 0; db < DB; ++db)
-                *reinterpret_cast<floatx4*>(pp + db * 16 + lg * 4) = o[blk][db];
-            if (lg == 0) {
-                pp[D] = m_run[blk];
+#pragma unroll
+                for (int q4 = 0; q4 < 4; ++q4) {
+                    const int dd = db * 32 + 8 * q4 + 4 * h;
+                    *reinterpret_cast<float4*>(pp + dd) =
+                        make_float4(o[nb][db][4 * q4], o[nb][db][4 * q4 + 1], o[nb][db][4 * q4 + 2],
+                                    o[nb][db][4 * q4 + 3]);
+                }
+            if (h == 0) {
+                pp[D] = m_run[nb];
                 pp[D + 1] = l;
             }
         }
     }
 }
 
-// Merge of the split partials: one thread per (row, 4 output dims).
+// Merge of the split partials: one wave per query row; lanes first read the
+// splits' (max, sum), then each lane combines its D/64 output dimensions.
 template <int D>
 __global__ __launch_bounds__(256) void tree_attn_merge_kernel(AttnArgs a) {
-    const int64_t gid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    constexpr int Q = D / 4;
+    constexpr int PER = D / kWave;  // output dims per lane
+    const int lane = lane_id();
+    const int64_t r = (int64_t)blockIdx.x * (blockDim.x / kWave) + threadIdx.x / kWave;
     const int64_t rows = (int64_t)a.batch * a.hkv * a.G * a.n_max;
-    if (gid >= rows * Q) return;
-    const int q4 = (int)(gid % Q);
-    const int64_t r = gid / Q;
+    if (r >= rows) return;
     const int rho = (int)(r % (a.G * a.n_max));
     const int g = (int)((r / (a.G * a.n_max)) % a.hkv);
     const int b = (int)(r / ((int64_t)a.G * a.n_max * a.hkv));
     const int n = rho / a.G, hh = rho - n * a.G;
     const int nn = clamp_nodes(a.n_nodes[b], a.n_max);
-    uint16_t* op = a.out + (((int64_t)b * a.n_max + n) * a.hq + g * a.G + hh) * D + q4 * 4;
-    float acc[4] = {0.f, 0.f, 0.f, 0.f};
+    uint16_t* op = a.out + (((int64_t)b * a.n_max + n) * a.hq + g * a.G + hh) * D + lane * PER;
+    float acc[PER];
+#pragma unroll
+    for (int e = 0; e < PER; ++e) acc[e] = 0.f;
     if (rho < a.G * nn) {
         const int keys = a.ctx_off[b + 1] - a.ctx_off[b] + nn;
         const int nsplit = min(a.splits, (keys + a.split_len - 1) / a.split_len);
         const float* pp = a.part + (((int64_t)b * a.hkv + g) * a.rows_pad + rho) * a.splits * (D + 2);
-        float M = -INFINITY;
-        for (int s = 0; s < nsplit; ++s) M = fmaxf(M, pp[s * (D + 2) + D]);
-        float L = 0.f;
+        float ms = -INFINITY, ls = 0.f;
+        for (int s = lane; s < nsplit; s += kWave) {
+            ms = fmaxf(ms, pp[s * (D + 2) + D]);
+        }
+        const float M = wave_max_f32_dpp(ms);
+        float wl = 0.f;  // this lane's split weight (lane s holds split s, s < 64)
+        for (int s = lane; s < nsplit; s += kWave) {
+            const float m = pp[s * (D + 2) + D];
+            const float w = m == -INFINITY ? 0.f : exp2f(m - M);
+            ls += w * pp[s * (D + 2) + D + 1];
+            if (s < kWave) wl = w;
+        }
+        const float L = wave_sum_f32_dpp(ls);
         for (int s = 0; s < nsplit; ++s) {
             const float* ps = pp + s * (D + 2);
-            const float w = ps[D] == -INFINITY ? 0.f : exp2f(ps[D] - M);
-            L += w * ps[D + 1];
-            const floatx4 v = *reinterpret_cast<const floatx4*>(ps + q4 * 4);
+            const float m = ps[D];
+            const float w = s < kWave ? __int_as_float(__builtin_amdgcn_readlane(__float_as_int(wl), s))
+                                      : (m == -INFINITY ? 0.f : exp2f(m - M));
 #pragma unroll
-            for (int e = 0; e < 4; ++e) acc[e] += w * v[e];
+            for (int e = 0; e < PER; ++e) acc[e] += w * ps[lane * PER + e];
         }
         const float inv = L > 0.f ? 1.f / L : 0.f;
 #pragma unroll
-        for (int e = 0; e < 4; ++e) acc[e] *= inv;
+        for (int e = 0; e < PER; ++e) acc[e] *= inv;
     }
-    uint2 w;
-    w.x = (uint32_t)f_to_bf16(acc[0]) | ((uint32_t)f_to_bf16(acc[1]) << 16);
-    w.y = (uint32_t)f_to_bf16(acc[2]) | ((uint32_t)f_to_bf16(acc[3]) << 16);
-    *reinterpret_cast<uint2*>(op) = w;
+    if constexpr (PER == 1) {
+        *op = f_to_bf16(acc[0]);
+    } else {
+        static_assert(PER == 2, "head_dim 64 or 128");
+        *reinterpret_cast<uint32_t*>(op) =
+            (uint32_t)f_to_bf16(acc[0]) | ((uint32_t)f_to_bf16(acc[1]) << 16);
+    }
 }
 
 // fp32 path: one wave per (b, n, h) row, plain fp32 arithmetic.  Each lane
@@ -394,15 +459,14 @@ static AttnPlan attn_plan(const presto_attn_desc* d) {
     AttnPlan p;
     p.G = d->hq / d->hkv;
     p.rows = p.G * d->n_max;
-    p.row_tiles = (p.rows + kMaxRowsPerTile - 1) / kMaxRowsPerTile;
-    const int per = (p.rows + p.row_tiles - 1) / p.row_tiles;
-    p.rows_per_tile = (per + kRowsPerWave - 1) / kRowsPerWave * kRowsPerWave;
-    p.waves = p.rows_per_tile / kRowsPerWave;
+    p.row_tiles = (p.rows + kRowsPerTile - 1) / kRowsPerTile;
+    p.rows_per_tile = kRowsPerTile;
+    p.waves = kAttnWaves;
     p.rows_pad = p.rows_per_tile * p.row_tiles;
     const int64_t base = (int64_t)d->batch * d->hkv * p.row_tiles;
     const int keys = d->max_ctx + d->n_max;
     const int max_splits = (keys + 255) / 256;
-    int splits = (int)((512 + base - 1) / base);
+    int splits = (int)((384 + base - 1) / base);
     splits = splits < 1 ? 1 : (splits > max_splits ? max_splits : splits);
     int len = (keys + splits - 1) / splits;
     len = (len + kKeyTile - 1) / kKeyTile * kKeyTile;
@@ -455,22 +519,21 @@ presto_status launch_tree_attention(const presto_attn_desc* d, const void* q, co
     a.G = p.G;
     a.W = (d->n_max + 63) / 64;
     a.row_tiles = p.row_tiles;
-    a.rows_per_tile = p.rows_per_tile;
     a.rows_pad = p.rows_pad;
     a.splits = p.splits;
     a.split_len = p.split_len;
     a.n_tasks = (int32_t)p.tasks;
     a.n_blocks = (int32_t)p.blocks;
     a.scale_log2 = d->scale * kLog2e;
-    const dim3 block(p.waves * kWave);
+    const dim3 block(kAttnThreads);
     if (d->head_dim == 64)
         tree_attn_bf16_kernel<64><<<(unsigned)p.blocks, block, 0, stream>>>(a);
     else
         tree_attn_bf16_kernel<128><<<(unsigned)p.blocks, block, 0, stream>>>(a);
     presto_status st = check_launch("tree_attn_bf16_kernel");
     if (st != PRESTO_OK || p.splits == 1) return st;
-    const int64_t threads = (int64_t)d->batch * d->hkv * p.G * d->n_max * (d->head_dim / 4);
-    const unsigned grid = (unsigned)((threads + 255) / 256);
+    const int64_t merge_rows = (int64_t)d->batch * d->hkv * p.G * d->n_max;
+    const unsigned grid = (unsigned)((merge_rows + 3) / 4);
     if (d->head_dim == 64)
         tree_attn_merge_kernel<64><<<grid, 256, 0, stream>>>(a);
     else

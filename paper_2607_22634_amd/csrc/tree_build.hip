@@ -1,10 +1,14 @@
 // Stage 2: prefix-aligned scoring and best-first tree construction.
 //
 // One wavefront builds one sequence's tree; the batch runs in parallel.
-// The candidate table (log q, token ids), lambda, the trigram lattice (when
-// it fits), the per-node child tables and the ancestor bitmask rows live in
-// LDS.  The frontier lives in registers, spread over the 64 lanes (SL slots
-// per lane), so a pop is a per-lane scan plus one wave-wide max.
+// LDS holds the candidate table (log q, token ids), the trigram lattice when
+// it fits, and per committed node one 8-byte record (parent, rank, depth, S)
+// plus the scores of its children.  The frontier lives in registers spread
+// over the 64 lanes (SL slots per lane), each slot only (S, packed
+// metadata): a pop is a per-lane max, one DPP wave max and a ballot.  Rank
+// path keys are rebuilt from the parent records only when several frontier
+// entries share the best S; token ids, the output rows and the ancestor
+// bitmasks are produced after the search, in parallel over the nodes.
 //
 // Frontier policy.  Committing nodes in pop order yields the B best prefixes
 // under the total order (S desc, rank path asc).  Instead of pushing all of
@@ -25,7 +29,7 @@
 namespace presto {
 
 struct TreeArgs {
-    int32_t D, k, branch, budget, N, W, wbits;
+    int32_t D, k, branch, budget, N, W, wbits, per_word;
     const int32_t* ids;
     const float* logprob;
     const float* log_rho;
@@ -40,94 +44,22 @@ struct TreeArgs {
     uint64_t* anc;
     bool rho_in_lds;
     // LDS byte offsets
-    int o_lp, o_ids, o_lam, o_rho, o_dep, o_rank, o_prank, o_crank, o_cs, o_anc;
+    int o_lp, o_ids, o_cord, o_rec, o_rho;
 };
 
-// 128-bit rank-path key as (hi, lo); digit (rank + 1) of depth d (1-based)
-// sits wbits wide at bit 128 - d * wbits, so a prefix sorts before its
-// extensions and siblings sort by rank.
-__device__ __forceinline__ void key_set_digit(uint64_t& hi, uint64_t& lo, int d, int wbits,
-                                              uint32_t digit) {
-    const int shift = 128 - d * wbits;
-    const uint64_t mask = (1ull << wbits) - 1ull;
-    if (shift >= 64) {
-        hi = (hi & ~(mask << (shift - 64))) | ((uint64_t)digit << (shift - 64));
-    } else {
-        lo = (lo & ~(mask << shift)) | ((uint64_t)digit << shift);
-        if (shift + wbits > 64) {
-            const int up = 64 - shift;  // bits of the digit that spill into hi
-            hi = (hi & ~(mask >> up)) | ((uint64_t)digit >> up);
-        }
-    }
+// Frontier metadata in one word: parent node (10 bits), candidate rank (4),
+// depth (6), rank of the parent (4).
+__device__ __forceinline__ uint32_t pack_meta(int p, int r, int d, int rp) {
+    return (uint32_t)p | ((uint32_t)r << 10) | ((uint32_t)d << 14) | ((uint32_t)rp << 20);
 }
 
-__device__ __forceinline__ bool entry_before(uint32_t sa, uint64_t ha, uint64_t la, uint32_t sb,
-                                             uint64_t hb, uint64_t lb) {
-    if (sa != sb) return sa > sb;
-    if (ha != hb) return ha < hb;
-    return la < lb;
-}
-
-__device__ __forceinline__ uint64_t wave_min_u64(uint64_t v) {
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) {
-        const uint64_t w = shfl_xor_u64(v, o);
-        v = w < v ? w : v;
-    }
-    return v;
-}
-
-__device__ __forceinline__ float rd_f(float x, int lane) {
-    return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), lane));
-}
-
-// Child table of node n (depth d, own rank rn, parent's rank rp, score Sn):
-// the top-`branch` candidates by token score, stored in the order in which
-// the best-first search will commit them (child S desc, rank asc).
-__device__ __forceinline__ void expand_node(const TreeArgs& a, char* lds, int n, int d, int rn,
-                                            int rp, float Sn) {
-    const int lane = lane_id();
-    const float* s_lp = reinterpret_cast<const float*>(lds + a.o_lp);
-    const float* s_lam = reinterpret_cast<const float*>(lds + a.o_lam);
-    uint8_t* s_crank = reinterpret_cast<uint8_t*>(lds + a.o_crank);
-    float* s_cs = reinterpret_cast<float*>(lds + a.o_cs);
-    const int k = a.k, row = d;
-    const int ctx2 = d >= 2 ? rp : 0;  // grandparent slot of the trigram
-    const int ctx1 = d >= 1 ? rn : 0;  // parent slot of the trigram
-    float s = -INFINITY;
-    if (lane < k) {
-        const float lq = s_lp[row * k + lane];
-        if (a.log_rho) {
-            const int64_t ri = (((int64_t)row * k + ctx2) * k + ctx1) * k + lane;
-            const float lr = a.rho_in_lds ? reinterpret_cast<const float*>(lds + a.o_rho)[ri]
-                                          : a.log_rho[ri];
-            const float t = s_lam[row] * lr;
-            s = lq + t;
-        } else {
-            s = lq;
-        }
-        s = (s == s) ? s : -INFINITY;
-    }
-    // selection by token score: larger s first, lower rank on ties
-    int sel = 0;
-    for (int j = 0; j < k; ++j) {
-        const float sj = rd_f(s, j);
-        sel += (sj > s || (sj == s && j < lane)) ? 1 : 0;
-    }
-    const bool in_set = lane < k && sel < a.branch;
-    const float sc = Sn + s;
-    // commit order among the chosen children: child S desc, rank asc
-    int pos = 0;
-    for (int j = 0; j < k; ++j) {
-        const float cj = rd_f(sc, j);
-        const int selj = __builtin_amdgcn_readlane(sel, j);
-        if (selj < a.branch) pos += (cj > sc || (cj == sc && j < lane)) ? 1 : 0;
-    }
-    if (in_set) {
-        s_crank[n * a.branch + pos] = (uint8_t)lane;
-        s_cs[n * a.branch + pos] = sc;
-    }
-    __builtin_amdgcn_wave_barrier();
+// u32 max over lanes 0..15 (row 0), returned to every lane.
+__device__ __forceinline__ uint32_t row0_max_u32_dpp(uint32_t v) {
+    v = max(v, dpp_u32<0xb1>(0u, v));
+    v = max(v, dpp_u32<0x4e>(0u, v));
+    v = max(v, dpp_u32<0x114>(0u, v));
+    v = max(v, dpp_u32<0x118>(0u, v));
+    return (uint32_t)__builtin_amdgcn_readlane((int)v, 15);
 }
 
 template <int SL>
@@ -135,16 +67,14 @@ __global__ __launch_bounds__(kWave) void tree_build_kernel(TreeArgs a) {
     extern __shared__ __align__(16) char lds[];
     const int lane = lane_id();
     const int b = blockIdx.x;
-    const int D = a.D, k = a.k, N = a.N, W = a.W;
+    const int D = a.D, k = a.k, N = a.N, W = a.W, wbits = a.wbits, per_word = a.per_word;
     float* s_lp = reinterpret_cast<float*>(lds + a.o_lp);
     int32_t* s_ids = reinterpret_cast<int32_t*>(lds + a.o_ids);
-    float* s_lam = reinterpret_cast<float*>(lds + a.o_lam);
-    int32_t* s_dep = reinterpret_cast<int32_t*>(lds + a.o_dep);
-    int32_t* s_rank = reinterpret_cast<int32_t*>(lds + a.o_rank);
-    int32_t* s_prank = reinterpret_cast<int32_t*>(lds + a.o_prank);
-    const uint8_t* s_crank = reinterpret_cast<const uint8_t*>(lds + a.o_crank);
-    const float* s_cs = reinterpret_cast<const float*>(lds + a.o_cs);
-    uint64_t* s_anc = reinterpret_cast<uint64_t*>(lds + a.o_anc);
+    uint32_t* s_cord = reinterpret_cast<uint32_t*>(lds + a.o_cord);  // [N][k] ord(child S) or 0
+    uint2* s_rec = reinterpret_cast<uint2*>(lds + a.o_rec);          // [N] (meta, S bits)
+    float* s_rho = reinterpret_cast<float*>(lds + a.o_rho);
+    const int rho_n = D * k * k * k;
+    const float* g_rho = a.log_rho ? a.log_rho + (int64_t)b * rho_n : nullptr;
 
     // stage the candidate table of this sequence
     const int64_t tb = (int64_t)b * D * k;
@@ -152,176 +82,219 @@ __global__ __launch_bounds__(kWave) void tree_build_kernel(TreeArgs a) {
         s_lp[i] = a.logprob[tb + i];
         s_ids[i] = a.ids[tb + i];
     }
-    for (int i = lane; i < D; i += kWave) s_lam[i] = a.lambda[i];
-    if (a.log_rho && a.rho_in_lds) {
-        float* s_rho = reinterpret_cast<float*>(lds + a.o_rho);
-        const int64_t rn = (int64_t)D * k * k * k;
-        const float* src = a.log_rho + (int64_t)b * rn;
-        for (int64_t i = lane; i < rn; i += kWave) s_rho[i] = src[i];
-    }
-    for (int i = lane; i < N * W; i += kWave) s_anc[i] = 0ull;
+    if (g_rho && a.rho_in_lds)
+        for (int i = lane; i < rho_n; i += kWave) s_rho[i] = g_rho[i];
+    const float lam_lane = lane < D ? a.lambda[lane] : 0.f;  // lambda_d held by lane d
     __builtin_amdgcn_wave_barrier();
 
-    int32_t* o_par = a.parent + (int64_t)b * N;
-    int32_t* o_tok = a.token + (int64_t)b * N;
-    int32_t* o_dep = a.depth + (int64_t)b * N;
-    int32_t* o_rank = a.rank + (int64_t)b * N;
-    float* o_score = a.score + (int64_t)b * N;
-    uint64_t* o_anc = a.anc + (int64_t)b * N * W;
+    // Child scores of node n (depth d, own rank rn, parent's rank rp, score Sn):
+    // ord(S) of its top-`branch` candidates stored in LDS (0 for the others);
+    // returns the first child in commit order as (ord S, rank), ord 0 if none.
+    auto expand = [&](int n, int d, int rn, int rp, float Sn, uint32_t& c_ord, int& c_rank) {
+        const int ctx2 = d >= 2 ? rp : 0;  // grandparent slot of the trigram
+        const int ctx1 = d >= 1 ? rn : 0;  // parent slot of the trigram
+        const float lam_d = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(lam_lane), d));
+        float s = -INFINITY;
+        if (lane < k) {
+            const float lq = s_lp[d * k + lane];
+            if (g_rho) {
+                const int ri = ((d * k + ctx2) * k + ctx1) * k + lane;
+                float lr;
+                if (a.rho_in_lds)
+                    lr = s_rho[ri];
+                else
+                    lr = g_rho[ri];
+                const float t = lam_d * lr;
+                s = lq + t;
+            } else {
+                s = lq;
+            }
+            s = (s == s) ? s : -INFINITY;
+        }
+        bool in = lane < k;
+        if (a.branch < k) {
+            // keep the top-`branch` by token score (larger s, then lower rank)
+            int sel = 0;
+            for (int j = 0; j < k; ++j) {
+                const float sj = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(s), j));
+                sel += (sj > s || (sj == s && j < lane)) ? 1 : 0;
+            }
+            in = in && sel < a.branch;
+        }
+        const float sc = Sn + s;
+        const uint32_t o = in ? ord32(sc) : 0u;
+        if (lane < k) s_cord[n * k + lane] = o;
+        c_ord = row0_max_u32_dpp(o);
+        c_rank = __ffsll((unsigned long long)__ballot(in && o == c_ord)) - 1;
+    };
 
-    // root
-    if (lane == 0) {
-        s_dep[0] = 0;
-        s_rank[0] = 0;
-        s_prank[0] = 0;
-        s_anc[0] = 1ull;
-        o_par[0] = -1;
-        o_tok[0] = a.root_token[b];
-        o_dep[0] = 0;
-        o_rank[0] = -1;
-        o_score[0] = 0.f;
-    }
-    for (int w = lane; w < W; w += kWave) o_anc[w] = w == 0 ? 1ull : 0ull;
-    __builtin_amdgcn_wave_barrier();
-    expand_node(a, lds, 0, 0, 0, 0, 0.f);
+    // Rank-path key (four 32-bit words, most significant first) of the child
+    // of committed node p with candidate rank r at depth d.
+    auto child_key = [&](int p, int r, int d, uint32_t (&kw)[4]) {
+        kw[0] = kw[1] = kw[2] = kw[3] = 0u;
+        int x = p, dx = d, rx = r;
+        while (dx > 0) {
+            const int wi = (dx - 1) / per_word, sh = 32 - ((dx - 1) % per_word + 1) * wbits;
+#pragma unroll
+            for (int q = 0; q < 4; ++q) kw[q] |= q == wi ? (uint32_t)(rx + 1) << sh : 0u;
+            if (x == 0) break;
+            const uint32_t m = s_rec[x].x;
+            rx = (m >> 10) & 15;
+            dx = (m >> 14) & 63;
+            x = m & 1023;
+        }
+    };
+
+    if (lane == 0) s_rec[0] = make_uint2(0xffffffffu, __float_as_uint(0.f));
+    uint32_t c_ord;
+    int c_rank;
+    expand(0, 0, 0, 0, 0.f, c_ord, c_rank);
 
     // frontier slots: slot j of lane l is entry j * 64 + l
-    uint32_t fS[SL];
-    uint64_t fH[SL], fL[SL];
-    int32_t fP[SL], fO[SL];
+    uint32_t fS[SL], fM[SL];
 #pragma unroll
-    for (int j = 0; j < SL; ++j) {
-        fS[j] = 0u;
-        fH[j] = fL[j] = 0ull;
-        fP[j] = fO[j] = 0;
+    for (int j = 0; j < SL; ++j) fS[j] = fM[j] = 0u;
+    if (lane == 0) {
+        fS[0] = c_ord;
+        fM[0] = pack_meta(0, c_rank, 1, 0);
     }
-    if (lane == 0 && D > 0) {
-        uint64_t h = 0, l = 0;
-        key_set_digit(h, l, 1, a.wbits, (uint32_t)s_crank[0] + 1u);
-        fS[0] = ord32(s_cs[0]);
-        fH[0] = h;
-        fL[0] = l;
-        fP[0] = 0;
-        fO[0] = 0;
-    }
-    int fcount = 1;
-    int committed = 1;
+    int fcount = 1, committed = 1;
 
     while (committed - 1 < a.budget) {
-        // best entry of this lane
-        uint32_t bS = 0u;
-        uint64_t bH = ~0ull, bL = ~0ull;
-        int bP = 0, bO = 0, bSlot = 0;
+        uint32_t lm = 0u;
 #pragma unroll
-        for (int j = 0; j < SL; ++j) {
-            if (fS[j] != 0u && entry_before(fS[j], fH[j], fL[j], bS, bH, bL)) {
-                bS = fS[j];
-                bH = fH[j];
-                bL = fL[j];
-                bP = fP[j];
-                bO = fO[j];
-                bSlot = j;
-            }
+        for (int j = 0; j < SL; ++j) lm = max(lm, fS[j]);
+        const uint32_t M = wave_max_u32_dpp(lm);
+        if (M == 0u) break;  // frontier exhausted: the whole candidate tree is committed
+
+        // winner: the unique entry holding M, else the one with the smallest path key
+        int cnt = 0, jsel = 0;
+#pragma unroll
+        for (int j = SL - 1; j >= 0; --j) {
+            const bool hit = fS[j] == M;
+            cnt += hit ? 1 : 0;
+            jsel = hit ? j : jsel;
         }
-        const uint32_t mS = wave_max_u32(bS);
-        if (mS == 0u) break;  // frontier exhausted: the whole candidate tree is committed
-        uint64_t tied = __ballot(bS == mS);
+        const uint64_t any = __ballot(cnt > 0);
         int w;
-        if (__popcll(tied) == 1) {
-            w = __ffsll((unsigned long long)tied) - 1;
+        if (__popcll(any) == 1 && __ballot(cnt > 1) == 0ull) {
+            w = __ffsll((unsigned long long)any) - 1;
         } else {
-            const bool t1 = bS == mS;
-            const uint64_t mh = wave_min_u64(t1 ? bH : ~0ull);
-            const bool t2 = t1 && bH == mh;
-            const uint64_t ml = wave_min_u64(t2 ? bL : ~0ull);
-            w = __ffsll((unsigned long long)__ballot(t2 && bL == ml)) - 1;
-        }
-        const uint64_t eH = ((uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)(bH >> 32), w) << 32) |
-                            (uint32_t)__builtin_amdgcn_readlane((int)bH, w);
-        const uint64_t eL = ((uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)(bL >> 32), w) << 32) |
-                            (uint32_t)__builtin_amdgcn_readlane((int)bL, w);
-        const int p = __builtin_amdgcn_readlane(bP, w);
-        const int o = __builtin_amdgcn_readlane(bO, w);
-        const int eslot = __builtin_amdgcn_readlane(bSlot, w);
-
-        // commit node n
-        const int n = committed;
-        const int r = s_crank[p * a.branch + o];
-        const int d = s_dep[p] + 1;
-        const float S = s_cs[p * a.branch + o];
-        const int rp = s_rank[p];
-        if (lane == 0) {
-            s_dep[n] = d;
-            s_rank[n] = r;
-            s_prank[n] = rp;
-            o_par[n] = p;
-            o_tok[n] = s_ids[(d - 1) * k + r];
-            o_dep[n] = d;
-            o_rank[n] = r;
-            o_score[n] = S;
-        }
-        for (int ww = lane; ww < W; ww += kWave) {
-            uint64_t word = s_anc[p * W + ww];
-            if (ww == (n >> 6)) word |= 1ull << (n & 63);
-            s_anc[n * W + ww] = word;
-            o_anc[(int64_t)n * W + ww] = word;
-        }
-        ++committed;
-        __builtin_amdgcn_wave_barrier();
-
-        // pushes: the first child of n, then the next sibling of n
-        bool has_child = d < D;
-        if (has_child) expand_node(a, lds, n, d, r, rp, S);
-        const bool has_sib = o + 1 < a.branch;
-        uint32_t cS = 0u, sS = 0u;
-        uint64_t cH = eH, cL = eL, sH = eH, sL = eL;
-        if (has_child) {
-            cS = ord32(s_cs[n * a.branch]);
-            key_set_digit(cH, cL, d + 1, a.wbits, (uint32_t)s_crank[n * a.branch] + 1u);
-        }
-        if (has_sib) {
-            sS = ord32(s_cs[p * a.branch + o + 1]);
-            key_set_digit(sH, sL, d, a.wbits, (uint32_t)s_crank[p * a.branch + o + 1] + 1u);
-        }
-        // first push reuses the popped slot, the second takes a fresh slot
-        uint32_t xS = 0u;
-        uint64_t xH = 0, xL = 0;
-        int xP = 0, xO = 0;
-        bool second = false;
-        uint32_t yS = 0u;
-        uint64_t yH = 0, yL = 0;
-        int yP = 0, yO = 0;
-        if (has_child) {
-            xS = cS; xH = cH; xL = cL; xP = n; xO = 0;
-            if (has_sib) {
-                second = true;
-                yS = sS; yH = sH; yL = sL; yP = p; yO = o + 1;
+            uint32_t bk[4] = {~0u, ~0u, ~0u, ~0u};
+            int bj = 0;
+            for (int j = 0; j < SL; ++j) {
+                if (fS[j] == M) {
+                    uint32_t kw[4];
+                    child_key(fM[j] & 1023, (fM[j] >> 10) & 15, (fM[j] >> 14) & 63, kw);
+                    const bool less =
+                        kw[0] != bk[0] ? kw[0] < bk[0]
+                                       : (kw[1] != bk[1] ? kw[1] < bk[1]
+                                                         : (kw[2] != bk[2] ? kw[2] < bk[2] : kw[3] < bk[3]));
+                    if (less) {
+                        bk[0] = kw[0]; bk[1] = kw[1]; bk[2] = kw[2]; bk[3] = kw[3];
+                        bj = j;
+                    }
+                }
             }
-        } else if (has_sib) {
-            xS = sS; xH = sH; xL = sL; xP = p; xO = o + 1;
+            bool t = cnt > 0;
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const uint32_t mq = wave_min_u32_dpp(t ? bk[q] : ~0u);
+                t = t && bk[q] == mq;
+            }
+            w = __ffsll((unsigned long long)__ballot(t)) - 1;
+            jsel = bj;
         }
+        uint32_t lmeta = 0u;
+#pragma unroll
+        for (int j = 0; j < SL; ++j) lmeta = j == jsel ? fM[j] : lmeta;
+        const uint32_t meta = (uint32_t)__builtin_amdgcn_readlane((int)lmeta, w);
+        const int eslot = __builtin_amdgcn_readlane(jsel, w);
+        const int p = meta & 1023, r = (meta >> 10) & 15, d = (meta >> 14) & 63, rp = (meta >> 20) & 15;
+        const float S = unord32(M);
+
+        // commit node n: one record; everything else is derived after the search
+        const int n = committed++;
+        if (lane == 0) s_rec[n] = make_uint2(meta, __float_as_uint(S));
+
+        // next sibling of n under p: the best child of p ordered after n
+        uint32_t o = 0u;
+        bool valid = false;
+        if (lane < k) {
+            o = s_cord[p * k + lane];
+            valid = o != 0u && (o < M || (o == M && lane > r));
+        }
+        // first child of n
+        uint32_t kid_ord = 0u;
+        int kid_rank = 0;
+        if (d < D) expand(n, d, r, rp, S, kid_ord, kid_rank);
+        const uint32_t sib_ord = row0_max_u32_dpp(valid ? o : 0u);
+        const int sib_rank = __ffsll((unsigned long long)__ballot(valid && o == sib_ord)) - 1;
+
+        // pushes: the first reuses the popped slot, the second takes a fresh slot
+        uint32_t xS = 0u, xM = 0u, yS = 0u, yM = 0u;
+        if (kid_ord != 0u) {
+            xS = kid_ord;
+            xM = pack_meta(n, kid_rank, d + 1, r);
+        }
+        if (sib_ord != 0u) {
+            const uint32_t m = pack_meta(p, sib_rank, d, rp);
+            if (xS != 0u) {
+                yS = sib_ord;
+                yM = m;
+            } else {
+                xS = sib_ord;
+                xM = m;
+            }
+        }
+        const bool second = yS != 0u;
         const int ylane = fcount & (kWave - 1), yslot = fcount >> 6;
 #pragma unroll
         for (int j = 0; j < SL; ++j) {
-            if (lane == w && j == eslot) {
-                fS[j] = xS; fH[j] = xH; fL[j] = xL; fP[j] = xP; fO[j] = xO;
-            }
-            if (second && lane == ylane && j == yslot) {
-                fS[j] = yS; fH[j] = yH; fL[j] = yL; fP[j] = yP; fO[j] = yO;
-            }
+            const bool px = lane == w && j == eslot;
+            const bool py = second && lane == ylane && j == yslot;
+            fS[j] = px ? xS : (py ? yS : fS[j]);
+            fM[j] = px ? xM : (py ? yM : fM[j]);
         }
         if (second) ++fcount;
     }
+    __builtin_amdgcn_wave_barrier();
 
-    // padding rows
-    for (int i = committed + lane; i < N; i += kWave) {
-        o_par[i] = -1;
-        o_tok[i] = -1;
-        o_dep[i] = -1;
-        o_rank[i] = -1;
-        o_score[i] = -INFINITY;
+    // Output rows and ancestor masks, one node per lane: the mask of node n has
+    // the bits of n and of every node on its parent chain (SL words suffice:
+    // SL = ceil(N / 64) = W).
+    const int64_t ob = (int64_t)b * N;
+    for (int i = lane; i < N; i += kWave) {
+        uint64_t words[SL];
+#pragma unroll
+        for (int q = 0; q < SL; ++q) words[q] = 0ull;
+        if (i < committed) {
+            const uint2 rec = s_rec[i];
+            const int p = i == 0 ? -1 : (int)(rec.x & 1023);
+            const int r = (rec.x >> 10) & 15, d = i == 0 ? 0 : (rec.x >> 14) & 63;
+            a.parent[ob + i] = p;
+            a.token[ob + i] = i == 0 ? a.root_token[b] : s_ids[(d - 1) * k + r];
+            a.depth[ob + i] = d;
+            a.rank[ob + i] = i == 0 ? -1 : r;
+            a.score[ob + i] = __uint_as_float(rec.y);
+            int x = i;
+            while (true) {
+#pragma unroll
+                for (int q = 0; q < SL; ++q) words[q] |= q == (x >> 6) ? 1ull << (x & 63) : 0ull;
+                if (x == 0) break;
+                x = (int)(s_rec[x].x & 1023);
+            }
+        } else {
+            a.parent[ob + i] = -1;
+            a.token[ob + i] = -1;
+            a.depth[ob + i] = -1;
+            a.rank[ob + i] = -1;
+            a.score[ob + i] = -INFINITY;
+        }
+#pragma unroll
+        for (int q = 0; q < SL; ++q)
+            if (q < W) a.anc[(ob + i) * W + q] = words[q];
     }
-    for (int64_t i = (int64_t)committed * W + lane; i < (int64_t)N * W; i += kWave) o_anc[i] = 0ull;
     if (lane == 0) a.n_nodes[b] = committed;
 }
 
@@ -335,22 +308,16 @@ static int align16(int x) { return (x + 15) & ~15; }
 
 struct TreeLayout {
     int total_no_rho, total_with_rho;
-    int o_lp, o_ids, o_lam, o_dep, o_rank, o_prank, o_crank, o_cs, o_anc, o_rho;
+    int o_lp, o_ids, o_cord, o_rec, o_rho;
 };
 
-static TreeLayout tree_layout(int D, int k, int branch, int N) {
+static TreeLayout tree_layout(int D, int k, int N) {
     TreeLayout L;
-    const int W = (N + 63) / 64;
     int off = 0;
     L.o_lp = off; off = align16(off + D * k * 4);
     L.o_ids = off; off = align16(off + D * k * 4);
-    L.o_lam = off; off = align16(off + D * 4);
-    L.o_dep = off; off = align16(off + N * 4);
-    L.o_rank = off; off = align16(off + N * 4);
-    L.o_prank = off; off = align16(off + N * 4);
-    L.o_crank = off; off = align16(off + N * branch);
-    L.o_cs = off; off = align16(off + N * branch * 4);
-    L.o_anc = off; off = align16(off + N * W * 8);
+    L.o_cord = off; off = align16(off + N * k * 4);
+    L.o_rec = off; off = align16(off + N * 8);
     L.total_no_rho = off;
     L.o_rho = off;
     L.total_with_rho = align16(off + D * k * k * k * 4);
@@ -359,8 +326,19 @@ static TreeLayout tree_layout(int D, int k, int branch, int N) {
 
 static constexpr int kTreeLdsBudget = 64 * 1024;
 
+int tree_key_bits(int k) {
+    int wbits = 1;
+    while ((1 << wbits) < k + 1) ++wbits;
+    return wbits;
+}
+
+// Deepest tree whose rank-path key fits four 32-bit words (digits never
+// straddle a word).
+int tree_max_depth(int k) { return 4 * (32 / tree_key_bits(k)); }
+
 bool tree_build_fits(int D, int k, int branch, int N) {
-    return tree_layout(D, k, branch, N).total_no_rho <= kTreeLdsBudget;
+    (void)branch;
+    return tree_layout(D, k, N).total_no_rho <= kTreeLdsBudget;
 }
 
 presto_status launch_build_tree(const presto_tree_desc* desc, const int32_t* ids,
@@ -375,9 +353,8 @@ presto_status launch_build_tree(const presto_tree_desc* desc, const int32_t* ids
     a.budget = desc->budget;
     a.N = desc->budget + 1;
     a.W = (a.N + 63) / 64;
-    int wbits = 1;
-    while ((1 << wbits) < a.k + 1) ++wbits;
-    a.wbits = wbits;
+    a.wbits = tree_key_bits(a.k);
+    a.per_word = 32 / a.wbits;
     a.ids = ids;
     a.logprob = logprob;
     a.log_rho = log_rho;
@@ -390,10 +367,9 @@ presto_status launch_build_tree(const presto_tree_desc* desc, const int32_t* ids
     a.rank = rank;
     a.score = score;
     a.anc = anc;
-    const TreeLayout L = tree_layout(a.D, a.k, a.branch, a.N);
-    a.o_lp = L.o_lp; a.o_ids = L.o_ids; a.o_lam = L.o_lam; a.o_dep = L.o_dep;
-    a.o_rank = L.o_rank; a.o_prank = L.o_prank; a.o_crank = L.o_crank; a.o_cs = L.o_cs;
-    a.o_anc = L.o_anc; a.o_rho = L.o_rho;
+    const TreeLayout L = tree_layout(a.D, a.k, a.N);
+    a.o_lp = L.o_lp; a.o_ids = L.o_ids; a.o_cord = L.o_cord; a.o_rec = L.o_rec;
+    a.o_rho = L.o_rho;
     a.rho_in_lds = log_rho != nullptr && L.total_with_rho <= kTreeLdsBudget;
     const int lds = a.rho_in_lds ? L.total_with_rho : L.total_no_rho;
     const int SL = (a.N + kWave - 1) / kWave;

@@ -89,9 +89,9 @@ def test_build_tree_unbuilt_modes_are_unsupported():
 
 
 def test_build_tree_path_key_limit():
-    d = P.TreeDesc(1, 32, 16, 16, 8, 0)  # 32 * 5 bits > 128
+    d = P.TreeDesc(1, 25, 16, 16, 8, 0)  # 5-bit digits: six per 32-bit word, 24 levels
     st, msg = _err(P.lib().presto_build_tree(ctypes.byref(d), *([None] * 13), 0, None))
-    assert st == P.PRESTO_ERR_INVALID_ARG and "128" in msg
+    assert st == P.PRESTO_ERR_INVALID_ARG and "24" in msg
 
 
 @pytest.mark.parametrize("field,value", [("head_dim", 96), ("hkv", 3), ("n_max", 0),

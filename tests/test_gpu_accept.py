@@ -102,3 +102,20 @@ def test_accept_nan_flag():
                     flags=flags)
     torch.cuda.synchronize()
     assert int(flags.item()) & P.PRESTO_FLAG_NAN_TARGET
+
+
+def test_accept_workspace_reuse_keeps_results():
+    w, rin = round_data(2)
+    ids, lp, _ = P.presto_topk(to_dev(rin["drafter_logits"], w.dtype), w.k)
+    t = P.presto_build_tree(ids, lp, to_dev(rin["rho"]), to_dev(rin["lam"]),
+                            to_dev(rin["root_token"]), w.depth, w.k, w.budget)
+    th = tree_to_host(t)
+    T = to_dev(sy.target_logits(w, rin["field"], th["parent"], th["rank"], th["n_nodes"]), w.dtype)
+    ws = torch.zeros(P.lib().presto_accept_workspace(w.batch, w.n_max, w.vocab), dtype=torch.uint8,
+                     device="cuda")
+    ref = {k: to_host(v) for k, v in P.presto_accept(T, t["parent"], t["token"], t["n_nodes"],
+                                                       w.depth, workspace=ws).items()}
+    for _ in range(3):
+        r = P.presto_accept(T, t["parent"], t["token"], t["n_nodes"], w.depth, workspace=ws)
+        for key in ref:
+            np.testing.assert_array_equal(to_host(r[key]), ref[key])

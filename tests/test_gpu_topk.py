@@ -94,3 +94,17 @@ def test_topk_is_deterministic():
     b = [to_host(x) for x in P.presto_topk(t, w.k)]
     for u, v in zip(a, b):
         np.testing.assert_array_equal(u, v)
+
+
+def test_topk_workspace_reuse_keeps_results():
+    """Counters in the workspace are re-armed by every call: reuse is safe."""
+    w, rin = round_data(3)
+    t = to_dev(rin["drafter_logits"], w.dtype)
+    rows = t.shape[0]
+    ws = torch.zeros(P.lib().presto_topk_workspace(rows, w.vocab, w.k), dtype=torch.uint8,
+                     device="cuda")
+    first = [to_host(x) for x in P.presto_topk(t, w.k, workspace=ws)]
+    for _ in range(3):
+        again = [to_host(x) for x in P.presto_topk(t, w.k, workspace=ws)]
+        for u, v in zip(first, again):
+            np.testing.assert_array_equal(u, v)
