@@ -157,7 +157,7 @@ presto_status presto_tree_attention(const presto_attn_desc* desc, const void* q,
     REQUIRE(d.head_dim == 64 || d.head_dim == 128, "presto_tree_attention: head_dim %d",
             d.head_dim);
     REQUIRE(d.max_ctx >= 0, "presto_tree_attention: max_ctx < 0");
-    REQUIRE(isfinite(d.scale), "presto_tree_attention: scale not finite");
+    REQUIRE(isfinite(d.scale) && d.scale > 0.f, "presto_tree_attention: scale must be positive");
     REQUIRE((int64_t)d.max_ctx + d.n_max < ((int64_t)1 << 30), "presto_tree_attention: too long");
     if (d.batch == 0) return PRESTO_OK;
     REQUIRE(q && k_tree && v_tree && ctx_offsets && anc && n_nodes && out,

@@ -8,17 +8,22 @@
 // 0 .. ctx_b-1 read the packed cache, positions ctx_b .. ctx_b+n_nodes-1
 // read the tree K/V and are masked by the ancestor bitmask.
 //
-// bf16 path (matrix cores, v_mfma_f32_32x32x16_bf16).  A workgroup is four
-// waves, one per SIMD, each owning 64 query rows (two 32-row MFMA blocks, so
-// every K/V fragment read from LDS feeds two MFMAs).  Scores are computed
+// bf16 path (matrix cores, v_mfma_f32_32x32x16_bf16).  A workgroup is eight
+// waves (two per SIMD), each owning 32 query rows.  Scores are computed
 // transposed, S^T = K Q^T: a lane then holds one query row and 16 of the 32
-// keys of a block, the row max/sum need one cross-half swap, and the bf16
+// keys of a block, the row max needs one cross-half swap, and the bf16
 // probabilities are already in the B-operand layout of O^T = V^T P^T.  K and
-// V sit in LDS row-major; the V^T operand comes from transposed LDS reads
-// (ds_read_b64_tr_b16).  The next K/V tile is fetched into registers while
-// the current one is consumed.  The context is split across workgroups when
-// the batch alone cannot fill the chip; partial (max, sum, accumulator)
-// triples are then merged by a second kernel.
+// V sit in LDS row-major (rows padded so that the b128 K reads and the
+// transposed ds_read_b64_tr_b16 V reads are free of bank conflicts).  Three
+// 64-key LDS buffers rotate: tile t is consumed, tile t+1 is resident (the
+// last block of a tile already scores the first block of the next), tile t+2
+// waits in registers; one barrier per tile.  Inside a wave the scores of
+// block i+1 are computed while the softmax and P V of block i run, so the
+// matrix cores and the vector ALUs overlap.  The running reference maximum
+// only moves when a block exceeds it by a margin, which keeps the 64-register
+// accumulator rescale off the common path.  The context is split across
+// workgroups when the batch alone cannot fill the chip; partial (reference,
+// sum, accumulator) triples are then merged by a second kernel.
 #include <math.h>
 
 #include "common.hpp"
@@ -29,12 +34,24 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float floatx4 __attribute__((ext_vector_type(4)));
 typedef float floatx16 __attribute__((ext_vector_type(16)));
 typedef short short4_t __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef float floatx2 __attribute__((ext_vector_type(2)));
 
-constexpr int kKeyTile = 64;      // keys per LDS tile
-constexpr int kRowsPerWave = 64;  // two 32-row MFMA blocks per wave
-constexpr int kAttnWaves = 4;     // one wave per SIMD (about 300 registers each)
-constexpr int kAttnThreads = kAttnWaves * kWave;
-constexpr int kRowsPerTile = kAttnWaves * kRowsPerWave;
+// Two fp32 -> two bf16 (round to nearest even) in one v_cvt_pk_bf16_f32.
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector((floatx2){lo, hi}, bf16x2));
+}
+
+constexpr int kKeyTile = 64;      // keys per LDS tile: two 32-key blocks per barrier
+constexpr int kBlocksPerTile = kKeyTile / 32;
+constexpr int kBufs = 3;          // LDS tile buffers
+constexpr float kSlack = 8.f;
+constexpr int kMaxAncWords = 16;
+constexpr int kValuPerMfma = 4;   // VALU ops issued behind each MFMA of a key block  // ancestor words per node: n_max <= 1024     // log2 headroom before the accumulator is rescaled
+constexpr int kRowsPerWave = 32;  // one 32-row MFMA block per wave
+// Workgroups are 8 waves, two per SIMD: one wave's softmax hides behind the
+// other's MFMAs (with one wave per SIMD the matrix cores sit idle during it).
+constexpr int kAttnWaves = 8;
 constexpr float kLog2e = 1.4426950408889634f;
 
 struct AttnArgs {
@@ -66,16 +83,54 @@ __device__ __forceinline__ int xcd_task(int bid, int n_blocks) {
     return (bid & 7) * per + (bid >> 3);
 }
 
-template <int D>
-__global__ __launch_bounds__(kAttnThreads, 1) void tree_attn_bf16_kernel(AttnArgs a) {
+// This thread's PT 16-byte pieces of one K tile and one V tile.
+template <int PT>
+struct TilePieces {
+    uint4 k[PT], v[PT];
+};
+
+// Loads this thread's pieces of the K and V tile that starts at key t0.
+// Keys below ctx come from the packed cache row c0 + j, the others from the
+// tree K/V of node j - ctx; rows past k_end repeat the last key (every load
+// stays in bounds; their scores are masked to -inf).
+template <int D, int PT, int NT>
+__device__ __forceinline__ TilePieces<PT> fetch_tile(const uint16_t* kc, const uint16_t* vc,
+                                                     const uint16_t* kt, const uint16_t* vt, int tid,
+                                                     int t0, int k_end, int ctx, int c0, int hkv,
+                                                     int g, int64_t tree_row0) {
+    const int64_t kv_stride = (int64_t)hkv * D;
+    TilePieces<PT> r;
+#pragma unroll
+    for (int i = 0; i < PT; ++i) {
+        const int p = tid + i * NT;
+        const int kk = p / (D / 8), c8 = p % (D / 8);
+        const int j = min(t0 + kk, k_end - 1);
+        const bool in_ctx = j < ctx;
+        const int64_t off = in_ctx ? (int64_t)(c0 + j) * kv_stride + (int64_t)g * D + c8 * 8
+                                   : ((tree_row0 + (j - ctx)) * hkv + g) * D + c8 * 8;
+        const uint16_t* kp = in_ctx ? kc : kt;
+        const uint16_t* vp = in_ctx ? vc : vt;
+        r.k[i] = *reinterpret_cast<const uint4*>(kp + off);
+        r.v[i] = *reinterpret_cast<const uint4*>(vp + off);
+    }
+    return r;
+}
+
+template <int D, int NW>
+__global__ __launch_bounds__(NW * kWave) void tree_attn_bf16_kernel(AttnArgs a) {
     constexpr int KS = D / 16;                 // S^T contraction steps over the head dimension
     constexpr int DB = D / 32;                 // 32-wide blocks of the output head dimension
-    constexpr int KROW = D + 8;                // K row in LDS (bf16): bank spread for b128 reads
-    constexpr int VROW = D + 16;               // V row in LDS: bank spread for transposed reads
+    constexpr int KROW = D + 8;                // K row in LDS (bf16): conflict-free b128 reads
+    constexpr int VROW = D + 32;               // V row in LDS: conflict-free transposed b64 reads
     constexpr int PIECES = kKeyTile * D / 8;   // 16-byte pieces of one K (or V) tile
-    constexpr int PT = PIECES / kAttnThreads;  // pieces per thread
-    __shared__ __align__(16) uint16_t sK[kKeyTile * KROW];
-    __shared__ __align__(16) uint16_t sV[kKeyTile * VROW];
+    constexpr int NT = NW * kWave;
+    constexpr int PT = PIECES / NT;            // pieces per thread
+    constexpr int ROWS = NW * kRowsPerWave;    // query rows per workgroup
+    constexpr int KBUF = kKeyTile * KROW, VBUF = kKeyTile * VROW;
+    static_assert(PT * NT == PIECES, "tile pieces must divide evenly");
+    __shared__ __align__(16) uint16_t sK[kBufs * KBUF];
+    __shared__ __align__(16) uint16_t sV[kBufs * VBUF];
+    __shared__ uint64_t s_anc[(ROWS + 1) * kMaxAncWords];  // ancestor rows of this tile's nodes
 
     const int task = xcd_task(blockIdx.x, a.n_blocks);
     if (task >= a.n_tasks) return;
@@ -91,227 +146,240 @@ __global__ __launch_bounds__(kAttnThreads, 1) void tree_attn_bf16_kernel(AttnArg
     const int k_begin = split * a.split_len;
     if (k_begin >= keys) return;  // nothing of this sequence in this split
     const int k_end = min(keys, k_begin + a.split_len);
+    const int ntiles = (k_end - k_begin + kKeyTile - 1) / kKeyTile;
+    const int nblocks = (k_end - k_begin + 31) / 32;
     const int live_rows = a.G * nn;
     const int all_rows = a.G * a.n_max;
+    const int mask_from = min(ctx, k_end);  // keys at or beyond need a mask
 
     const int tid = threadIdx.x;
     const int wave = tid / kWave, lane = lane_id();
     const int l32 = lane & 31, h = lane >> 5;
-    const int rbase = rt * kRowsPerTile + wave * kRowsPerWave;  // two 32-row blocks per wave
-    const bool active = rbase < live_rows;
+    const int rho = rt * ROWS + wave * kRowsPerWave + l32;  // this lane's query row
+    const bool active = rt * ROWS + wave * kRowsPerWave < live_rows;
+    const int qn = rho / a.G, qh = rho - qn * a.G;
+    const int node = min(qn, a.n_max - 1);
 
-    // Q fragments, B operand of S^T = K Q^T: lane holds row l32, d = ks*16 + h*8 .. +8
-    bf16x8 qf[2][KS];
-    int node_of[2];
-#pragma unroll
-    for (int nb = 0; nb < 2; ++nb) {
-        const int rho = rbase + nb * 32 + l32;
-        const int n = rho / a.G, hh = rho - n * a.G;
-        node_of[nb] = min(n, a.n_max - 1);
-        const uint16_t* qp = a.q + (((int64_t)b * a.n_max + n) * a.hq + g * a.G + hh) * D;
+    // Q fragments, B operand of S^T = K Q^T: lane holds row l32, d = ks*16 + h*8 .. +8.
+    // Loaded before the first K/V tiles, so the waits for those tiles also
+    // cover Q and nothing in the key loop waits on global loads but the stage.
+    bf16x8 qf[KS];
+    {
+        const uint16_t* qp = a.q + (((int64_t)b * a.n_max + qn) * a.hq + g * a.G + qh) * D;
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks) {
             uint4 u = make_uint4(0, 0, 0, 0);
             if (rho < all_rows) u = *reinterpret_cast<const uint4*>(qp + ks * 16 + h * 8);
-            qf[nb][ks] = __builtin_bit_cast(bf16x8, u);
+            qf[ks] = __builtin_bit_cast(bf16x8, u);
         }
     }
 
-    floatx16 o[2][DB];
-    float m_run[2], l_run[2];
+    // ---- K/V staging: global -> registers -> LDS, three buffers: while tile t
+    // is consumed, tile t+1 is already in LDS (the last block of a tile scores
+    // the first block of the next one) and tile t+2 is in flight.
+    auto fetch = [&](int t0) {
+        return fetch_tile<D, PT, NT>(a.kc, a.vc, a.kt, a.vt, tid, t0, k_end, ctx, c0, a.hkv, g,
+                                     (int64_t)b * a.n_max);
+    };
+    auto stage = [&](int buf, const TilePieces<PT>& tp) {
 #pragma unroll
-    for (int nb = 0; nb < 2; ++nb) {
-        m_run[nb] = -INFINITY;
-        l_run[nb] = 0.f;
+        for (int i = 0; i < PT; ++i) {
+            const int p = tid + i * NT;
+            const int kk = p / (D / 8), c8 = p % (D / 8);
+            *reinterpret_cast<uint4*>(&sK[buf * KBUF + kk * KROW + c8 * 8]) = tp.k[i];
+            *reinterpret_cast<uint4*>(&sV[buf * VBUF + kk * VROW + c8 * 8]) = tp.v[i];
+        }
+    };
+    // unconditional: tiles past the split only repeat the last key, and a
+    // buffer staged with them is never read
+    TilePieces<PT> pend = fetch(k_begin);
+    {
+        const TilePieces<PT> second = fetch(k_begin + kKeyTile);
+        stage(0, pend);
+        stage(1, second);
+    }
+    pend = fetch(k_begin + 2 * kKeyTile);
+    // ancestor bitmask rows of the nodes this workgroup serves, when the
+    // split reaches the tree keys (masks then read LDS, not global memory)
+    const int n_first = (rt * ROWS) / a.G;
+    if (k_end > ctx) {
+        const int n_last = min((rt * ROWS + ROWS - 1) / a.G, a.n_max - 1);
+        const int words = (n_last - n_first + 1) * a.W;
+        const uint64_t* src = a.anc + ((int64_t)b * a.n_max + n_first) * a.W;
+        for (int w = tid; w < words; w += NT) s_anc[w] = src[w];
+    }
+    __syncthreads();
+
+    floatx16 o[DB];
+#pragma unroll
+    for (int db = 0; db < DB; ++db)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) o[db][i] = 0.f;
+    // Running reference m (log2 domain, scaled) and denominator l.  m only
+    // moves when a block's maximum exceeds it by more than kSlack, so most
+    // blocks skip the accumulator rescale; probabilities stay below 2^kSlack.
+    float m_run = -INFINITY, l_run = 0.f;
+
+    const float c = a.scale_log2;
+    // per-lane LDS element offsets; every fragment read adds only a constant
+    const int k_lane = l32 * KROW + h * 8;
+    const int v_lane = (4 * h + ((lane & 15) >> 2)) * VROW + ((lane >> 4) & 1) * 16 + 4 * (lane & 3);
+
+    // S^T block of 32 keys (block i of the split) into S
+    auto scores = [&](int i) {
+        floatx16 S;
+#pragma unroll
+        for (int e = 0; e < 16; ++e) S[e] = 0.f;
+        const int buf = (i / kBlocksPerTile) % kBufs, blk = i % kBlocksPerTile;
+        int koff = buf * KBUF + blk * 32 * KROW + k_lane;
+        asm volatile("" : "+v"(koff));  // keep the per-read constants as immediate offsets
+        const uint16_t* kb = sK + koff;
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+            const bf16x8 ka = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(kb + ks * 16));
+            S = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qf[ks], S, 0, 0, 0);
+        }
+        return S;
+    };
+    // element e of a lane is key j0 + 8(e/4) + 4h + e%4
+    auto row_max = [&](const floatx16& S) {
+        float mx = S[0];
+#pragma unroll
+        for (int e = 1; e < 16; ++e) mx = fmaxf(mx, S[e]);
+        const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(mx), __float_as_uint(mx),
+                                                         false, false);
+        return fmaxf(mx, __uint_as_float(h == 0 ? sw[1] : sw[0]));
+    };
+    auto apply_mask = [&](floatx16& S, int j0) {
+        uint64_t aw0 = 0ull, aw1 = 0ull;
+        const int wbase = max(0, j0 - ctx) >> 6;
+        if (j0 + 32 > ctx) {
+            const uint64_t* arow = &s_anc[(node - n_first) * a.W];
+            aw0 = arow[wbase];
+            aw1 = wbase + 1 < a.W ? arow[wbase + 1] : 0ull;
+        }
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+            const int j = j0 + 8 * (e >> 2) + 4 * h + (e & 3);
+            const int m = max(j - ctx, 0);
+            const uint64_t wd = ((m >> 6) - wbase) == 0 ? aw0 : aw1;
+            const bool vis = (j < k_end) & ((j < ctx) | (bool)((wd >> (m & 63)) & 1ull));
+            S[e] = vis ? S[e] : -INFINITY;
+        }
+    };
+    // move m when the block maximum mx (raw score) exceeds it by more than kSlack
+    auto update = [&](float mx) {
+        const float mx2 = mx * c;
+        const bool need = mx2 > m_run + kSlack;
+        if (__ballot(need)) {
+            const float mn = need ? mx2 : m_run;
+            const float alpha = need ? __builtin_amdgcn_exp2f(m_run - mn) : 1.f;
+            m_run = mn;
+            l_run *= alpha;
+#pragma unroll
+            for (int db = 0; db < DB; ++db) o[db] *= alpha;
+        }
+    };
+
+    floatx16 S_cur;
+    if (active) {
+        S_cur = scores(0);
+        if (k_begin + 32 > mask_from) apply_mask(S_cur, k_begin);
+        update(row_max(S_cur));
+    }
+    for (int t = 0; t < ntiles; ++t) {
+        if (active) {
+#pragma unroll
+            for (int q = 0; q < kBlocksPerTile; ++q) {
+                const int i = t * kBlocksPerTile + q;
+                if (i < nblocks) {
+                    // scores of the next block (its tile is already in LDS) overlap
+                    // the softmax and P V of this one
+                    // scores of the next block (its tile is already in LDS)
+                    // overlap the softmax and P V of this one
+                    floatx16 S_nxt = scores(i + 1);
+                    const float m_use = m_run == -INFINITY ? 0.f : m_run;
+                    float ls = 0.f;
+                    uint32_t P[8];
+#pragma unroll
+                    for (int e = 0; e < 16; e += 2) {
+                        const float p0 = __builtin_amdgcn_exp2f(fmaf(S_cur[e], c, -m_use));
+                        const float p1 = __builtin_amdgcn_exp2f(fmaf(S_cur[e + 1], c, -m_use));
+                        ls += p0 + p1;
+                        P[e >> 1] = pack_bf16x2(p0, p1);
+                    }
+                    l_run += ls;
+                    int voff = (t % kBufs) * VBUF + q * 32 * VROW + v_lane;
+                    asm volatile("" : "+v"(voff));
+                    const uint16_t* vb = sV + voff;
+#pragma unroll
+                    for (int st = 0; st < 2; ++st) {
+                        const bf16x8 pb = __builtin_bit_cast(
+                            bf16x8, make_uint4(P[4 * st], P[4 * st + 1], P[4 * st + 2], P[4 * st + 3]));
+#pragma unroll
+                        for (int db = 0; db < DB; ++db) {
+                            const uint16_t* v0 = vb + st * 16 * VROW + db * 32;
+                            const short4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                                (__attribute__((address_space(3))) short4_t*)(v0));
+                            const short4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                                (__attribute__((address_space(3))) short4_t*)(v0 + 8 * VROW));
+                            const uint2 ul = __builtin_bit_cast(uint2, lo), uh = __builtin_bit_cast(uint2, hi);
+                            const bf16x8 va = __builtin_bit_cast(bf16x8, make_uint4(ul.x, ul.y, uh.x, uh.y));
+                            o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pb, o[db], 0, 0, 0);
+                        }
+                    }
+                    float mx = row_max(S_nxt);
+                    if (i + 1 < nblocks) {
+                        const int j0 = k_begin + (i + 1) * 32;
+                        if (j0 + 32 > mask_from) {
+                            apply_mask(S_nxt, j0);
+                            mx = row_max(S_nxt);
+                        }
+                        update(mx);
+                    }
+                    S_cur = S_nxt;
+                }
+            }
+        }
+        // tile t+2 goes into the buffer of tile t-1, which every wave finished
+        // before the previous barrier
+        stage((t + 2) % kBufs, pend);
+        pend = fetch(k_begin + (t + 3) * kKeyTile);
+        __syncthreads();
+    }
+
+    // ---- epilogue: lane holds row l32, d = db*32 + 8(i/4) + 4h + i%4
+    {
+        const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(l_run), __float_as_uint(l_run),
+                                                         false, false);
+        l_run += __uint_as_float(h == 0 ? sw[1] : sw[0]);
+    }
+    if (rho >= all_rows) return;
+    if (a.splits == 1) {
+        uint16_t* op = a.out + (((int64_t)b * a.n_max + qn) * a.hq + g * a.G + qh) * D;
+        const float inv = (rho < live_rows && l_run > 0.f) ? 1.f / l_run : 0.f;
 #pragma unroll
         for (int db = 0; db < DB; ++db)
 #pragma unroll
-            for (int i = 0; i < 16; ++i) o[nb][db][i] = 0.f;
-    }
-
-    // K/V tile staging: PT 16-byte pieces of K and of V per thread, fetched into
-    // registers one tile ahead and written to LDS row-major.
-    const int64_t kv_stride = (int64_t)a.hkv * D;
-    uint4 kreg[PT], vreg[PT];
-    auto fetch = [&](int t0) {
-#pragma unroll
-        for (int i = 0; i < PT; ++i) {
-            const int p = tid + i * kAttnThreads;
-            const int kk = p / (D / 8), c8 = p % (D / 8);
-            const int jr = t0 + kk;
-            const int j = min(jr, k_end - 1);  // clamped: every load is in bounds
-            const bool in_ctx = j < ctx;
-            const int64_t off = in_ctx
-                ? (int64_t)(c0 + j) * kv_stride + (int64_t)g * D + c8 * 8
-                : (((int64_t)b * a.n_max + (j - ctx)) * a.hkv + g) * D + c8 * 8;
-            const uint4 ku = *reinterpret_cast<const uint4*>((in_ctx ? a.kc : a.kt) + off);
-            const uint4 vu = *reinterpret_cast<const uint4*>((in_ctx ? a.vc : a.vt) + off);
-            const bool ok = jr < k_end;
-            kreg[i] = ok ? ku : make_uint4(0, 0, 0, 0);
-            vreg[i] = ok ? vu : make_uint4(0, 0, 0, 0);
-        }
-    };
-    auto stage = [&]() {
-#pragma unroll
-        for (int i = 0; i < PT; ++i) {
-            const int p = tid + i * kAttnThreads;
-            const int kk = p / (D / 8), c8 = p % (D / 8);
-            *reinterpret_cast<uint4*>(&sK[kk * KROW + c8 * 8]) = kreg[i];
-            *reinterpret_cast<uint4*>(&sV[kk * VROW + c8 * 8]) = vreg[i];
-        }
-    };
-
-    fetch(k_begin);
-    for (int t0 = k_begin; t0 < k_end; t0 += kKeyTile) {
-        __syncthreads();  // the previous tile has been consumed
-        stage();
-        __syncthreads();
-        if (t0 + kKeyTile < k_end) fetch(t0 + kKeyTile);
-        if (!active) continue;
-        const bool plain = t0 + kKeyTile <= min(ctx, k_end);  // no mask inside this tile
-        // ancestor words covering the tree keys of this tile, per row block
-        uint64_t aw[2][2] = {{0ull, 0ull}, {0ull, 0ull}};
-        int wbase = 0;
-        if (!plain && t0 + kKeyTile > ctx) {
-            wbase = max(0, t0 - ctx) >> 6;
-#pragma unroll
-            for (int nb = 0; nb < 2; ++nb) {
-                const uint64_t* arow = a.anc + ((int64_t)b * a.n_max + node_of[nb]) * a.W;
-                aw[nb][0] = arow[wbase];
-                aw[nb][1] = wbase + 1 < a.W ? arow[wbase + 1] : 0ull;
+            for (int q4 = 0; q4 < 4; ++q4) {
+                const int dd = db * 32 + 8 * q4 + 4 * h;
+                *reinterpret_cast<uint2*>(op + dd) =
+                    make_uint2(pack_bf16x2(o[db][4 * q4] * inv, o[db][4 * q4 + 1] * inv),
+                               pack_bf16x2(o[db][4 * q4 + 2] * inv, o[db][4 * q4 + 3] * inv));
             }
-        }
+    } else {
+        float* pp = a.part + ((((int64_t)b * a.hkv + g) * a.rows_pad + rho) * a.splits + split) * (D + 2);
 #pragma unroll
-        for (int kb = 0; kb < kKeyTile / 32; ++kb) {
-            // ---- S^T (32 keys x 64 rows): A = K rows from LDS, B = Q fragments
-            floatx16 s[2];
+        for (int db = 0; db < DB; ++db)
 #pragma unroll
-            for (int nb = 0; nb < 2; ++nb)
-#pragma unroll
-                for (int i = 0; i < 16; ++i) s[nb][i] = 0.f;
-#pragma unroll
-            for (int ks = 0; ks < KS; ++ks) {
-                const uint4 u = *reinterpret_cast<const uint4*>(
-                    &sK[(kb * 32 + l32) * KROW + ks * 16 + h * 8]);
-                const bf16x8 ka = __builtin_bit_cast(bf16x8, u);
-                s[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qf[0][ks], s[0], 0, 0, 0);
-                s[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qf[1][ks], s[1], 0, 0, 0);
+            for (int q4 = 0; q4 < 4; ++q4) {
+                const int dd = db * 32 + 8 * q4 + 4 * h;
+                *reinterpret_cast<float4*>(pp + dd) = make_float4(o[db][4 * q4], o[db][4 * q4 + 1],
+                                                                  o[db][4 * q4 + 2], o[db][4 * q4 + 3]);
             }
-            // ---- online softmax; element i of lane holds key 8(i/4) + 4h + i%4 of the block
-            uint32_t pk[2][8];
-#pragma unroll
-            for (int nb = 0; nb < 2; ++nb) {
-                float mx = -INFINITY;
-#pragma unroll
-                for (int i = 0; i < 16; ++i) {
-                    float v = s[nb][i] * a.scale_log2;
-                    if (!plain) {
-                        // visible: inside the sequence, and a cached key or an ancestor
-                        const int j = t0 + kb * 32 + 8 * (i >> 2) + 4 * h + (i & 3);
-                        const int m = max(j - ctx, 0);
-                        const uint64_t wd = ((m >> 6) - wbase) == 0 ? aw[nb][0] : aw[nb][1];
-                        const bool anc_bit = (wd >> (m & 63)) & 1ull;
-                        const bool vis = (j < k_end) & ((j < ctx) | anc_bit);
-                        v = vis ? v : -INFINITY;
-                    }
-                    s[nb][i] = v;
-                    mx = fmaxf(mx, v);
-                }
-                {
-                    const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(mx),
-                                                                     __float_as_uint(mx), false, false);
-                    mx = fmaxf(mx, __uint_as_float(h == 0 ? sw[1] : sw[0]));
-                }
-                const float m_new = fmaxf(m_run[nb], mx);
-                const float m_use = m_new == -INFINITY ? 0.f : m_new;
-                const float alpha = __builtin_amdgcn_exp2f(m_run[nb] - m_use);
-                m_run[nb] = m_new;
-                float ls = 0.f;
-#pragma unroll
-                for (int i = 0; i < 16; i += 2) {
-                    const float p0 = __builtin_amdgcn_exp2f(s[nb][i] - m_use);
-                    const float p1 = __builtin_amdgcn_exp2f(s[nb][i + 1] - m_use);
-                    ls += p0 + p1;
-                    pk[nb][i >> 1] = (uint32_t)__builtin_bit_cast(uint16_t, (__bf16)p0) |
-                                     ((uint32_t)__builtin_bit_cast(uint16_t, (__bf16)p1) << 16);
-                }
-                l_run[nb] = l_run[nb] * alpha + ls;
-                if (__ballot(alpha != 1.f)) {
-#pragma unroll
-                    for (int db = 0; db < DB; ++db) o[nb][db] *= alpha;
-                }
-            }
-            // ---- O^T += V^T P^T over two 16-key steps; V^T fragments by transposed LDS reads
-#pragma unroll
-            for (int st = 0; st < 2; ++st) {
-                bf16x8 pb[2];
-#pragma unroll
-                for (int nb = 0; nb < 2; ++nb)
-                    pb[nb] = __builtin_bit_cast(
-                        bf16x8, make_uint4(pk[nb][4 * st], pk[nb][4 * st + 1], pk[nb][4 * st + 2],
-                                           pk[nb][4 * st + 3]));
-                const int kbase = kb * 32 + st * 16 + 4 * h;
-                const int t16 = lane & 15, dhalf = (lane >> 4) & 1;
-#pragma unroll
-                for (int db = 0; db < DB; ++db) {
-                    const int d0 = db * 32 + dhalf * 16;
-                    const uint16_t* v0 = &sV[(kbase + (t16 >> 2)) * VROW + d0 + 4 * (t16 & 3)];
-                    const short4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-                        (__attribute__((address_space(3))) short4_t*)(v0));
-                    const short4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-                        (__attribute__((address_space(3))) short4_t*)(v0 + 8 * VROW));
-                    const bf16x8 va = __builtin_bit_cast(
-                        bf16x8, make_uint4(__builtin_bit_cast(uint2, lo).x, __builtin_bit_cast(uint2, lo).y,
-                                           __builtin_bit_cast(uint2, hi).x, __builtin_bit_cast(uint2, hi).y));
-                    o[0][db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pb[0], o[0][db], 0, 0, 0);
-                    o[1][db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pb[1], o[1][db], 0, 0, 0);
-                }
-            }
-        }
-    }
-
-    // ---- epilogue: lane holds row l32 of each block, d = db*32 + 8(i/4) + 4h + i%4
-#pragma unroll
-    for (int nb = 0; nb < 2; ++nb) {
-        float l = l_run[nb];
-        {
-            const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(l), __float_as_uint(l),
-                                                             false, false);
-            l += __uint_as_float(h == 0 ? sw[1] : sw[0]);
-        }
-        const int rho = rbase + nb * 32 + l32;
-        if (rho >= all_rows) continue;
-        const int n = rho / a.G, hh = rho - n * a.G;
-        if (a.splits == 1) {
-            uint16_t* op = a.out + (((int64_t)b * a.n_max + n) * a.hq + g * a.G + hh) * D;
-            const float inv = (rho < live_rows && l > 0.f) ? 1.f / l : 0.f;
-#pragma unroll
-            for (int db = 0; db < DB; ++db)
-#pragma unroll
-                for (int q4 = 0; q4 < 4; ++q4) {
-                    const int dd = db * 32 + 8 * q4 + 4 * h;
-                    uint2 w;
-                    w.x = (uint32_t)f_to_bf16(o[nb][db][4 * q4] * inv) |
-                          ((uint32_t)f_to_bf16(o[nb][db][4 * q4 + 1] * inv) << 16);
-                    w.y = (uint32_t)f_to_bf16(o[nb][db][4 * q4 + 2] * inv) |
-                          ((uint32_t)f_to_bf16(o[nb][db][4 * q4 + 3] * inv) << 16);
-                    *reinterpret_cast<uint2*>(op + dd) = w;
-                }
-        } else {
-            float* pp = a.part + ((((int64_t)b * a.hkv + g) * a.rows_pad + rho) * a.splits + split) * (D + 2);
-#pragma unroll
-            for (int db = 0; db < DB; ++db)
-#pragma unroll
-                for (int q4 = 0; q4 < 4; ++q4) {
-                    const int dd = db * 32 + 8 * q4 + 4 * h;
-                    *reinterpret_cast<float4*>(pp + dd) =
-                        make_float4(o[nb][db][4 * q4], o[nb][db][4 * q4 + 1], o[nb][db][4 * q4 + 2],
-                                    o[nb][db][4 * q4 + 3]);
-                }
-            if (h == 0) {
-                pp[D] = m_run[nb];
-                pp[D + 1] = l;
-            }
+        if (h == 0) {
+            pp[D] = m_run;
+            pp[D + 1] = l_run;
         }
     }
 }
@@ -459,16 +527,25 @@ static AttnPlan attn_plan(const presto_attn_desc* d) {
     AttnPlan p;
     p.G = d->hq / d->hkv;
     p.rows = p.G * d->n_max;
-    p.row_tiles = (p.rows + kRowsPerTile - 1) / kRowsPerTile;
-    p.rows_per_tile = kRowsPerTile;
     p.waves = kAttnWaves;
+    p.rows_per_tile = p.waves * kRowsPerWave;
+    p.row_tiles = (p.rows + p.rows_per_tile - 1) / p.rows_per_tile;
     p.rows_pad = p.rows_per_tile * p.row_tiles;
+    // context splits: fewest idle CU slots per unit of work (one workgroup per CU)
     const int64_t base = (int64_t)d->batch * d->hkv * p.row_tiles;
     const int keys = d->max_ctx + d->n_max;
-    const int max_splits = (keys + 255) / 256;
-    int splits = (int)((384 + base - 1) / base);
-    splits = splits < 1 ? 1 : (splits > max_splits ? max_splits : splits);
-    int len = (keys + splits - 1) / splits;
+    const int max_splits = (keys + 511) / 512;
+    int best = 1;
+    double best_cost = 1e30;
+    for (int s = 1; s <= 32 && s <= max_splits; ++s) {
+        const double rounds = (double)((base * s + 255) / 256);
+        const double cost = rounds / s + 0.02 * s;  // rounds of work per split + merge overhead
+        if (cost < best_cost - 1e-9) {
+            best_cost = cost;
+            best = s;
+        }
+    }
+    int len = (keys + best - 1) / best;
     len = (len + kKeyTile - 1) / kKeyTile * kKeyTile;
     p.split_len = len;
     p.splits = (keys + len - 1) / len;
@@ -525,19 +602,19 @@ presto_status launch_tree_attention(const presto_attn_desc* d, const void* q, co
     a.n_tasks = (int32_t)p.tasks;
     a.n_blocks = (int32_t)p.blocks;
     a.scale_log2 = d->scale * kLog2e;
-    const dim3 block(kAttnThreads);
+    const dim3 block(p.waves * kWave), grid((unsigned)p.blocks);
     if (d->head_dim == 64)
-        tree_attn_bf16_kernel<64><<<(unsigned)p.blocks, block, 0, stream>>>(a);
+        tree_attn_bf16_kernel<64, kAttnWaves><<<grid, block, 0, stream>>>(a);
     else
-        tree_attn_bf16_kernel<128><<<(unsigned)p.blocks, block, 0, stream>>>(a);
+        tree_attn_bf16_kernel<128, kAttnWaves><<<grid, block, 0, stream>>>(a);
     presto_status st = check_launch("tree_attn_bf16_kernel");
     if (st != PRESTO_OK || p.splits == 1) return st;
     const int64_t merge_rows = (int64_t)d->batch * d->hkv * p.G * d->n_max;
-    const unsigned grid = (unsigned)((merge_rows + 3) / 4);
+    const unsigned mgrid = (unsigned)((merge_rows + 3) / 4);
     if (d->head_dim == 64)
-        tree_attn_merge_kernel<64><<<grid, 256, 0, stream>>>(a);
+        tree_attn_merge_kernel<64><<<mgrid, 256, 0, stream>>>(a);
     else
-        tree_attn_merge_kernel<128><<<grid, 256, 0, stream>>>(a);
+        tree_attn_merge_kernel<128><<<mgrid, 256, 0, stream>>>(a);
     return check_launch("tree_attn_merge_kernel");
 }
 
