@@ -5,8 +5,8 @@
 // maximum and the lowest id holding it, packed into one orderable 64-bit
 // key.  Kernel 2, queued right behind, runs one workgroup per sequence: its
 // waves reduce the chunk keys of the live nodes to the target's greedy
-// prediction a[n] (into LDS), then one wave walks the tree from the root:
-// move to the child whose token equals a[current] until no child does.
+// prediction a[n] (into LDS), then find the accepted root path in parallel
+// (pointer jumping over the parent links) instead of walking it.
 #include <math.h>
 
 #include "common.hpp"
@@ -16,6 +16,7 @@ namespace presto {
 constexpr int kArgmaxWavesPerBlock = 4;
 constexpr int kWalkThreads = 1024;
 constexpr int kMaxNodes = 1024;
+constexpr int kNodesPerWave = 8;
 
 template <bool BF16, int NLOAD>
 __global__ __launch_bounds__(kArgmaxWavesPerBlock * kWave) void argmax_partial_kernel(
@@ -90,7 +91,13 @@ __global__ __launch_bounds__(kArgmaxWavesPerBlock * kWave) void argmax_partial_k
     }
 }
 
-// One workgroup per sequence: per-node argmax from the chunk keys, then the walk.
+// One workgroup per sequence: per-node argmax from the chunk keys, then the
+// accepted path without a sequential walk.  Node c is "good" when its token
+// is the target's prediction after its parent, a[parent(c)]; siblings carry
+// distinct tokens, so every node has at most one good child and the accepted
+// path is the chain of nodes whose whole root path is good.  Pointer jumping
+// (ceil(log2(depth + 1)) rounds) gives every node that property and its
+// depth at once; the accepted nodes then write themselves into the path.
 __global__ __launch_bounds__(kWalkThreads) void accept_walk_kernel(
     int32_t n_max, int32_t depth, int32_t chunks, const uint64_t* __restrict__ part,
     const int32_t* __restrict__ parent, const int32_t* __restrict__ token,
@@ -98,22 +105,25 @@ __global__ __launch_bounds__(kWalkThreads) void accept_walk_kernel(
     int32_t* __restrict__ path, int32_t* __restrict__ bonus, int32_t* __restrict__ target_argmax) {
     __shared__ int32_t s_a[kMaxNodes];
     __shared__ int32_t s_par[kMaxNodes];
-    __shared__ int32_t s_tok[kMaxNodes];
+    __shared__ int32_t s_jmp[2][kMaxNodes];
+    __shared__ int32_t s_dep[2][kMaxNodes];  // edges to the jump target; -1: a bad node on the way
+    __shared__ int32_t s_len;
     const int b = blockIdx.x;
     const int nn = min(max(n_nodes[b], 1), n_max);
     const int wave = threadIdx.x / kWave, lane = lane_id();
     const int nwaves = blockDim.x / kWave;
     const int64_t rb = (int64_t)b * n_max;
-    for (int n = threadIdx.x; n < n_max; n += blockDim.x) {
-        s_par[n] = n < nn ? parent[rb + n] : -2;
-        s_tok[n] = token[rb + n];
-    }
-    // each wave reduces the chunk keys of four nodes at a time
-    for (int n0 = wave * 4; n0 < nn; n0 += nwaves * 4) {
-        uint64_t best[4] = {0ull, 0ull, 0ull, 0ull};
+    if (threadIdx.x == 0) s_len = 0;
+    for (int n = threadIdx.x; n < nn; n += blockDim.x) s_par[n] = n == 0 ? 0 : parent[rb + n];
+    // each wave reduces the chunk keys of kNodesPerWave nodes at a time (all
+    // their loads in flight before the first reduction)
+    for (int n0 = wave * kNodesPerWave; n0 < nn; n0 += nwaves * kNodesPerWave) {
+        uint64_t best[kNodesPerWave];
+#pragma unroll
+        for (int u = 0; u < kNodesPerWave; ++u) best[u] = 0ull;
         for (int c = lane; c < chunks; c += kWave) {
 #pragma unroll
-            for (int u = 0; u < 4; ++u) {
+            for (int u = 0; u < kNodesPerWave; ++u) {
                 if (n0 + u < nn) {
                     const uint64_t x = part[(rb + n0 + u) * chunks + c];
                     best[u] = x > best[u] ? x : best[u];
@@ -121,36 +131,49 @@ __global__ __launch_bounds__(kWalkThreads) void accept_walk_kernel(
             }
         }
 #pragma unroll
-        for (int u = 0; u < 4; ++u) {
+        for (int u = 0; u < kNodesPerWave; ++u) {
             const uint64_t m = wave_max_u64_dpp(best[u]);
             if (lane == 0 && n0 + u < nn) s_a[n0 + u] = (int32_t)key_id(m);
         }
     }
     __syncthreads();
-    for (int n = threadIdx.x; n < n_max; n += blockDim.x)
+    for (int n = threadIdx.x; n < n_max; n += blockDim.x) {
         if (target_argmax) target_argmax[rb + n] = n < nn ? s_a[n] : -1;
-    if (wave != 0) return;
-    int32_t* pth = path + (int64_t)b * (depth + 1);
-    int cur = 0, L = 0;
-    for (;;) {
-        const int32_t want = s_a[cur];
-        int next = -1;
-        for (int base = 1; base < nn && next < 0; base += kWave) {
-            const int c = base + lane;
-            const bool hit = c < nn && s_par[c] == cur && s_tok[c] == want;
-            const uint64_t m = __ballot(hit);
-            if (m) next = base + (int)__ffsll((unsigned long long)m) - 1;
+        if (n < nn) {
+            const int p = s_par[n];
+            const bool good = n == 0 || token[rb + n] == s_a[p];
+            s_jmp[0][n] = p;
+            s_dep[0][n] = good ? (n == 0 ? 0 : 1) : -1;
         }
-        if (next < 0 || L >= depth) break;
-        cur = next;
-        ++L;
-        if (lane == 0) pth[L] = cur;
     }
-    for (int i = L + 1 + lane; i <= depth; i += kWave) pth[i] = -1;
-    if (lane == 0) {
-        pth[0] = 0;
-        accept_len[b] = L;
-        bonus[b] = s_a[cur];
+    __syncthreads();
+    int cur = 0;
+    for (int reach = 1; reach < depth + 1; reach *= 2) {
+        for (int n = threadIdx.x; n < nn; n += blockDim.x) {
+            const int j = s_jmp[cur][n], dn = s_dep[cur][n], dj = s_dep[cur][j];
+            s_jmp[cur ^ 1][n] = s_jmp[cur][j];
+            s_dep[cur ^ 1][n] = (dn < 0 || dj < 0) ? -1 : dn + dj;
+        }
+        cur ^= 1;
+        __syncthreads();
+    }
+    // accepted nodes: a good root path no longer than `depth` moves
+    int32_t* pth = path + (int64_t)b * (depth + 1);
+    for (int n = threadIdx.x; n < nn; n += blockDim.x) {
+        const int dn = s_dep[cur][n];
+        if (dn >= 0 && dn <= depth) {
+            pth[dn] = n;
+            atomicMax(&s_len, dn);
+        }
+    }
+    __syncthreads();
+    const int L = s_len;
+    for (int i = L + 1 + threadIdx.x; i <= depth; i += blockDim.x) pth[i] = -1;
+    for (int n = threadIdx.x; n < nn; n += blockDim.x) {
+        if (s_dep[cur][n] == L) {
+            accept_len[b] = L;
+            bonus[b] = s_a[n];
+        }
     }
 }
 
@@ -197,7 +220,7 @@ presto_status launch_accept(bool bf16, const void* logits, int32_t vocab, int64_
 #undef PRESTO_ARGMAX
     presto_status st = check_launch("argmax_partial_kernel");
     if (st != PRESTO_OK) return st;
-    const int threads = n_max >= 512 ? kWalkThreads : (n_max >= 128 ? 512 : 256);
+    const int threads = n_max >= 64 ? kWalkThreads : 256;
     accept_walk_kernel<<<batch, threads, 0, stream>>>(n_max, depth, (int32_t)chunks, part, parent,
                                                       token, n_nodes, accept_len, path, bonus,
                                                       target_argmax);

@@ -3,12 +3,14 @@
 // One wavefront builds one sequence's tree; the batch runs in parallel.
 // LDS holds the candidate table (log q, token ids), the trigram lattice when
 // it fits, and per committed node one 8-byte record (parent, rank, depth, S)
-// plus the scores of its children.  The frontier lives in registers spread
-// over the 64 lanes (SL slots per lane), each slot only (S, packed
-// metadata): a pop is a per-lane max, one DPP wave max and a ballot.  Rank
-// path keys are rebuilt from the parent records only when several frontier
-// entries share the best S; token ids, the output rows and the ancestor
-// bitmasks are produced after the search, in parallel over the nodes.
+// plus its children in commit order (ranked once, when the node is
+// committed).  The frontier lives in registers spread over the 64 lanes (SL
+// slots per lane), each slot only (S, packed metadata): a pop is a per-lane
+// max, one DPP wave max and a ballot; the next sibling of a popped node is
+// one LDS read.  Rank-path keys are rebuilt from the parent records only
+// when several frontier entries share the best S; token ids, the output rows
+// and the ancestor bitmasks are produced after the search, in parallel over
+// the nodes.
 //
 // Frontier policy.  Committing nodes in pop order yields the B best prefixes
 // under the total order (S desc, rank path asc).  Instead of pushing all of
@@ -44,25 +46,56 @@ struct TreeArgs {
     uint64_t* anc;
     bool rho_in_lds;
     // LDS byte offsets
-    int o_lp, o_ids, o_cord, o_rec, o_rho;
+    int o_lp, o_ids, o_kord, o_krank, o_rec, o_rho;
 };
 
 // Frontier metadata in one word: parent node (10 bits), candidate rank (4),
-// depth (6), rank of the parent (4).
-__device__ __forceinline__ uint32_t pack_meta(int p, int r, int d, int rp) {
-    return (uint32_t)p | ((uint32_t)r << 10) | ((uint32_t)d << 14) | ((uint32_t)rp << 20);
+// depth (6), rank of the parent (4), position among the parent's children
+// in commit order (4).
+__device__ __forceinline__ uint32_t pack_meta(int p, int r, int d, int rp, int pos) {
+    return (uint32_t)p | ((uint32_t)r << 10) | ((uint32_t)d << 14) | ((uint32_t)rp << 20) |
+           ((uint32_t)pos << 24);
 }
 
-// u32 max over lanes 0..15 (row 0), returned to every lane.
-__device__ __forceinline__ uint32_t row0_max_u32_dpp(uint32_t v) {
-    v = max(v, dpp_u32<0xb1>(0u, v));
-    v = max(v, dpp_u32<0x4e>(0u, v));
-    v = max(v, dpp_u32<0x114>(0u, v));
-    v = max(v, dpp_u32<0x118>(0u, v));
-    return (uint32_t)__builtin_amdgcn_readlane((int)v, 15);
+// Number of lanes of this lane's row of 16 holding a larger key (row
+// rotations by 1..R, each another lane of the row exactly once).
+template <int R>
+__device__ __forceinline__ int row_count_greater(uint64_t key) {
+    if constexpr (R == 0) {
+        return 0;
+    } else {
+        return (dpp_u64<0x120 + R>(0ull, key) > key ? 1 : 0) + row_count_greater<R - 1>(key);
+    }
 }
 
-template <int SL>
+// Same within this lane's quad (quad_perm rotations by 1, 2, 3).
+__device__ __forceinline__ int quad_count_greater(uint64_t key) {
+    return (dpp_u64<0x39>(0ull, key) > key ? 1 : 0) + (dpp_u64<0x4e>(0ull, key) > key ? 1 : 0) +
+           (dpp_u64<0x93>(0ull, key) > key ? 1 : 0);
+}
+
+// Copies n 32-bit words from global memory to LDS with one wave, 16 loads
+// in flight per lane before the first store.
+__device__ __forceinline__ void stage_words(uint32_t* dst, const uint32_t* src, int n, int lane) {
+    constexpr int U = 16;
+    for (int base = 0; base < n; base += U * kWave) {
+        uint32_t r[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int i = base + u * kWave + lane;
+            r[u] = i < n ? src[i] : 0u;
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int i = base + u * kWave + lane;
+            if (i < n) dst[i] = r[u];
+        }
+    }
+}
+
+// RHO: 0 no lattice (s = log q), 1 lattice staged in LDS, 2 lattice read
+// from global memory.  KQ: k <= 4, children ranked within a quad.
+template <int SL, int RHO, bool KQ>
 __global__ __launch_bounds__(kWave) void tree_build_kernel(TreeArgs a) {
     extern __shared__ __align__(16) char lds[];
     const int lane = lane_id();
@@ -70,37 +103,46 @@ __global__ __launch_bounds__(kWave) void tree_build_kernel(TreeArgs a) {
     const int D = a.D, k = a.k, N = a.N, W = a.W, wbits = a.wbits, per_word = a.per_word;
     float* s_lp = reinterpret_cast<float*>(lds + a.o_lp);
     int32_t* s_ids = reinterpret_cast<int32_t*>(lds + a.o_ids);
-    uint32_t* s_cord = reinterpret_cast<uint32_t*>(lds + a.o_cord);  // [N][k] ord(child S) or 0
+    // children of every committed node in commit order: ord(S) (0 ends the
+    // list) and candidate rank
+    uint32_t* s_kord = reinterpret_cast<uint32_t*>(lds + a.o_kord);  // [N][k]
+    uint8_t* s_krank = reinterpret_cast<uint8_t*>(lds + a.o_krank);  // [N][k]
     uint2* s_rec = reinterpret_cast<uint2*>(lds + a.o_rec);          // [N] (meta, S bits)
     float* s_rho = reinterpret_cast<float*>(lds + a.o_rho);
     const int rho_n = D * k * k * k;
-    const float* g_rho = a.log_rho ? a.log_rho + (int64_t)b * rho_n : nullptr;
+    const float* g_rho = RHO ? a.log_rho + (int64_t)b * rho_n : nullptr;
 
-    // stage the candidate table of this sequence
+    // stage the candidate table of this sequence (and the lattice when it
+    // fits), with many loads in flight per lane
     const int64_t tb = (int64_t)b * D * k;
-    for (int i = lane; i < D * k; i += kWave) {
-        s_lp[i] = a.logprob[tb + i];
-        s_ids[i] = a.ids[tb + i];
-    }
-    if (g_rho && a.rho_in_lds)
-        for (int i = lane; i < rho_n; i += kWave) s_rho[i] = g_rho[i];
+    stage_words(reinterpret_cast<uint32_t*>(s_lp), reinterpret_cast<const uint32_t*>(a.logprob + tb),
+                D * k, lane);
+    stage_words(reinterpret_cast<uint32_t*>(s_ids), reinterpret_cast<const uint32_t*>(a.ids + tb), D * k,
+                lane);
+    if constexpr (RHO == 1)
+        stage_words(reinterpret_cast<uint32_t*>(s_rho), reinterpret_cast<const uint32_t*>(g_rho), rho_n,
+                    lane);
     const float lam_lane = lane < D ? a.lambda[lane] : 0.f;  // lambda_d held by lane d
     __builtin_amdgcn_wave_barrier();
 
-    // Child scores of node n (depth d, own rank rn, parent's rank rp, score Sn):
-    // ord(S) of its top-`branch` candidates stored in LDS (0 for the others);
-    // returns the first child in commit order as (ord S, rank), ord 0 if none.
+    // Children of node n (depth d, own rank rn, parent's rank rp, score Sn):
+    // lane r < k scores candidate r, the children are ranked by (S desc,
+    // rank asc) with in-row rotations and stored in that order; returns the
+    // first child as (ord S, rank), ord 0 if none.
     auto expand = [&](int n, int d, int rn, int rp, float Sn, uint32_t& c_ord, int& c_rank) {
         const int ctx2 = d >= 2 ? rp : 0;  // grandparent slot of the trigram
         const int ctx1 = d >= 1 ? rn : 0;  // parent slot of the trigram
         const float lam_d = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(lam_lane), d));
-        float s = -INFINITY;
-        if (lane < k) {
-            const float lq = s_lp[d * k + lane];
-            if (g_rho) {
-                const int ri = ((d * k + ctx2) * k + ctx1) * k + lane;
+        // every lane reads (lanes >= k at a clamped index) so that no branch
+        // separates the reads from their use; only lanes < k are kept
+        const int rl = min(lane, k - 1);
+        float s;
+        {
+            const float lq = s_lp[d * k + rl];
+            if constexpr (RHO != 0) {
+                const int ri = ((d * k + ctx2) * k + ctx1) * k + rl;
                 float lr;
-                if (a.rho_in_lds)
+                if constexpr (RHO == 1)
                     lr = s_rho[ri];
                 else
                     lr = g_rho[ri];
@@ -109,7 +151,7 @@ __global__ __launch_bounds__(kWave) void tree_build_kernel(TreeArgs a) {
             } else {
                 s = lq;
             }
-            s = (s == s) ? s : -INFINITY;
+            s = (s == s && lane < k) ? s : -INFINITY;
         }
         bool in = lane < k;
         if (a.branch < k) {
@@ -122,10 +164,22 @@ __global__ __launch_bounds__(kWave) void tree_build_kernel(TreeArgs a) {
             in = in && sel < a.branch;
         }
         const float sc = Sn + s;
-        const uint32_t o = in ? ord32(sc) : 0u;
-        if (lane < k) s_cord[n * k + lane] = o;
-        c_ord = row0_max_u32_dpp(o);
-        c_rank = __ffsll((unsigned long long)__ballot(in && o == c_ord)) - 1;
+        const uint32_t o = ord32(sc);  // nonzero for every non-NaN score
+        const uint64_t key = in ? (((uint64_t)o << 8) | (uint64_t)(255 - lane)) : 0ull;
+        int pos;
+        if constexpr (KQ)
+            pos = quad_count_greater(key);
+        else
+            pos = row_count_greater<15>(key);
+        // the lanes that are not children all land on the first free position
+        // and write the end marker there
+        if (lane < k) {
+            s_kord[n * k + pos] = in ? o : 0u;
+            s_krank[n * k + pos] = (uint8_t)lane;
+        }
+        const uint64_t first = __ballot(in && pos == 0);
+        c_rank = first ? __ffsll((unsigned long long)first) - 1 : 0;
+        c_ord = first ? (uint32_t)__builtin_amdgcn_readlane((int)o, c_rank) : 0u;
     };
 
     // Rank-path key (four 32-bit words, most significant first) of the child
@@ -156,7 +210,7 @@ __global__ __launch_bounds__(kWave) void tree_build_kernel(TreeArgs a) {
     for (int j = 0; j < SL; ++j) fS[j] = fM[j] = 0u;
     if (lane == 0) {
         fS[0] = c_ord;
-        fM[0] = pack_meta(0, c_rank, 1, 0);
+        fM[0] = pack_meta(0, c_rank, 1, 0, 0);
     }
     int fcount = 1, committed = 1;
 
@@ -211,34 +265,32 @@ __global__ __launch_bounds__(kWave) void tree_build_kernel(TreeArgs a) {
         const uint32_t meta = (uint32_t)__builtin_amdgcn_readlane((int)lmeta, w);
         const int eslot = __builtin_amdgcn_readlane(jsel, w);
         const int p = meta & 1023, r = (meta >> 10) & 15, d = (meta >> 14) & 63, rp = (meta >> 20) & 15;
+        const int pos = (meta >> 24) & 15;
         const float S = unord32(M);
 
         // commit node n: one record; everything else is derived after the search
         const int n = committed++;
         if (lane == 0) s_rec[n] = make_uint2(meta, __float_as_uint(S));
 
-        // next sibling of n under p: the best child of p ordered after n
-        uint32_t o = 0u;
-        bool valid = false;
-        if (lane < k) {
-            o = s_cord[p * k + lane];
-            valid = o != 0u && (o < M || (o == M && lane > r));
-        }
+        // next sibling of n: the next entry of its parent's ordered children
+        // (read unconditionally, at a clamped index, so that its latency
+        // overlaps the expansion's reads)
+        const int si = p * k + min(pos + 1, k - 1);
+        const uint32_t sib_ord = pos + 1 < k ? s_kord[si] : 0u;
+        const int sib_rank = s_krank[si];
         // first child of n
         uint32_t kid_ord = 0u;
         int kid_rank = 0;
         if (d < D) expand(n, d, r, rp, S, kid_ord, kid_rank);
-        const uint32_t sib_ord = row0_max_u32_dpp(valid ? o : 0u);
-        const int sib_rank = __ffsll((unsigned long long)__ballot(valid && o == sib_ord)) - 1;
 
         // pushes: the first reuses the popped slot, the second takes a fresh slot
         uint32_t xS = 0u, xM = 0u, yS = 0u, yM = 0u;
         if (kid_ord != 0u) {
             xS = kid_ord;
-            xM = pack_meta(n, kid_rank, d + 1, r);
+            xM = pack_meta(n, kid_rank, d + 1, r, 0);
         }
         if (sib_ord != 0u) {
-            const uint32_t m = pack_meta(p, sib_rank, d, rp);
+            const uint32_t m = pack_meta(p, sib_rank, d, rp, pos + 1);
             if (xS != 0u) {
                 yS = sib_ord;
                 yM = m;
@@ -264,6 +316,7 @@ __global__ __launch_bounds__(kWave) void tree_build_kernel(TreeArgs a) {
     // the bits of n and of every node on its parent chain (SL words suffice:
     // SL = ceil(N / 64) = W).
     const int64_t ob = (int64_t)b * N;
+    const int root_tok = __builtin_amdgcn_readfirstlane(a.root_token[b]);
     for (int i = lane; i < N; i += kWave) {
         uint64_t words[SL];
 #pragma unroll
@@ -273,7 +326,7 @@ __global__ __launch_bounds__(kWave) void tree_build_kernel(TreeArgs a) {
             const int p = i == 0 ? -1 : (int)(rec.x & 1023);
             const int r = (rec.x >> 10) & 15, d = i == 0 ? 0 : (rec.x >> 14) & 63;
             a.parent[ob + i] = p;
-            a.token[ob + i] = i == 0 ? a.root_token[b] : s_ids[(d - 1) * k + r];
+            a.token[ob + i] = i == 0 ? root_tok : s_ids[(d > 0 ? d - 1 : 0) * k + r];
             a.depth[ob + i] = d;
             a.rank[ob + i] = i == 0 ? -1 : r;
             a.score[ob + i] = __uint_as_float(rec.y);
@@ -308,7 +361,7 @@ static int align16(int x) { return (x + 15) & ~15; }
 
 struct TreeLayout {
     int total_no_rho, total_with_rho;
-    int o_lp, o_ids, o_cord, o_rec, o_rho;
+    int o_lp, o_ids, o_kord, o_krank, o_rec, o_rho;
 };
 
 static TreeLayout tree_layout(int D, int k, int N) {
@@ -316,7 +369,8 @@ static TreeLayout tree_layout(int D, int k, int N) {
     int off = 0;
     L.o_lp = off; off = align16(off + D * k * 4);
     L.o_ids = off; off = align16(off + D * k * 4);
-    L.o_cord = off; off = align16(off + N * k * 4);
+    L.o_kord = off; off = align16(off + N * k * 4);
+    L.o_krank = off; off = align16(off + N * k);
     L.o_rec = off; off = align16(off + N * 8);
     L.total_no_rho = off;
     L.o_rho = off;
@@ -368,17 +422,26 @@ presto_status launch_build_tree(const presto_tree_desc* desc, const int32_t* ids
     a.score = score;
     a.anc = anc;
     const TreeLayout L = tree_layout(a.D, a.k, a.N);
-    a.o_lp = L.o_lp; a.o_ids = L.o_ids; a.o_cord = L.o_cord; a.o_rec = L.o_rec;
+    a.o_lp = L.o_lp; a.o_ids = L.o_ids; a.o_kord = L.o_kord; a.o_krank = L.o_krank; a.o_rec = L.o_rec;
     a.o_rho = L.o_rho;
     a.rho_in_lds = log_rho != nullptr && L.total_with_rho <= kTreeLdsBudget;
     const int lds = a.rho_in_lds ? L.total_with_rho : L.total_no_rho;
     const int SL = (a.N + kWave - 1) / kWave;
-#define PRESTO_TREE(S) tree_build_kernel<S><<<desc->batch, kWave, lds, stream>>>(a)
-    if (SL <= 1) PRESTO_TREE(1);
-    else if (SL <= 2) PRESTO_TREE(2);
-    else if (SL <= 4) PRESTO_TREE(4);
-    else PRESTO_TREE(8);
+    const int rho_mode = log_rho == nullptr ? 0 : (a.rho_in_lds ? 1 : 2);
+#define PRESTO_TREE3(S, R, Q) tree_build_kernel<S, R, Q><<<desc->batch, kWave, lds, stream>>>(a)
+#define PRESTO_TREE2(S, R) \
+    if (a.k <= 4) PRESTO_TREE3(S, R, true); else PRESTO_TREE3(S, R, false)
+#define PRESTO_TREE(S)                      \
+    if (rho_mode == 0) { PRESTO_TREE2(S, 0); } \
+    else if (rho_mode == 1) { PRESTO_TREE2(S, 1); } \
+    else { PRESTO_TREE2(S, 2); }
+    if (SL <= 1) { PRESTO_TREE(1) }
+    else if (SL <= 2) { PRESTO_TREE(2) }
+    else if (SL <= 4) { PRESTO_TREE(4) }
+    else { PRESTO_TREE(8) }
 #undef PRESTO_TREE
+#undef PRESTO_TREE2
+#undef PRESTO_TREE3
     return check_launch("tree_build_kernel");
 }
 
