@@ -5,12 +5,14 @@
 // produces, with no block-level synchronisation:
 //   * the chunk maximum m and sum exp(z - m)           (for the row's LSE)
 //   * the chunk's k best (value desc, id asc) entries  (as 64-bit keys)
-// The k-th largest lane maximum (found by a 32-step ballot bisection on its
-// orderable bits) is a lower bound on the chunk's k-th value, so only entries
-// at or above it are candidates (normally k to 2k of them); they are
-// compacted through a small per-wave LDS list and ranked there.  A chunk
-// with more than kCandCap candidates (massive ties) falls back to k rounds
-// of exact wave-wide selection.  A second kernel, queued right behind,
+// The k-th largest lane maximum (k rounds of wave max, or a ballot bisection
+// on its orderable bits for k > 8) is a lower bound on the chunk's k-th value, so only the
+// 16-byte groups whose maximum reaches it can hold a top-k entry (normally a
+// handful); their entries at or above it are compacted through a small
+// per-wave LDS list and the k best taken by k rounds of wave max.  A chunk
+// with more candidate groups than the list holds (massive ties) falls back
+// to k rounds of exact wave-wide selection over the chunk re-read from
+// memory.  A second kernel, queued right behind,
 // merges each row's chunk partials with one wave per row.
 #include <math.h>
 
@@ -20,6 +22,7 @@ namespace presto {
 
 constexpr int kCandCap = 64;
 constexpr int kTopkWavesPerBlock = 4;
+constexpr float kLog2eF = 1.4426950408889634f;
 
 template <bool BF16>
 struct VecTraits;
@@ -78,9 +81,20 @@ __device__ __forceinline__ void load_chunk(const void* __restrict__ row, int64_t
     }
 }
 
-// The k-th largest value of one u32 per lane (k <= 64): bisection on the
+// The k-th largest value of one u32 per lane (k <= 64).  Small k: k rounds
+// of "wave max, then retire one lane holding it"; larger k: bisection on the
 // bits, counting lanes at or above each probe with a ballot.
 __device__ __forceinline__ uint32_t wave_kth_largest_u32(uint32_t x, int k) {
+    if (k <= 8) {
+        const int lane = lane_id();
+        uint32_t t = 0u;
+        for (int j = 0; j < k; ++j) {
+            t = wave_max_u32_dpp(x);
+            const int l = __ffsll((unsigned long long)__ballot(x == t)) - 1;
+            x = lane == l ? 0u : x;
+        }
+        return t;
+    }
     uint32_t t = 0u;
 #pragma unroll
     for (int bit = 31; bit >= 0; --bit) {
@@ -95,9 +109,10 @@ __global__ __launch_bounds__(kTopkWavesPerBlock * kWave) void topk_partial_kerne
     const void* __restrict__ logits, int64_t rows, int32_t vocab, int64_t row_stride, int32_t k,
     int32_t chunks, bool aligned, float2* __restrict__ part_ms, uint64_t* __restrict__ part_keys,
     int32_t* __restrict__ flags) {
-    constexpr int P = VecTraits<BF16>::kPerVec;
+    constexpr int P = VecTraits<BF16>::kPerVec;  // elements per 16-byte load (a "group")
     constexpr int E = NLOAD * P;
     constexpr int64_t CH = (int64_t)kWave * E;
+    constexpr int kGroupCap = kCandCap / P;      // candidate groups a wave list holds
     __shared__ uint64_t cand[kTopkWavesPerBlock][kCandCap];
     __shared__ uint32_t cand_n[kTopkWavesPerBlock];
 
@@ -113,48 +128,85 @@ __global__ __launch_bounds__(kTopkWavesPerBlock * kWave) void topk_partial_kerne
     float v[E];
     load_chunk<BF16, NLOAD>(rowp, c0, vocab, full, v);
 
-    float lm = -INFINITY;
+    // group maxima (one group = the P elements of one 16-byte load), lane max
+    float gmax[NLOAD];
 #pragma unroll
-    for (int e = 0; e < E; ++e) lm = fmaxf(lm, v[e]);
-    const float M = wave_max_f32_dpp(lm);
-    float s = 0.f;
-    if (M != -INFINITY) {
+    for (int i = 0; i < NLOAD; ++i) {
+        float m = v[i * P];
 #pragma unroll
-        for (int e = 0; e < E; ++e) s += __expf(v[e] - M);
+        for (int j = 1; j < P; ++j) m = fmaxf(m, v[i * P + j]);
+        gmax[i] = m;
     }
-    const float S = wave_sum_f32_dpp(s);
+    float lm = gmax[0];
+#pragma unroll
+    for (int i = 1; i < NLOAD; ++i) lm = fmaxf(lm, gmax[i]);
+    const float M = wave_max_f32_dpp(lm);
+    // For moderate M: exp(z - M) = exp2(fma(z, log2 e, -mo)) * 2^r with
+    // mo = fl(M log2 e) and r = M log2 e - mo taken exactly by one fma (|r| is
+    // below 2^-16 here), so one fma and one exp per entry.  Larger |M| takes
+    // the plain form exp2((z - M) log2 e).
+    float s = 0.f;
+    float corr = 1.f;
+    if (fabsf(M) < 256.f) {
+        const float mo = M * kLog2eF;
+        corr = __builtin_amdgcn_exp2f(fmaf(M, kLog2eF, -mo));
+#pragma unroll
+        for (int e = 0; e < E; ++e) s += __builtin_amdgcn_exp2f(fmaf(v[e], kLog2eF, -mo));
+    } else if (M != -INFINITY) {
+#pragma unroll
+        for (int e = 0; e < E; ++e) s += __builtin_amdgcn_exp2f((v[e] - M) * kLog2eF);
+    }
+    const float S = wave_sum_f32_dpp(s) * corr;
+    // the k-th largest lane maximum bounds the chunk's k-th value from below:
+    // only groups whose maximum reaches it can hold a top-k entry
     const float thr = unord32(wave_kth_largest_u32(ord32(lm), k));
 
     if (lane == 0) cand_n[wave] = 0u;
     __builtin_amdgcn_wave_barrier();
 #pragma unroll
-    for (int e = 0; e < E; ++e) {
-        const int64_t idx = c0 + (int64_t)((e / P) * kWave + lane) * P + (e % P);
-        if (v[e] >= thr && (full || idx < vocab)) {
-            const uint32_t pos = atomicAdd(&cand_n[wave], 1u);
-            if (pos < kCandCap) cand[wave][pos] = vocab_key(v[e], (uint32_t)idx);
+    for (int i = 0; i < NLOAD; ++i) {
+        if (gmax[i] >= thr) {
+            const uint32_t slot = atomicAdd(&cand_n[wave], 1u);
+            if (slot < (uint32_t)kGroupCap) {
+#pragma unroll
+                for (int j = 0; j < P; ++j) {
+                    const int64_t idx = c0 + (int64_t)(i * kWave + lane) * P + j;
+                    const bool ok = (full || idx < vocab) && v[i * P + j] >= thr;
+                    cand[wave][slot * P + j] = ok ? vocab_key(v[i * P + j], (uint32_t)idx) : 0ull;
+                }
+            }
         }
     }
     __builtin_amdgcn_wave_barrier();
-    const uint32_t total = __builtin_amdgcn_readfirstlane(cand_n[wave]);
+    const uint32_t ngroups = __builtin_amdgcn_readfirstlane(cand_n[wave]);
     uint64_t* out = part_keys + gw * k;
 
-    if (total <= (uint32_t)kCandCap) {
-        const uint64_t mine = lane < (int)total ? cand[wave][lane] : 0ull;
-        int rank = 0;
-        for (uint32_t j = 0; j < total; ++j) rank += cand[wave][j] > mine ? 1 : 0;
-        if (lane < (int)total && rank < k) out[rank] = mine;
-        if (lane >= (int)total && lane < k) out[lane] = 0ull;
+    if (ngroups <= (uint32_t)kGroupCap) {
+        // one candidate key per lane (keys are unique); k rounds of wave max,
+        // retiring the lane that held it (0 past the last valid entry)
+        const int total = (int)ngroups * P;
+        uint64_t x = lane < total ? cand[wave][lane] : 0ull;
+        uint64_t mine = 0ull;
+        for (int j = 0; j < k; ++j) {
+            const uint64_t m = wave_max_u64_dpp(x);
+            mine = lane == j ? m : mine;
+            x = x == m ? 0ull : x;
+        }
+        if (lane < k) out[lane] = mine;
     } else {
-        // exact selection: k rounds of "largest key below the last one"
+        // massive ties: exact selection, k rounds of "largest key below the
+        // last one", re-reading the chunk from memory (rare; keeps the
+        // register copy of the chunk out of this path)
         uint64_t last = ~0ull;
         for (int j = 0; j < k; ++j) {
             uint64_t best = 0ull;
-#pragma unroll
+#pragma unroll 1
             for (int e = 0; e < E; ++e) {
                 const int64_t idx = c0 + (int64_t)((e / P) * kWave + lane) * P + (e % P);
-                if (full || idx < vocab) {
-                    const uint64_t key = vocab_key(v[e], (uint32_t)idx);
+                if (idx < vocab) {
+                    const float x = BF16 ? bf16_to_f(reinterpret_cast<const uint16_t*>(rowp)[idx])
+                                         : reinterpret_cast<const float*>(rowp)[idx];
+                    const uint64_t key = vocab_key(x, (uint32_t)idx);
                     if (key < last && key > best) best = key;
                 }
             }
@@ -234,7 +286,8 @@ using namespace presto;
 static int topk_nload(bool bf16, int64_t rows, int32_t vocab) {
     const int64_t ch8 = (int64_t)kWave * 8 * (bf16 ? 8 : 4);
     const int64_t waves8 = rows * ((vocab + ch8 - 1) / ch8);
-    return waves8 >= 4 * 256 * 4 ? 8 : 4;
+    // 8 loads per lane only when that still leaves >= 16 waves per CU
+    return waves8 >= 16 * 256 ? 8 : 4;
 }
 
 size_t topk_workspace_bytes(int64_t rows, int32_t vocab, int32_t k) {
