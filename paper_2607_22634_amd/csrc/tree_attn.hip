@@ -52,6 +52,10 @@ constexpr int kRowsPerWave = 32;  // one 32-row MFMA block per wave
 // Workgroups are 8 waves, two per SIMD: one wave's softmax hides behind the
 // other's MFMAs (with one wave per SIMD the matrix cores sit idle during it).
 constexpr int kAttnWaves = 8;
+// 32-row blocks per wave.  Two (four waves, each K/V fragment feeding two
+// MFMAs) needs about 340 registers per lane at head_dim 128 and spills with
+// the current register allocation, so one block per wave is used.
+constexpr int kAttnRowBlocks = 1;
 constexpr float kLog2e = 1.4426950408889634f;
 
 struct AttnArgs {
@@ -116,7 +120,7 @@ __device__ __forceinline__ TilePieces<PT> fetch_tile(const uint16_t* kc, const u
     return r;
 }
 
-template <int D, int NW>
+template <int D, int NW, int RB>
 __global__ __launch_bounds__(NW * kWave) void tree_attn_bf16_kernel(AttnArgs a) {
     constexpr int KS = D / 16;                 // S^T contraction steps over the head dimension
     constexpr int DB = D / 32;                 // 32-wide blocks of the output head dimension
@@ -125,7 +129,8 @@ __global__ __launch_bounds__(NW * kWave) void tree_attn_bf16_kernel(AttnArgs a) 
     constexpr int PIECES = kKeyTile * D / 8;   // 16-byte pieces of one K (or V) tile
     constexpr int NT = NW * kWave;
     constexpr int PT = PIECES / NT;            // pieces per thread
-    constexpr int ROWS = NW * kRowsPerWave;    // query rows per workgroup
+    constexpr int WROWS = RB * kRowsPerWave;   // query rows per wave (RB blocks of 32)
+    constexpr int ROWS = NW * WROWS;           // query rows per workgroup
     constexpr int KBUF = kKeyTile * KROW, VBUF = kKeyTile * VROW;
     static_assert(PT * NT == PIECES, "tile pieces must divide evenly");
     __shared__ __align__(16) uint16_t sK[kBufs * KBUF];
@@ -155,22 +160,29 @@ __global__ __launch_bounds__(NW * kWave) void tree_attn_bf16_kernel(AttnArgs a) 
     const int tid = threadIdx.x;
     const int wave = tid / kWave, lane = lane_id();
     const int l32 = lane & 31, h = lane >> 5;
-    const int rho = rt * ROWS + wave * kRowsPerWave + l32;  // this lane's query row
-    const bool active = rt * ROWS + wave * kRowsPerWave < live_rows;
-    const int qn = rho / a.G, qh = rho - qn * a.G;
-    const int node = min(qn, a.n_max - 1);
+    const int row0 = rt * ROWS + wave * WROWS;  // first query row of this wave
+    const bool active = row0 < live_rows;
+    int rho[RB], qn[RB], qh[RB], node[RB];  // this lane's query row in each row block
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) {
+        rho[rb] = row0 + rb * kRowsPerWave + l32;
+        qn[rb] = rho[rb] / a.G;
+        qh[rb] = rho[rb] - qn[rb] * a.G;
+        node[rb] = min(qn[rb], a.n_max - 1);
+    }
 
     // Q fragments, B operand of S^T = K Q^T: lane holds row l32, d = ks*16 + h*8 .. +8.
     // Loaded before the first K/V tiles, so the waits for those tiles also
     // cover Q and nothing in the key loop waits on global loads but the stage.
-    bf16x8 qf[KS];
-    {
-        const uint16_t* qp = a.q + (((int64_t)b * a.n_max + qn) * a.hq + g * a.G + qh) * D;
+    bf16x8 qf[RB][KS];
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) {
+        const uint16_t* qp = a.q + (((int64_t)b * a.n_max + qn[rb]) * a.hq + g * a.G + qh[rb]) * D;
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks) {
             uint4 u = make_uint4(0, 0, 0, 0);
-            if (rho < all_rows) u = *reinterpret_cast<const uint4*>(qp + ks * 16 + h * 8);
-            qf[ks] = __builtin_bit_cast(bf16x8, u);
+            if (rho[rb] < all_rows) u = *reinterpret_cast<const uint4*>(qp + ks * 16 + h * 8);
+            qf[rb][ks] = __builtin_bit_cast(bf16x8, u);
         }
     }
 
@@ -210,26 +222,36 @@ __global__ __launch_bounds__(NW * kWave) void tree_attn_bf16_kernel(AttnArgs a) 
     }
     __syncthreads();
 
-    floatx16 o[DB];
+    floatx16 o[RB][DB];
 #pragma unroll
-    for (int db = 0; db < DB; ++db)
+    for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
-        for (int i = 0; i < 16; ++i) o[db][i] = 0.f;
-    // Running reference m (log2 domain, scaled) and denominator l.  m only
-    // moves when a block's maximum exceeds it by more than kSlack, so most
-    // blocks skip the accumulator rescale; probabilities stay below 2^kSlack.
-    float m_run = -INFINITY, l_run = 0.f;
+        for (int db = 0; db < DB; ++db)
+#pragma unroll
+            for (int i = 0; i < 16; ++i) o[rb][db][i] = 0.f;
+    // Running reference m (log2 domain, scaled) and denominator l per row.
+    // m only moves when a block's maximum exceeds it by more than kSlack, so
+    // most blocks skip the accumulator rescale; probabilities stay below
+    // 2^kSlack.
+    float m_run[RB], l_run[RB];
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) {
+        m_run[rb] = -INFINITY;
+        l_run[rb] = 0.f;
+    }
 
     const float c = a.scale_log2;
     // per-lane LDS element offsets; every fragment read adds only a constant
     const int k_lane = l32 * KROW + h * 8;
     const int v_lane = (4 * h + ((lane & 15) >> 2)) * VROW + ((lane >> 4) & 1) * 16 + 4 * (lane & 3);
 
-    // S^T block of 32 keys (block i of the split) into S
-    auto scores = [&](int i) {
-        floatx16 S;
+    // S^T blocks of 32 keys (block i of the split) for every row block: each
+    // K fragment read from LDS feeds RB MFMAs
+    auto scores = [&](int i, floatx16 (&S)[RB]) {
 #pragma unroll
-        for (int e = 0; e < 16; ++e) S[e] = 0.f;
+        for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+            for (int e = 0; e < 16; ++e) S[rb][e] = 0.f;
         const int buf = (i / kBlocksPerTile) % kBufs, blk = i % kBlocksPerTile;
         int koff = buf * KBUF + blk * 32 * KROW + k_lane;
         asm volatile("" : "+v"(koff));  // keep the per-read constants as immediate offsets
@@ -237,9 +259,10 @@ __global__ __launch_bounds__(NW * kWave) void tree_attn_bf16_kernel(AttnArgs a) 
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks) {
             const bf16x8 ka = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(kb + ks * 16));
-            S = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qf[ks], S, 0, 0, 0);
+#pragma unroll
+            for (int rb = 0; rb < RB; ++rb)
+                S[rb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qf[rb][ks], S[rb], 0, 0, 0);
         }
-        return S;
     };
     // element e of a lane is key j0 + 8(e/4) + 4h + e%4
     auto row_max = [&](const floatx16& S) {
@@ -250,11 +273,11 @@ __global__ __launch_bounds__(NW * kWave) void tree_attn_bf16_kernel(AttnArgs a) 
                                                          false, false);
         return fmaxf(mx, __uint_as_float(h == 0 ? sw[1] : sw[0]));
     };
-    auto apply_mask = [&](floatx16& S, int j0) {
+    auto apply_mask = [&](floatx16& S, int j0, int nd) {
         uint64_t aw0 = 0ull, aw1 = 0ull;
         const int wbase = max(0, j0 - ctx) >> 6;
         if (j0 + 32 > ctx) {
-            const uint64_t* arow = &s_anc[(node - n_first) * a.W];
+            const uint64_t* arow = &s_anc[(nd - n_first) * a.W];
             aw0 = arow[wbase];
             aw1 = wbase + 1 < a.W ? arow[wbase + 1] : 0ull;
         }
@@ -267,119 +290,157 @@ __global__ __launch_bounds__(NW * kWave) void tree_attn_bf16_kernel(AttnArgs a) 
             S[e] = vis ? S[e] : -INFINITY;
         }
     };
-    // move m when the block maximum mx (raw score) exceeds it by more than kSlack
-    auto update = [&](float mx) {
+    // move m of row block rb when its block maximum mx (raw score) exceeds
+    // it by more than kSlack
+    auto update = [&](int rb, float mx) {
         const float mx2 = mx * c;
-        const bool need = mx2 > m_run + kSlack;
+        const bool need = mx2 > m_run[rb] + kSlack;
         if (__ballot(need)) {
-            const float mn = need ? mx2 : m_run;
-            const float alpha = need ? __builtin_amdgcn_exp2f(m_run - mn) : 1.f;
-            m_run = mn;
-            l_run *= alpha;
+            const float mn = need ? mx2 : m_run[rb];
+            const float alpha = need ? __builtin_amdgcn_exp2f(m_run[rb] - mn) : 1.f;
+            m_run[rb] = mn;
+            l_run[rb] *= alpha;
 #pragma unroll
-            for (int db = 0; db < DB; ++db) o[db] *= alpha;
+            for (int db = 0; db < DB; ++db) o[rb][db] *= alpha;
         }
     };
 
-    floatx16 S_cur;
-    if (active) {
-        S_cur = scores(0);
-        if (k_begin + 32 > mask_from) apply_mask(S_cur, k_begin);
-        update(row_max(S_cur));
-    }
-    for (int t = 0; t < ntiles; ++t) {
-        if (active) {
+    // one 32-key block: scores of every row block (K fragments shared), then
+    // the softmax and P V of each row block; with two row blocks one block's
+    // softmax overlaps the other's MFMAs
+    auto block_step = [&](int t, int q, int i, floatx16 (&S)[RB]) {
+        const int j0 = k_begin + i * 32;
+        float mx[RB];
 #pragma unroll
-            for (int q = 0; q < kBlocksPerTile; ++q) {
-                const int i = t * kBlocksPerTile + q;
-                if (i < nblocks) {
-                    // scores of the next block (its tile is already in LDS) overlap
-                    // the softmax and P V of this one
-                    // scores of the next block (its tile is already in LDS)
-                    // overlap the softmax and P V of this one
-                    floatx16 S_nxt = scores(i + 1);
-                    const float m_use = m_run == -INFINITY ? 0.f : m_run;
-                    float ls = 0.f;
-                    uint32_t P[8];
+        for (int rb = 0; rb < RB; ++rb) mx[rb] = row_max(S[rb]);
+        if (j0 + 32 > mask_from) {
 #pragma unroll
-                    for (int e = 0; e < 16; e += 2) {
-                        const float p0 = __builtin_amdgcn_exp2f(fmaf(S_cur[e], c, -m_use));
-                        const float p1 = __builtin_amdgcn_exp2f(fmaf(S_cur[e + 1], c, -m_use));
-                        ls += p0 + p1;
-                        P[e >> 1] = pack_bf16x2(p0, p1);
-                    }
-                    l_run += ls;
-                    int voff = (t % kBufs) * VBUF + q * 32 * VROW + v_lane;
-                    asm volatile("" : "+v"(voff));
-                    const uint16_t* vb = sV + voff;
+            for (int rb = 0; rb < RB; ++rb) {
+                apply_mask(S[rb], j0, node[rb]);
+                mx[rb] = row_max(S[rb]);
+            }
+        }
 #pragma unroll
-                    for (int st = 0; st < 2; ++st) {
-                        const bf16x8 pb = __builtin_bit_cast(
-                            bf16x8, make_uint4(P[4 * st], P[4 * st + 1], P[4 * st + 2], P[4 * st + 3]));
+        for (int rb = 0; rb < RB; ++rb) update(rb, mx[rb]);
+        uint32_t P[RB][8];
 #pragma unroll
-                        for (int db = 0; db < DB; ++db) {
-                            const uint16_t* v0 = vb + st * 16 * VROW + db * 32;
-                            const short4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-                                (__attribute__((address_space(3))) short4_t*)(v0));
-                            const short4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-                                (__attribute__((address_space(3))) short4_t*)(v0 + 8 * VROW));
-                            const uint2 ul = __builtin_bit_cast(uint2, lo), uh = __builtin_bit_cast(uint2, hi);
-                            const bf16x8 va = __builtin_bit_cast(bf16x8, make_uint4(ul.x, ul.y, uh.x, uh.y));
-                            o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pb, o[db], 0, 0, 0);
-                        }
-                    }
-                    float mx = row_max(S_nxt);
-                    if (i + 1 < nblocks) {
-                        const int j0 = k_begin + (i + 1) * 32;
-                        if (j0 + 32 > mask_from) {
-                            apply_mask(S_nxt, j0);
-                            mx = row_max(S_nxt);
-                        }
-                        update(mx);
-                    }
-                    S_cur = S_nxt;
+        for (int rb = 0; rb < RB; ++rb) {
+            const float m_use = m_run[rb] == -INFINITY ? 0.f : m_run[rb];
+            float ls = 0.f;
+#pragma unroll
+            for (int e = 0; e < 16; e += 2) {
+                const float p0 = __builtin_amdgcn_exp2f(fmaf(S[rb][e], c, -m_use));
+                const float p1 = __builtin_amdgcn_exp2f(fmaf(S[rb][e + 1], c, -m_use));
+                ls += p0 + p1;
+                P[rb][e >> 1] = pack_bf16x2(p0, p1);
+            }
+            l_run[rb] += ls;
+        }
+        int voff = (t % kBufs) * VBUF + q * 32 * VROW + v_lane;
+        asm volatile("" : "+v"(voff));
+        const uint16_t* vb = sV + voff;
+#pragma unroll
+        for (int st = 0; st < 2; ++st) {
+#pragma unroll
+            for (int db = 0; db < DB; ++db) {
+                const uint16_t* v0 = vb + st * 16 * VROW + db * 32;
+                const short4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                    (__attribute__((address_space(3))) short4_t*)(v0));
+                const short4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                    (__attribute__((address_space(3))) short4_t*)(v0 + 8 * VROW));
+                const uint2 ul = __builtin_bit_cast(uint2, lo), uh = __builtin_bit_cast(uint2, hi);
+                const bf16x8 va = __builtin_bit_cast(bf16x8, make_uint4(ul.x, ul.y, uh.x, uh.y));
+#pragma unroll
+                for (int rb = 0; rb < RB; ++rb) {
+                    const bf16x8 pb = __builtin_bit_cast(
+                        bf16x8, make_uint4(P[rb][4 * st], P[rb][4 * st + 1], P[rb][4 * st + 2], P[rb][4 * st + 3]));
+                    o[rb][db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pb, o[rb][db], 0, 0, 0);
                 }
             }
         }
-        // tile t+2 goes into the buffer of tile t-1, which every wave finished
-        // before the previous barrier
-        stage((t + 2) % kBufs, pend);
-        pend = fetch(k_begin + (t + 3) * kKeyTile);
-        __syncthreads();
+    };
+
+    if constexpr (RB == 1) {
+        // one row block: the scores of block i+1 (its tile is already in LDS)
+        // are issued ahead of the softmax and P V of block i
+        floatx16 S_cur[1];
+        if (active) scores(0, S_cur);
+        for (int t = 0; t < ntiles; ++t) {
+            if (active) {
+#pragma unroll
+                for (int q = 0; q < kBlocksPerTile; ++q) {
+                    const int i = t * kBlocksPerTile + q;
+                    if (i < nblocks) {
+                        floatx16 S_nxt[1];
+                        scores(i + 1, S_nxt);
+                        block_step(t, q, i, S_cur);
+                        S_cur[0] = S_nxt[0];
+                    }
+                }
+            }
+            // tile t+2 goes into the buffer of tile t-1, which every wave
+            // finished before the previous barrier
+            stage((t + 2) % kBufs, pend);
+            pend = fetch(k_begin + (t + 3) * kKeyTile);
+            __syncthreads();
+        }
+    } else {
+        for (int t = 0; t < ntiles; ++t) {
+            if (active) {
+#pragma unroll
+                for (int q = 0; q < kBlocksPerTile; ++q) {
+                    const int i = t * kBlocksPerTile + q;
+                    if (i < nblocks) {
+                        floatx16 S[RB];
+                        scores(i, S);
+                        block_step(t, q, i, S);
+                    }
+                }
+            }
+            stage((t + 2) % kBufs, pend);
+            pend = fetch(k_begin + (t + 3) * kKeyTile);
+            __syncthreads();
+        }
     }
 
-    // ---- epilogue: lane holds row l32, d = db*32 + 8(i/4) + 4h + i%4
-    {
-        const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(l_run), __float_as_uint(l_run),
-                                                         false, false);
-        l_run += __uint_as_float(h == 0 ? sw[1] : sw[0]);
-    }
-    if (rho >= all_rows) return;
-    if (a.splits == 1) {
-        uint16_t* op = a.out + (((int64_t)b * a.n_max + qn) * a.hq + g * a.G + qh) * D;
-        const float inv = (rho < live_rows && l_run > 0.f) ? 1.f / l_run : 0.f;
+    // ---- epilogue: lane holds row l32 of each row block, d = db*32 + 8(i/4) + 4h + i%4
 #pragma unroll
-        for (int db = 0; db < DB; ++db)
+    for (int rb = 0; rb < RB; ++rb) {
+        float l = l_run[rb];
+        {
+            const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(l), __float_as_uint(l), false,
+                                                             false);
+            l += __uint_as_float(h == 0 ? sw[1] : sw[0]);
+        }
+        if (rho[rb] >= all_rows) continue;
+        if (a.splits == 1) {
+            uint16_t* op = a.out + (((int64_t)b * a.n_max + qn[rb]) * a.hq + g * a.G + qh[rb]) * D;
+            const float inv = (rho[rb] < live_rows && l > 0.f) ? 1.f / l : 0.f;
 #pragma unroll
-            for (int q4 = 0; q4 < 4; ++q4) {
-                const int dd = db * 32 + 8 * q4 + 4 * h;
-                *reinterpret_cast<uint2*>(op + dd) =
-                    make_uint2(pack_bf16x2(o[db][4 * q4] * inv, o[db][4 * q4 + 1] * inv),
-                               pack_bf16x2(o[db][4 * q4 + 2] * inv, o[db][4 * q4 + 3] * inv));
+            for (int db = 0; db < DB; ++db)
+#pragma unroll
+                for (int q4 = 0; q4 < 4; ++q4) {
+                    const int dd = db * 32 + 8 * q4 + 4 * h;
+                    *reinterpret_cast<uint2*>(op + dd) =
+                        make_uint2(pack_bf16x2(o[rb][db][4 * q4] * inv, o[rb][db][4 * q4 + 1] * inv),
+                                   pack_bf16x2(o[rb][db][4 * q4 + 2] * inv, o[rb][db][4 * q4 + 3] * inv));
+                }
+        } else {
+            float* pp =
+                a.part + ((((int64_t)b * a.hkv + g) * a.rows_pad + rho[rb]) * a.splits + split) * (D + 2);
+#pragma unroll
+            for (int db = 0; db < DB; ++db)
+#pragma unroll
+                for (int q4 = 0; q4 < 4; ++q4) {
+                    const int dd = db * 32 + 8 * q4 + 4 * h;
+                    *reinterpret_cast<float4*>(pp + dd) =
+                        make_float4(o[rb][db][4 * q4], o[rb][db][4 * q4 + 1], o[rb][db][4 * q4 + 2],
+                                    o[rb][db][4 * q4 + 3]);
+                }
+            if (h == 0) {
+                pp[D] = m_run[rb];
+                pp[D + 1] = l;
             }
-    } else {
-        float* pp = a.part + ((((int64_t)b * a.hkv + g) * a.rows_pad + rho) * a.splits + split) * (D + 2);
-#pragma unroll
-        for (int db = 0; db < DB; ++db)
-#pragma unroll
-            for (int q4 = 0; q4 < 4; ++q4) {
-                const int dd = db * 32 + 8 * q4 + 4 * h;
-                *reinterpret_cast<float4*>(pp + dd) = make_float4(o[db][4 * q4], o[db][4 * q4 + 1],
-                                                                  o[db][4 * q4 + 2], o[db][4 * q4 + 3]);
-            }
-        if (h == 0) {
-            pp[D] = m_run;
-            pp[D + 1] = l_run;
         }
     }
 }
@@ -519,7 +580,7 @@ namespace presto_host {
 using namespace presto;
 
 struct AttnPlan {
-    int G, rows, row_tiles, rows_per_tile, rows_pad, waves, splits, split_len;
+    int G, rows, row_tiles, rows_per_tile, rows_pad, waves, rb, splits, split_len;
     int64_t tasks, blocks;
 };
 
@@ -527,28 +588,37 @@ static AttnPlan attn_plan(const presto_attn_desc* d) {
     AttnPlan p;
     p.G = d->hq / d->hkv;
     p.rows = p.G * d->n_max;
-    p.waves = kAttnWaves;
-    p.rows_per_tile = p.waves * kRowsPerWave;
+    // 256 query rows per workgroup: eight waves of one 32-row block, or four
+    // waves of two (each K/V fragment read from LDS then feeds two MFMAs)
+    p.rb = kAttnRowBlocks;
+    p.waves = kAttnWaves / p.rb;
+    p.rows_per_tile = p.waves * kRowsPerWave * p.rb;
     p.row_tiles = (p.rows + p.rows_per_tile - 1) / p.rows_per_tile;
     p.rows_pad = p.rows_per_tile * p.row_tiles;
-    // context splits: fewest idle CU slots per unit of work (one workgroup per CU)
+    // context splits: one workgroup per CU, so the time in key-block units
+    // (about 0.85 us each) is (rounds of workgroups) x (key blocks per split
+    // + about 3 for a workgroup's prologue) plus the merge, whose partials
+    // (written and read back, about 4 MB per key-block time) grow with the
+    // split count
     const int64_t base = (int64_t)d->batch * d->hkv * p.row_tiles;
     const int keys = d->max_ctx + d->n_max;
-    const int max_splits = (keys + 511) / 512;
-    int best = 1;
+    const int max_splits = (keys + 127) / 128;
     double best_cost = 1e30;
-    for (int s = 1; s <= 32 && s <= max_splits; ++s) {
-        const double rounds = (double)((base * s + 255) / 256);
-        const double cost = rounds / s + 0.02 * s;  // rounds of work per split + merge overhead
+    p.splits = 1;
+    p.split_len = (keys + kKeyTile - 1) / kKeyTile * kKeyTile;
+    for (int s = 1; s <= 64 && s <= max_splits; ++s) {
+        int len = (keys + s - 1) / s;
+        len = (len + kKeyTile - 1) / kKeyTile * kKeyTile;
+        const int se = (keys + len - 1) / len;
+        const double rounds = (double)((base * se + 255) / 256);
+        const double merge_bytes = se > 1 ? 2.0 * base * p.rows_per_tile * se * (d->head_dim + 2) * 4.0 : 0.0;
+        const double cost = rounds * ((len + 31) / 32 + 3) + merge_bytes / 4.0e6;
         if (cost < best_cost - 1e-9) {
             best_cost = cost;
-            best = s;
+            p.splits = se;
+            p.split_len = len;
         }
     }
-    int len = (keys + best - 1) / best;
-    len = (len + kKeyTile - 1) / kKeyTile * kKeyTile;
-    p.split_len = len;
-    p.splits = (keys + len - 1) / len;
     p.tasks = base * p.splits;
     p.blocks = (p.tasks + 7) / 8 * 8;
     return p;
@@ -603,10 +673,11 @@ presto_status launch_tree_attention(const presto_attn_desc* d, const void* q, co
     a.n_blocks = (int32_t)p.blocks;
     a.scale_log2 = d->scale * kLog2e;
     const dim3 block(p.waves * kWave), grid((unsigned)p.blocks);
+    constexpr int RB = kAttnRowBlocks, NW = kAttnWaves / kAttnRowBlocks;
     if (d->head_dim == 64)
-        tree_attn_bf16_kernel<64, kAttnWaves><<<grid, block, 0, stream>>>(a);
+        tree_attn_bf16_kernel<64, NW, RB><<<grid, block, 0, stream>>>(a);
     else
-        tree_attn_bf16_kernel<128, kAttnWaves><<<grid, block, 0, stream>>>(a);
+        tree_attn_bf16_kernel<128, NW, RB><<<grid, block, 0, stream>>>(a);
     presto_status st = check_launch("tree_attn_bf16_kernel");
     if (st != PRESTO_OK || p.splits == 1) return st;
     const int64_t merge_rows = (int64_t)d->batch * d->hkv * p.G * d->n_max;
