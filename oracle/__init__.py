@@ -20,6 +20,7 @@ _LIB = None
 
 BEST_FIRST = 0
 BEST_FIRST_ALG2 = 1
+BEAM = 2
 
 
 def lib():
@@ -70,8 +71,9 @@ def topk(logits: np.ndarray, k: int, dtype: str):
 
 
 def build_tree(ids, logprob, rho, lam, root_token, depth: int, k: int, budget: int,
-               branch: int | None = None, mode: int = BEST_FIRST) -> dict:
-    """Best-first tree per sequence; ids/logprob [b, D, k], rho [b, D, k, k, k] or None."""
+               branch: int | None = None, mode: int = BEST_FIRST, beam_width: int = 0) -> dict:
+    """Tree per sequence (best-first, literal Alg. 2, or beam search with beam
+    width `beam_width`); ids/logprob [b, D, k], rho [b, D, k, k, k] or None."""
     branch = k if branch is None else branch
     ids = np.ascontiguousarray(ids, np.int32)
     logprob = np.ascontiguousarray(logprob, np.float32)
@@ -90,7 +92,8 @@ def build_tree(ids, logprob, rho, lam, root_token, depth: int, k: int, budget: i
     f = lib().oracle_build_tree
     f.restype = ctypes.c_int
     rc = f(ctypes.c_int(mode), ctypes.c_int32(b), ctypes.c_int32(depth), ctypes.c_int32(k),
-           ctypes.c_int32(branch), ctypes.c_int32(budget), _p(ids), _p(logprob), _p(rho), _p(lam),
+           ctypes.c_int32(branch), ctypes.c_int32(budget), ctypes.c_int32(beam_width), _p(ids),
+           _p(logprob), _p(rho), _p(lam),
            _p(root_token), _p(out["n_nodes"]), _p(out["parent"]), _p(out["token"]),
            _p(out["depth"]), _p(out["rank"]), _p(out["score"]), _p(out["anc"]))
     if rc != 0:

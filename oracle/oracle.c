@@ -321,16 +321,68 @@ static int build_alg2(const seqctx *c, int32_t budget, int32_t root_token, onode
     return keep + 1;
 }
 
+/* Alg. 1, beam search with global retention: the beam starts as {root}; at
+ * each depth every beam node is expanded (its top-`branch` children join T
+ * and the candidate set), and the W best candidates in the total order form
+ * the next beam.  Depths are taken while T holds fewer than `budget`
+ * non-root nodes (checked before each depth), at most D of them.  The result
+ * is TopB(T): the `budget` best nodes of T (with the root), in the total
+ * order.  T is prefix-closed, so TopB(T) is too. */
+static int build_beam(const seqctx *c, int32_t budget, int32_t W, int32_t root_token,
+                      onode *nodes, onode *T, int32_t *beam, int32_t *cand, int *order,
+                      int32_t *remap) {
+    onode root;
+    memset(&root, 0, sizeof(root));
+    root.parent = -1;
+    root.token = root_token;
+    int nT = 0, nbeam = 1;
+    beam[0] = -1; /* -1 = the root; T entries reference parents as T indices */
+    for (int d = 1; d <= c->D && nT < budget && nbeam > 0; ++d) {
+        int ncand = 0;
+        for (int i = 0; i < nbeam; ++i) {
+            const int v_index = beam[i];
+            const onode *v = v_index < 0 ? &root : &T[v_index];
+            const onode *vp = (v_index < 0 || v->parent < 0) ? &root : &T[v->parent];
+            const int nk = expand(c, v, v_index, vp, &T[nT]);
+            for (int j = 0; j < nk; ++j) cand[ncand++] = nT + j;
+            nT += nk;
+        }
+        qsort_r(cand, (size_t)ncand, sizeof(int32_t), cmp_index_by_order, T);
+        nbeam = ncand < W ? ncand : W;
+        for (int i = 0; i < nbeam; ++i) beam[i] = cand[i];
+    }
+    for (int i = 0; i < nT; ++i) order[i] = i;
+    qsort_r(order, (size_t)nT, sizeof(int), cmp_index_by_order, T);
+    const int keep = nT < budget ? nT : budget;
+    nodes[0] = root;
+    for (int i = 0; i < nT; ++i) remap[i] = -2;
+    for (int i = 0; i < keep; ++i) remap[order[i]] = i + 1;
+    for (int i = 0; i < keep; ++i) {
+        nodes[i + 1] = T[order[i]];
+        const int p = T[order[i]].parent;
+        nodes[i + 1].parent = p < 0 ? 0 : remap[p];
+    }
+    return keep + 1;
+}
+
 int oracle_build_tree(int mode, int32_t batch, int32_t depth, int32_t k, int32_t branch,
-                      int32_t budget, const int32_t *ids, const float *logprob,
+                      int32_t budget, int32_t beam_width, const int32_t *ids, const float *logprob,
                       const float *log_rho, const float *lambda, const int32_t *root_token,
                       int32_t *n_nodes, int32_t *parent, int32_t *token, int32_t *depth_out,
                       int32_t *rank, float *score, uint64_t *anc) {
     if (depth < 1 || depth > MAXD || k < 1 || k > 64 || branch < 1 || branch > k || budget < 1)
         return -1;
-    if (mode != ORACLE_BEST_FIRST && mode != ORACLE_BEST_FIRST_ALG2) return -1;
+    if (mode != ORACLE_BEST_FIRST && mode != ORACLE_BEST_FIRST_ALG2 && mode != ORACLE_BEAM) return -1;
+    if (mode == ORACLE_BEAM && beam_width < 1) return -1;
     const int32_t N = budget + 1, W = (N + 63) / 64;
-    const int64_t cap = (int64_t)budget * branch + branch + 1;
+    /* T capacity: best-first and Alg. 2 add at most `branch` nodes per pop; beam
+     * search adds at most W * branch per depth and exceeds the budget by at most
+     * one depth's worth */
+    int64_t cap = (int64_t)budget * branch + branch + 1;
+    if (mode == ORACLE_BEAM) {
+        const int64_t beam_cap = (int64_t)budget + (int64_t)beam_width * branch + 1;
+        if (beam_cap > cap) cap = beam_cap;
+    }
     int err = 0;
 #pragma omp parallel for schedule(dynamic, 1) reduction(| : err)
     for (int b = 0; b < batch; ++b) {
@@ -340,14 +392,20 @@ int oracle_build_tree(int mode, int32_t batch, int32_t depth, int32_t k, int32_t
         onode *pool = (onode *)malloc(sizeof(onode) * (size_t)(cap + branch));
         onode *kids = (onode *)malloc(sizeof(onode) * (size_t)branch);
         int32_t *fidx = (int32_t *)malloc(sizeof(int32_t) * (size_t)(cap + branch));
+        int32_t *beam = (int32_t *)malloc(sizeof(int32_t) * (size_t)(beam_width > 0 ? beam_width : 1));
         int *order = (int *)malloc(sizeof(int) * (size_t)(cap + branch));
         int32_t *remap = (int32_t *)malloc(sizeof(int32_t) * (size_t)(cap + branch));
-        if (!nodes || !pool || !kids || !fidx || !order || !remap) {
+        if (!nodes || !pool || !kids || !fidx || !order || !remap || !beam) {
             err |= 1;
         } else {
-            int n = mode == ORACLE_BEST_FIRST
-                        ? build_best_first(&c, budget, root_token[b], nodes, pool, kids)
-                        : build_alg2(&c, budget, root_token[b], nodes, pool, fidx, order, remap);
+            int n;
+            if (mode == ORACLE_BEST_FIRST)
+                n = build_best_first(&c, budget, root_token[b], nodes, pool, kids);
+            else if (mode == ORACLE_BEST_FIRST_ALG2)
+                n = build_alg2(&c, budget, root_token[b], nodes, pool, fidx, order, remap);
+            else
+                n = build_beam(&c, budget, beam_width, root_token[b], nodes, pool, beam, fidx, order,
+                               remap);
             write_tree(nodes, n, N, W, &n_nodes[b], parent + (int64_t)b * N, token + (int64_t)b * N,
                        depth_out + (int64_t)b * N, rank + (int64_t)b * N, score + (int64_t)b * N,
                        anc + (int64_t)b * N * W);
@@ -356,6 +414,7 @@ int oracle_build_tree(int mode, int32_t batch, int32_t depth, int32_t k, int32_t
         free(pool);
         free(kids);
         free(fidx);
+        free(beam);
         free(order);
         free(remap);
     }

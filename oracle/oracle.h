@@ -17,7 +17,7 @@ extern "C" {
 #endif
 
 enum { ORACLE_BF16 = 0, ORACLE_F32 = 1 };
-enum { ORACLE_BEST_FIRST = 0, ORACLE_BEST_FIRST_ALG2 = 1 };
+enum { ORACLE_BEST_FIRST = 0, ORACLE_BEST_FIRST_ALG2 = 1, ORACLE_BEAM = 2 };
 
 void oracle_set_threads(int n);
 int oracle_get_threads(void);
@@ -30,7 +30,7 @@ int oracle_topk(int dtype, const void *logits, int64_t rows, int32_t vocab, int6
 /* Prefix-aligned scoring (Eq. 9) and best-first tree construction (Sec. 4.2).
  * Returns 0, or -1 on an argument the oracle cannot represent. */
 int oracle_build_tree(int mode, int32_t batch, int32_t depth, int32_t k, int32_t branch,
-                      int32_t budget, const int32_t *ids, const float *logprob,
+                      int32_t budget, int32_t beam_width, const int32_t *ids, const float *logprob,
                       const float *log_rho, const float *lambda, const int32_t *root_token,
                       int32_t *n_nodes, int32_t *parent, int32_t *token, int32_t *depth_out,
                       int32_t *rank, float *score, uint64_t *anc);

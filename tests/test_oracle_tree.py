@@ -8,6 +8,10 @@
   product of softmax probabilities, and rho is ignored.
 * k = 1 gives the linear chain of the dFlash baseline (Sec. 1).
 * Hand-worked fixtures for rho re-ranking and for literal Alg. 2.
+* Beam search with global retention (Alg. 1): a literal Python simulation on
+  the enumerated candidate tree; with a beam wide enough to hold every node
+  it reduces to the B best prefixes of the depths it explored; with width 1
+  and one child per node it is the greedy chain.
 """
 import json
 import os
@@ -36,9 +40,10 @@ def _instance(seed, D, k, quant=True, lam=0.2, with_rho=True):
             R.astype(np.float32) if with_rho else None, np.full(D, lam, np.float32))
 
 
-def _build(ids, lp, R, lam, D, k, B, branch=None, mode=oracle.BEST_FIRST, root=7):
+def _build(ids, lp, R, lam, D, k, B, branch=None, mode=oracle.BEST_FIRST, root=7, beam_width=0):
     return oracle.build_tree(ids[None], lp[None], None if R is None else R[None], lam,
-                             np.array([root], np.int32), D, k, B, branch=branch, mode=mode)
+                             np.array([root], np.int32), D, k, B, branch=branch, mode=mode,
+                             beam_width=beam_width)
 
 
 def _check_structure(t, ids, s=0):
@@ -207,3 +212,87 @@ def test_batch_sequences_are_independent():
         t1 = _build(ids[s], lp[s], R[s], lam, D, k, B, root=int(roots[s]))
         for key in ("parent", "token", "rank", "score", "anc", "depth"):
             np.testing.assert_array_equal(tb[key][s], t1[key][0])
+
+
+def _beam_literal(nodes, D, W, B):
+    """Alg. 1 on the enumerated candidate tree: per depth, every beam node's
+    children join T; the W best of them (total order) are the next beam."""
+    order = lambda u: (-float(nodes[u]), u)
+    beam, T = [()], []
+    for d in range(1, D + 1):
+        if len(T) >= B or not beam:
+            break
+        kids = [u for u in nodes if len(u) == d and u[:-1] in set(beam)]
+        T += kids
+        beam = sorted(kids, key=order)[:W]
+    return sorted(T, key=order)[:B]
+
+
+@pytest.mark.parametrize("seed", range(40))
+def test_beam_literal_and_invariants(seed):
+    rng = np.random.default_rng(7000 + seed)
+    D, k = int(rng.integers(1, 6)), int(rng.integers(1, 4))
+    branch = int(rng.integers(1, k + 1))
+    ids, lp, R, lam = _instance(seed + 500, D, k, quant=seed % 2 == 0,
+                                lam=[0.0, 0.2, 1.0][seed % 3])
+    nodes = full_tree(lp, lam, R, D, k, branch)
+    for W in (1, 2, 3, 5):
+        for B in sorted({1, 2, 4, max(1, (len(nodes) - 1) // 2), len(nodes) + 2}):
+            want = _beam_literal(nodes, D, W, B)
+            t = _build(ids, lp, R, lam, D, k, B, branch=branch, mode=oracle.BEAM, beam_width=W)
+            paths = _check_structure(t, ids)
+            assert paths[1:] == want
+            assert all(len(p) == 1 or p[:-1] in set(paths) for p in paths[1:])
+            # never more surrogate mass than the B best prefixes (Eq. 3)
+            best = _build(ids, lp, R, lam, D, k, B, branch=branch)
+            n = int(t["n_nodes"][0])
+            m_beam = np.exp(t["score"][0, 1:n].astype(np.float64)).sum()
+            m_best = np.exp(best["score"][0, 1:int(best["n_nodes"][0])].astype(np.float64)).sum()
+            assert m_beam <= m_best * (1 + 1e-12)
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_beam_full_width_is_top_b_of_explored_depths(seed):
+    """With a beam that holds every node, T is the whole candidate tree down
+    to the first depth at which it reaches B nodes (or D): TopB(T) is then
+    the B best prefixes of that depth-truncated tree."""
+    rng = np.random.default_rng(7500 + seed)
+    D, k = int(rng.integers(1, 6)), int(rng.integers(1, 4))
+    ids, lp, R, lam = _instance(seed + 800, D, k)
+    nodes = full_tree(lp, lam, R, D, k)
+    W = k ** D
+    for B in (1, 3, 7, len(nodes) + 1):
+        count, stop = 0, 0
+        for d in range(1, D + 1):
+            if count >= B:
+                break
+            count += sum(1 for u in nodes if len(u) == d)
+            stop = d
+        truncated = {u: v for u, v in nodes.items() if len(u) <= stop}
+        t = _build(ids, lp, R, lam, D, k, B, mode=oracle.BEAM, beam_width=W)
+        assert paths_of(t)[1:] == top_b(truncated, B)
+
+
+def test_beam_width_one_single_child_is_greedy_chain():
+    D, k = 6, 3
+    ids, lp, R, lam = _instance(11, D, k)
+    t = _build(ids, lp, R, lam, D, k, 10, branch=1, mode=oracle.BEAM, beam_width=1)
+    paths = paths_of(t)
+    # every node has the best-scoring child of its parent's context
+    for i in range(1, len(paths)):
+        p = paths[i]
+        d = len(p) - 1
+        a = p[-3] if len(p) >= 3 else 0
+        b = p[-2] if len(p) >= 2 else 0
+        from brute import token_score
+        s = [token_score(lp, lam, R, d, a, b, r) for r in range(k)]
+        assert p[-1] == min(range(k), key=lambda r: (-float(s[r]), r))
+    assert [len(p) for p in paths] == list(range(D + 1))
+
+
+def test_beam_rejects_zero_width():
+    D, k = 3, 2
+    ids, lp, R, lam = _instance(3, D, k)
+    with pytest.raises(ValueError):
+        _build(ids, lp, R, lam, D, k, 4, mode=oracle.BEAM, beam_width=0)
+
