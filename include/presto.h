@@ -115,7 +115,13 @@ presto_status presto_topk(presto_dtype dt, const void *logits, int64_t rows, int
  *   when it has fewer nodes.
  * PRESTO_TREE_BEST_FIRST_ALG2: Alg. 2 as printed: every pop adds all its
  *   children to T; stop once T holds `budget` non-root nodes; keep TopB(T).
- * PRESTO_TREE_BEAM: reserved (returns PRESTO_ERR_UNSUPPORTED).
+ * PRESTO_TREE_BEAM (Sec. 4.2, Alg. 1, beam search with global retention):
+ *   the beam starts as {root}; at each depth every beam node is expanded
+ *   (its top-`branch` children join T), and the `beam_width` best of them
+ *   in the total order form the next beam.  Depths are taken while T holds
+ *   fewer than `budget` non-root nodes (checked before each depth), at most
+ *   `depth` of them.  The tree is TopB(T): the `budget` best nodes of T.
+ *   Limits: 1 <= beam_width <= 64, beam_width * k <= 256.
  *
  * The budget counts draft (non-root) nodes: the output has N = budget + 1
  * rows, row 0 being the root (the last committed token, root_token[b]).
@@ -127,6 +133,7 @@ typedef struct {
     int32_t branch; /* children per expansion, 1 .. k                          */
     int32_t budget; /* B, draft nodes excluding the root, 1 .. 511            */
     int32_t mode;   /* presto_tree_mode                                        */
+    int32_t beam_width; /* W, PRESTO_TREE_BEAM only (ignored otherwise)        */
 } presto_tree_desc;
 
 /* ids, logprob [batch, depth, k] from presto_topk (logprob <= 0);

@@ -48,7 +48,8 @@ class PrestoError(RuntimeError):
 
 class TreeDesc(ctypes.Structure):
     _fields_ = [("batch", ctypes.c_int32), ("depth", ctypes.c_int32), ("k", ctypes.c_int32),
-                ("branch", ctypes.c_int32), ("budget", ctypes.c_int32), ("mode", ctypes.c_int32)]
+                ("branch", ctypes.c_int32), ("budget", ctypes.c_int32), ("mode", ctypes.c_int32),
+                ("beam_width", ctypes.c_int32)]
 
 
 class AttnDesc(ctypes.Structure):
@@ -160,8 +161,9 @@ def presto_topk(logits: torch.Tensor, k: int, *, ids=None, logprob=None, lse=Non
 def presto_build_tree(ids: torch.Tensor, logprob: torch.Tensor, log_rho, lam: torch.Tensor,
                       root_token: torch.Tensor, depth: int, k: int, budget: int,
                       branch: int | None = None, mode: int = PRESTO_TREE_BEST_FIRST, *, out=None,
-                      workspace=None, stream=None) -> dict:
-    """Best-first draft tree per sequence: ids/logprob [b*D, k] or [b, D, k]."""
+                      workspace=None, stream=None, beam_width: int = 0) -> dict:
+    """Draft tree per sequence (best-first, or beam search of width
+    `beam_width`): ids/logprob [b*D, k] or [b, D, k]."""
     branch = k if branch is None else branch
     b = root_token.shape[0]
     N = budget + 1
@@ -177,7 +179,7 @@ def presto_build_tree(ids: torch.Tensor, logprob: torch.Tensor, log_rho, lam: to
             "score": torch.empty(b, N, dtype=torch.float32, device=dev),
             "anc": torch.empty(b, N, W, dtype=torch.int64, device=dev),
         }
-    desc = TreeDesc(b, depth, k, branch, budget, mode)
+    desc = TreeDesc(b, depth, k, branch, budget, mode, beam_width)
     need = lib().presto_build_tree_workspace(ctypes.byref(desc))
     ws, nb = _workspace(need, dev, workspace)
     _check(lib().presto_build_tree(

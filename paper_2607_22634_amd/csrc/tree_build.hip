@@ -30,6 +30,8 @@
 
 namespace presto {
 
+constexpr int kBeamCandSlots = 4;  // beam search: W * k <= 4 * 64 candidates per depth
+
 struct TreeArgs {
     int32_t D, k, branch, budget, N, W, wbits, per_word;
     const int32_t* ids;
@@ -45,8 +47,9 @@ struct TreeArgs {
     float* score;
     uint64_t* anc;
     bool rho_in_lds;
+    int32_t beam_width;  // beam search only
     // LDS byte offsets
-    int o_lp, o_ids, o_kord, o_krank, o_rec, o_rho;
+    int o_lp, o_ids, o_kord, o_krank, o_rec, o_ktab, o_beam, o_bidx, o_rho;
 };
 
 // Frontier metadata in one word: parent node (10 bits), candidate rank (4),
@@ -93,9 +96,19 @@ __device__ __forceinline__ void stage_words(uint32_t* dst, const uint32_t* src, 
     }
 }
 
+// One entry of a beam (beam search): score, candidate rank, rank of its
+// parent, and its place in rank-path order among the entries of its depth.
+struct BeamEntry {
+    float S;
+    int32_t rank, prank, path;
+};
+
 // RHO: 0 no lattice (s = log q), 1 lattice staged in LDS, 2 lattice read
-// from global memory.  KQ: k <= 4, children ranked within a quad.
-template <int SL, int RHO, bool KQ>
+// from global memory.  KQ: k <= 4, children ranked within a quad.  BEAM:
+// beam search with global retention (Alg. 1): a level-by-level beam pass
+// fixes the retained set T, then the best-first pass below, restricted to
+// T, emits TopB(T) in the total order.
+template <int SL, int RHO, bool KQ, bool BEAM>
 __global__ __launch_bounds__(kWave) void tree_build_kernel(TreeArgs a) {
     extern __shared__ __align__(16) char lds[];
     const int lane = lane_id();
@@ -125,11 +138,130 @@ __global__ __launch_bounds__(kWave) void tree_build_kernel(TreeArgs a) {
     const float lam_lane = lane < D ? a.lambda[lane] : 0.f;  // lambda_d held by lane d
     __builtin_amdgcn_wave_barrier();
 
+    // token score of candidate r at drafter row `row` under the trigram
+    // context (ctx2, ctx1): fl(log q + fl(lambda * log rho)), NaN -> -inf
+    auto token_score = [&](int row, int ctx2, int ctx1, int r) {
+        const float lam_d = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(lam_lane), row));
+        const float lq = s_lp[row * k + r];
+        float s = lq;
+        if constexpr (RHO != 0) {
+            const int ri = ((row * k + ctx2) * k + ctx1) * k + r;
+            float lr;
+            if constexpr (RHO == 1)
+                lr = s_rho[ri];
+            else
+                lr = g_rho[ri];
+            const float t = lam_d * lr;
+            s = lq + t;
+        }
+        return (s == s) ? s : -INFINITY;
+    };
+
+    // ---- beam pass (Alg. 1): per depth, every beam entry's top-`branch`
+    // children join T; the W best (total order) form the next beam.  The
+    // table ktab[d][beam entry of the parent][rank] records, for every node of
+    // depth d, whether it is in T (-1) and if so whether it is in the beam of
+    // its depth (its index there, >= 0); -2: not in T.
+    int8_t* s_ktab = reinterpret_cast<int8_t*>(lds + a.o_ktab);
+    BeamEntry* s_beam = reinterpret_cast<BeamEntry*>(lds + a.o_beam);  // [2][Wb]
+    int8_t* s_bidx = reinterpret_cast<int8_t*>(lds + a.o_bidx);        // [N] beam index per node
+    const int Wb = a.beam_width;
+    if constexpr (BEAM) {
+        const int tab = (D + 1) * Wb * k;
+        for (int i = lane; i < tab; i += kWave) s_ktab[i] = -2;
+        if (lane == 0) s_beam[0] = BeamEntry{0.f, 0, 0, 0};  // the root
+        __builtin_amdgcn_wave_barrier();
+        int nb = 1, cur = 0, nT = 0;
+        constexpr int CS = kBeamCandSlots;
+        for (int d = 1; d <= D && nT < a.budget && nb > 0; ++d) {
+            const int row = d - 1;  // drafter row of depth d
+            const BeamEntry* bc = s_beam + cur * Wb;
+            uint64_t key[CS];
+            int cpb[CS], cr[CS];
+            int count = 0;
+#pragma unroll
+            for (int q = 0; q < CS; ++q) {
+                const int ci = q * kWave + lane;
+                const bool valid = ci < nb * k;
+                const int pb = valid ? ci / k : 0, r = valid ? ci % k : 0;
+                const BeamEntry e = bc[pb];
+                const float sv = token_score(row, row >= 2 ? e.prank : 0, row >= 1 ? e.rank : 0, r);
+                bool in = valid;
+                if (a.branch < k) {
+                    // top-`branch` of the parent's k candidates by token score
+                    int sel = 0;
+                    for (int j = 0; j < k; ++j) {
+                        const float sj = token_score(row, row >= 2 ? e.prank : 0, row >= 1 ? e.rank : 0, j);
+                        sel += (sj > sv || (sj == sv && j < r)) ? 1 : 0;
+                    }
+                    in = in && sel < a.branch;
+                }
+                const float S = e.S + sv;
+                key[q] = in ? ((uint64_t)ord32(S) << 32) | (uint64_t)(0xffffffffu - (uint32_t)(e.path * 16 + r))
+                            : 0ull;
+                cpb[q] = pb;
+                cr[q] = r;
+                if (in) s_ktab[(d * Wb + pb) * k + r] = -1;
+                count += __popcll(__ballot(in));
+            }
+            nT += count;
+            // the W best candidates, in the total order (S desc, rank path asc)
+            const int nn = min(Wb, count);
+            BeamEntry mine{0.f, 0, 0, 0};
+            int mine_pb = 0;
+            for (int j = 0; j < nn; ++j) {
+                uint64_t lm = 0ull;
+#pragma unroll
+                for (int q = 0; q < CS; ++q) lm = key[q] > lm ? key[q] : lm;
+                const uint64_t m = wave_max_u64_dpp(lm);
+                int wq = 0, wl = 0;
+#pragma unroll
+                for (int q = CS - 1; q >= 0; --q) {
+                    const uint64_t hit = __ballot(key[q] == m);
+                    if (hit) {
+                        wq = q;
+                        wl = __ffsll((unsigned long long)hit) - 1;
+                    }
+                }
+                int lpb = 0, lr = 0;
+#pragma unroll
+                for (int q = 0; q < CS; ++q) {
+                    lpb = q == wq ? cpb[q] : lpb;
+                    lr = q == wq ? cr[q] : lr;
+                }
+                const int pb = __builtin_amdgcn_readlane(lpb, wl);
+                const int r = __builtin_amdgcn_readlane(lr, wl);
+                if (lane == j) {
+                    mine = BeamEntry{unord32((uint32_t)(m >> 32)), r, bc[pb].rank, 0};
+                    mine_pb = pb;
+                }
+                if (lane == 0) s_ktab[(d * Wb + pb) * k + r] = (int8_t)j;
+#pragma unroll
+                for (int q = 0; q < CS; ++q) key[q] = (q == wq && lane == wl) ? 0ull : key[q];
+            }
+            // place of each new entry in rank-path order: (parent's place, rank)
+            const int okey = bc[mine_pb].path * 16 + mine.rank;
+            int place = 0;
+            for (int j = 0; j < nn; ++j) {
+                const int oj = __builtin_amdgcn_readlane(okey, j);
+                place += (oj < okey) ? 1 : 0;
+            }
+            mine.path = place;
+            __builtin_amdgcn_wave_barrier();
+            if (lane < nn) s_beam[(cur ^ 1) * Wb + lane] = mine;
+            __builtin_amdgcn_wave_barrier();
+            cur ^= 1;
+            nb = nn;
+        }
+        if (lane == 0) s_bidx[0] = 0;  // the root is the beam of depth 0
+        __builtin_amdgcn_wave_barrier();
+    }
+
     // Children of node n (depth d, own rank rn, parent's rank rp, score Sn):
     // lane r < k scores candidate r, the children are ranked by (S desc,
     // rank asc) with in-row rotations and stored in that order; returns the
     // first child as (ord S, rank), ord 0 if none.
-    auto expand = [&](int n, int d, int rn, int rp, float Sn, uint32_t& c_ord, int& c_rank) {
+    auto expand = [&](int n, int d, int rn, int rp, float Sn, int bidx, uint32_t& c_ord, int& c_rank) {
         const int ctx2 = d >= 2 ? rp : 0;  // grandparent slot of the trigram
         const int ctx1 = d >= 1 ? rn : 0;  // parent slot of the trigram
         const float lam_d = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(lam_lane), d));
@@ -154,7 +286,10 @@ __global__ __launch_bounds__(kWave) void tree_build_kernel(TreeArgs a) {
             s = (s == s && lane < k) ? s : -INFINITY;
         }
         bool in = lane < k;
-        if (a.branch < k) {
+        if constexpr (BEAM) {
+            // the children in T (the beam pass applied the branch filter)
+            in = in && s_ktab[((d + 1) * Wb + bidx) * k + rl] >= -1;
+        } else if (a.branch < k) {
             // keep the top-`branch` by token score (larger s, then lower rank)
             int sel = 0;
             for (int j = 0; j < k; ++j) {
@@ -202,7 +337,7 @@ __global__ __launch_bounds__(kWave) void tree_build_kernel(TreeArgs a) {
     if (lane == 0) s_rec[0] = make_uint2(0xffffffffu, __float_as_uint(0.f));
     uint32_t c_ord;
     int c_rank;
-    expand(0, 0, 0, 0, 0.f, c_ord, c_rank);
+    expand(0, 0, 0, 0, 0.f, 0, c_ord, c_rank);
 
     // frontier slots: slot j of lane l is entry j * 64 + l
     uint32_t fS[SL], fM[SL];
@@ -271,6 +406,11 @@ __global__ __launch_bounds__(kWave) void tree_build_kernel(TreeArgs a) {
         // commit node n: one record; everything else is derived after the search
         const int n = committed++;
         if (lane == 0) s_rec[n] = make_uint2(meta, __float_as_uint(S));
+        int bidx = 0;  // beam search: n's entry in the beam of its depth, or < 0
+        if constexpr (BEAM) {
+            bidx = s_ktab[(d * Wb + s_bidx[p]) * k + r];
+            if (lane == 0) s_bidx[n] = (int8_t)bidx;
+        }
 
         // next sibling of n: the next entry of its parent's ordered children
         // (read unconditionally, at a clamped index, so that its latency
@@ -281,7 +421,7 @@ __global__ __launch_bounds__(kWave) void tree_build_kernel(TreeArgs a) {
         // first child of n
         uint32_t kid_ord = 0u;
         int kid_rank = 0;
-        if (d < D) expand(n, d, r, rp, S, kid_ord, kid_rank);
+        if (d < D && bidx >= 0) expand(n, d, r, rp, S, bidx, kid_ord, kid_rank);
 
         // pushes: the first reuses the popped slot, the second takes a fresh slot
         uint32_t xS = 0u, xM = 0u, yS = 0u, yM = 0u;
@@ -361,16 +501,19 @@ static int align16(int x) { return (x + 15) & ~15; }
 
 struct TreeLayout {
     int total_no_rho, total_with_rho;
-    int o_lp, o_ids, o_kord, o_krank, o_rec, o_rho;
+    int o_lp, o_ids, o_kord, o_krank, o_rec, o_ktab, o_beam, o_bidx, o_rho;
 };
 
-static TreeLayout tree_layout(int D, int k, int N) {
+static TreeLayout tree_layout(int D, int k, int N, int Wb) {
     TreeLayout L;
     int off = 0;
     L.o_lp = off; off = align16(off + D * k * 4);
     L.o_ids = off; off = align16(off + D * k * 4);
     L.o_kord = off; off = align16(off + N * k * 4);
     L.o_krank = off; off = align16(off + N * k);
+    L.o_ktab = off; off = align16(off + (D + 1) * Wb * k);
+    L.o_beam = off; off = align16(off + 2 * Wb * (int)sizeof(BeamEntry));
+    L.o_bidx = off; off = align16(off + N);
     L.o_rec = off; off = align16(off + N * 8);
     L.total_no_rho = off;
     L.o_rho = off;
@@ -390,9 +533,9 @@ int tree_key_bits(int k) {
 // straddle a word).
 int tree_max_depth(int k) { return 4 * (32 / tree_key_bits(k)); }
 
-bool tree_build_fits(int D, int k, int branch, int N) {
+bool tree_build_fits(int D, int k, int branch, int N, int beam_width) {
     (void)branch;
-    return tree_layout(D, k, N).total_no_rho <= kTreeLdsBudget;
+    return tree_layout(D, k, N, beam_width).total_no_rho <= kTreeLdsBudget;
 }
 
 presto_status launch_build_tree(const presto_tree_desc* desc, const int32_t* ids,
@@ -421,16 +564,21 @@ presto_status launch_build_tree(const presto_tree_desc* desc, const int32_t* ids
     a.rank = rank;
     a.score = score;
     a.anc = anc;
-    const TreeLayout L = tree_layout(a.D, a.k, a.N);
+    const bool beam = desc->mode == PRESTO_TREE_BEAM;
+    a.beam_width = beam ? desc->beam_width : 0;
+    const TreeLayout L = tree_layout(a.D, a.k, a.N, a.beam_width);
     a.o_lp = L.o_lp; a.o_ids = L.o_ids; a.o_kord = L.o_kord; a.o_krank = L.o_krank; a.o_rec = L.o_rec;
+    a.o_ktab = L.o_ktab; a.o_beam = L.o_beam; a.o_bidx = L.o_bidx;
     a.o_rho = L.o_rho;
     a.rho_in_lds = log_rho != nullptr && L.total_with_rho <= kTreeLdsBudget;
     const int lds = a.rho_in_lds ? L.total_with_rho : L.total_no_rho;
     const int SL = (a.N + kWave - 1) / kWave;
     const int rho_mode = log_rho == nullptr ? 0 : (a.rho_in_lds ? 1 : 2);
-#define PRESTO_TREE3(S, R, Q) tree_build_kernel<S, R, Q><<<desc->batch, kWave, lds, stream>>>(a)
+#define PRESTO_TREE4(S, R, Q)                                                       \
+    if (beam) tree_build_kernel<S, R, Q, true><<<desc->batch, kWave, lds, stream>>>(a); \
+    else tree_build_kernel<S, R, Q, false><<<desc->batch, kWave, lds, stream>>>(a)
 #define PRESTO_TREE2(S, R) \
-    if (a.k <= 4) PRESTO_TREE3(S, R, true); else PRESTO_TREE3(S, R, false)
+    if (a.k <= 4) { PRESTO_TREE4(S, R, true); } else { PRESTO_TREE4(S, R, false); }
 #define PRESTO_TREE(S)                      \
     if (rho_mode == 0) { PRESTO_TREE2(S, 0); } \
     else if (rho_mode == 1) { PRESTO_TREE2(S, 1); } \
@@ -441,7 +589,7 @@ presto_status launch_build_tree(const presto_tree_desc* desc, const int32_t* ids
     else { PRESTO_TREE(8) }
 #undef PRESTO_TREE
 #undef PRESTO_TREE2
-#undef PRESTO_TREE3
+#undef PRESTO_TREE4
     return check_launch("tree_build_kernel");
 }
 

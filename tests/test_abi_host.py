@@ -83,9 +83,16 @@ def test_build_tree_rejects_bad_descriptor(field, value):
 
 
 def test_build_tree_unbuilt_modes_are_unsupported():
-    d = P.TreeDesc(1, 4, 4, 4, 8, P.PRESTO_TREE_BEAM)
+    d = P.TreeDesc(1, 4, 4, 4, 8, P.PRESTO_TREE_BEST_FIRST_ALG2)
     st, _ = _err(P.lib().presto_build_tree(ctypes.byref(d), *([None] * 13), 0, None))
     assert st == P.PRESTO_ERR_UNSUPPORTED
+
+
+@pytest.mark.parametrize("width,k", [(0, 4), (65, 1), (33, 8)])
+def test_build_tree_rejects_bad_beam_width(width, k):
+    d = P.TreeDesc(1, 4, k, k, 8, P.PRESTO_TREE_BEAM, width)
+    st, msg = _err(P.lib().presto_build_tree(ctypes.byref(d), *([None] * 13), 0, None))
+    assert st == P.PRESTO_ERR_INVALID_ARG and "beam_width" in msg
 
 
 def test_build_tree_path_key_limit():

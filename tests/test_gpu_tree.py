@@ -15,12 +15,16 @@ pytestmark = pytest.mark.gpu
 KEYS = ("n_nodes", "parent", "token", "depth", "rank", "score", "anc")
 
 
-def _gpu_and_oracle(ids, lp, rho, lam, root, D, k, B, branch=None):
+def _gpu_and_oracle(ids, lp, rho, lam, root, D, k, B, branch=None, beam_width=0):
+    mode = P.PRESTO_TREE_BEAM if beam_width else P.PRESTO_TREE_BEST_FIRST
     g = P.presto_build_tree(to_dev(ids), to_dev(lp), None if rho is None else to_dev(rho),
-                            to_dev(lam), to_dev(root), D, k, B, branch=branch)
+                            to_dev(lam), to_dev(root), D, k, B, branch=branch, mode=mode,
+                            beam_width=beam_width)
     torch.cuda.synchronize()
     g = tree_to_host(g)
-    o = oracle.build_tree(ids, lp, rho, lam, root, D, k, B, branch=branch)
+    o = oracle.build_tree(ids, lp, rho, lam, root, D, k, B, branch=branch,
+                          mode=oracle.BEAM if beam_width else oracle.BEST_FIRST,
+                          beam_width=beam_width)
     return g, o
 
 
@@ -83,3 +87,29 @@ def test_tree_is_deterministic():
                                          to_dev(root), 16, 8, 256))
     for key in KEYS:
         np.testing.assert_array_equal(a[key], b[key])
+
+
+@pytest.mark.parametrize("cfg,W", [(2, 10), (3, 4), (4, 10), (5, 10)])
+def test_beam_tree_matches_oracle_on_workload(cfg, W):
+    w, rin = round_data(cfg)
+    print(f"beam cfg={cfg} W={W}", flush=True)
+    ids, lp, _ = P.presto_topk(to_dev(rin["drafter_logits"], w.dtype), w.k)
+    ids = to_host(ids).reshape(w.batch, w.depth, w.k)
+    lp = to_host(lp).reshape(w.batch, w.depth, w.k)
+    g, o = _gpu_and_oracle(ids, lp, rin["rho"], rin["lam"], rin["root_token"], w.depth, w.k,
+                           w.budget, beam_width=W)
+    _assert_same(g, o)
+
+
+@pytest.mark.parametrize("D,k,branch,B,W", [(1, 1, 1, 1, 1), (3, 2, 2, 4, 1), (4, 3, 2, 40, 3),
+                                            (5, 3, 3, 200, 64), (6, 2, 1, 9, 2), (16, 8, 8, 256, 10),
+                                            (32, 4, 3, 128, 16), (8, 16, 16, 255, 16),
+                                            (12, 5, 5, 130, 51), (10, 4, 4, 511, 64)])
+@pytest.mark.parametrize("quant", [False, True])
+def test_beam_tree_matches_oracle_random(D, k, branch, B, W, quant):
+    ids, lp, R, root = _random_batch([D, k, B, W, int(quant)], 12, D, k, quant)
+    for lam_v, rho in ((0.2, R), (1.0, None)):
+        lam = np.full(D, lam_v, np.float32)
+        g, o = _gpu_and_oracle(ids, lp, rho, lam, root, D, k, B, branch=branch, beam_width=W)
+        _assert_same(g, o)
+
