@@ -83,6 +83,10 @@ enum {
  * logprob    [rows, k] fp32 out: log q(id) = z_id - LSE.
  * lse        [rows] fp32 out, may be NULL: LSE = log sum_v exp(z_v), fp32.
  *            A row of only -inf gives LSE = -inf and logprob = -inf.
+ * entropy    [rows] fp32 out, may be NULL: H = -sum_v q(v) log q(v) of the
+ *            row's softmax (Appendix F), terms with q(v) = 0 taken as 0; it
+ *            comes out of the same pass over the row as LSE.  A row of only
+ *            -inf gives H = 0.
  * flags      optional: PRESTO_FLAG_NAN_DRAFTER when a row holds NaN or
  *            +inf; that row's outputs are then unspecified.
  * Limits: 1 <= k <= 16, k <= vocab, row_stride >= vocab, rows >= 0
@@ -91,7 +95,19 @@ enum {
 size_t presto_topk_workspace(int64_t rows, int32_t vocab, int32_t k);
 presto_status presto_topk(presto_dtype dt, const void *logits, int64_t rows, int32_t vocab,
                           int64_t row_stride, int32_t k, int32_t *ids, float *logprob, float *lse,
-                          int32_t *flags, void *ws, size_t ws_bytes, hipStream_t stream);
+                          float *entropy, int32_t *flags, void *ws, size_t ws_bytes,
+                          hipStream_t stream);
+
+/* Entropy-adaptive prefix weight (Appendix F):
+ *   lambda[r] = beta * H[r] / (H[r] + C), fp32, H from presto_topk's
+ * entropy output ([batch, depth] rows give a [batch, depth] lambda for
+ * presto_build_tree with lambda_per_seq = 1).  Low-entropy (confident)
+ * positions get a weight near 0, high-entropy ones approach beta.
+ * entropy, lambda [rows] fp32 device; entropy must be finite and >= 0.
+ * Limits: beta > 0 and C > 0, finite; rows >= 0 (0 is a no-op).
+ */
+presto_status presto_entropy_lambda(int64_t rows, const float *entropy, float beta, float c,
+                                    float *lambda, hipStream_t stream);
 
 /* ------------------------------------------------------------------------ */
 /* Stage 2: prefix-aligned scoring and best-first tree construction.
@@ -134,11 +150,14 @@ typedef struct {
     int32_t budget; /* B, draft nodes excluding the root, 1 .. 511            */
     int32_t mode;   /* presto_tree_mode                                        */
     int32_t beam_width; /* W, PRESTO_TREE_BEAM only (ignored otherwise)        */
+    int32_t lambda_per_seq; /* 0: lambda is [depth]; 1: lambda is [batch, depth] */
 } presto_tree_desc;
 
 /* ids, logprob [batch, depth, k] from presto_topk (logprob <= 0);
  * log_rho [batch, depth, k, k, k] fp32, finite and <= 0, or NULL for s = log q;
- * lambda [depth] fp32, finite and >= 0 (device);  root_token [batch] int32.
+ * lambda [depth] fp32, finite and >= 0 (device), or [batch, depth] when
+ *   desc->lambda_per_seq is 1 (e.g. from presto_entropy_lambda);
+ * root_token [batch] int32.
  * Outputs, N = budget + 1 rows per sequence, rows in the total order above
  * (every parent precedes its children):
  *   n_nodes [batch]             live rows, 1 .. N

@@ -70,10 +70,30 @@ def topk(logits: np.ndarray, k: int, dtype: str):
     return ids, lp, lse, int(nan_rows)
 
 
+def entropy(logits: np.ndarray, dtype: str) -> np.ndarray:
+    """fp64 softmax entropy H of every row of logits [rows, V] (Appendix F)."""
+    _check(logits, dtype)
+    rows, V = logits.shape
+    h = np.empty(rows, np.float64)
+    lib().oracle_entropy(ctypes.c_int(_dt(dtype)), _p(logits), ctypes.c_int64(rows),
+                         ctypes.c_int32(V), ctypes.c_int64(V), _p(h))
+    return h
+
+
+def entropy_lambda(h, beta: float, c: float) -> np.ndarray:
+    """fp64 entropy-adaptive weight beta * H / (H + C) (Appendix F)."""
+    h = np.ascontiguousarray(h, np.float64)
+    out = np.empty_like(h)
+    lib().oracle_entropy_lambda(ctypes.c_int64(h.size), _p(h), ctypes.c_double(beta),
+                                ctypes.c_double(c), _p(out))
+    return out
+
+
 def build_tree(ids, logprob, rho, lam, root_token, depth: int, k: int, budget: int,
                branch: int | None = None, mode: int = BEST_FIRST, beam_width: int = 0) -> dict:
     """Tree per sequence (best-first, literal Alg. 2, or beam search with beam
-    width `beam_width`); ids/logprob [b, D, k], rho [b, D, k, k, k] or None."""
+    width `beam_width`); ids/logprob [b, D, k], rho [b, D, k, k, k] or None;
+    lam [D], or [b, D] for a weight per sequence and position."""
     branch = k if branch is None else branch
     ids = np.ascontiguousarray(ids, np.int32)
     logprob = np.ascontiguousarray(logprob, np.float32)
@@ -81,6 +101,9 @@ def build_tree(ids, logprob, rho, lam, root_token, depth: int, k: int, budget: i
     root_token = np.ascontiguousarray(root_token, np.int32)
     rho = None if rho is None else np.ascontiguousarray(rho, np.float32)
     b = root_token.shape[0]
+    per_seq = lam.ndim == 2
+    if per_seq and lam.shape != (b, depth):
+        raise ValueError("a 2-D lambda must be [batch, depth]")
     N = budget + 1
     W = (N + 63) // 64
     out = {
@@ -93,7 +116,7 @@ def build_tree(ids, logprob, rho, lam, root_token, depth: int, k: int, budget: i
     f.restype = ctypes.c_int
     rc = f(ctypes.c_int(mode), ctypes.c_int32(b), ctypes.c_int32(depth), ctypes.c_int32(k),
            ctypes.c_int32(branch), ctypes.c_int32(budget), ctypes.c_int32(beam_width), _p(ids),
-           _p(logprob), _p(rho), _p(lam),
+           _p(logprob), _p(rho), _p(lam), ctypes.c_int32(int(per_seq)),
            _p(root_token), _p(out["n_nodes"]), _p(out["parent"]), _p(out["token"]),
            _p(out["depth"]), _p(out["rank"]), _p(out["score"]), _p(out["anc"]))
     if rc != 0:

@@ -118,18 +118,21 @@ int oracle_topk(int dtype, const void *logits, int64_t rows, int32_t vocab, int6
                 if (have < k) ++have;
             }
         }
-        /* log sum_v exp(z_v) = m + log sum_v exp(z_v - m), in fp64 */
-        double l;
+        /* log sum_v exp(z_v) = m + log sum_v exp(z_v - m), in fp64; log q(t) =
+         * z_t - LSE is formed as (z_t - m) - log sum, which keeps the log of
+         * the sum even where |m| dwarfs it (a row near -1e30) */
+        double l, ls = 0.0;
         if (m == -INFINITY) {
             l = -INFINITY;
         } else {
             double acc = 0.0;
             for (int32_t v = 0; v < vocab; ++v) acc += exp((double)load_f(dtype, logits, base + v) - m);
-            l = m + log(acc);
+            ls = log(acc);
+            l = m + ls;
         }
         for (int j = 0; j < k; ++j) {
             ids[r * k + j] = bi[j];
-            logprob[r * k + j] = (l == -INFINITY) ? -INFINITY : (float)((double)bv[j] - l);
+            logprob[r * k + j] = (l == -INFINITY) ? -INFINITY : (float)(((double)bv[j] - m) - ls);
         }
         if (lse) lse[r] = (float)l;
         nan_rows += saw_nan;
@@ -137,6 +140,43 @@ int oracle_topk(int dtype, const void *logits, int64_t rows, int32_t vocab, int6
         free(bi);
     }
     return nan_rows;
+}
+
+/* Entropy of the diffusion marginal, H_d = -sum_w q_d(w) log q_d(w)
+ * (Appendix F), with q_d = softmax(z_d) (Eq. 6) formed in fp64 from the
+ * row max m and log sum_w exp(z_w - m).  A term whose q is 0 contributes 0 (its limit); a row of
+ * only -inf has no distribution and is given H = 0. */
+void oracle_entropy(int dtype, const void *logits, int64_t rows, int32_t vocab, int64_t row_stride,
+                    double *entropy) {
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int64_t r = 0; r < rows; ++r) {
+        const int64_t base = r * row_stride;
+        double m = -INFINITY;
+        for (int32_t v = 0; v < vocab; ++v) {
+            double z = (double)load_f(dtype, logits, base + v);
+            if (z > m) m = z;
+        }
+        if (m == -INFINITY) {
+            entropy[r] = 0.0;
+            continue;
+        }
+        double acc = 0.0;
+        for (int32_t v = 0; v < vocab; ++v) acc += exp((double)load_f(dtype, logits, base + v) - m);
+        const double ls = log(acc);
+        double h = 0.0;
+        for (int32_t v = 0; v < vocab; ++v) {
+            /* log q = (z - m) - log sum, shifted so that |m| >> log sum keeps it */
+            const double q = exp(((double)load_f(dtype, logits, base + v) - m) - ls);
+            if (q > 0.0) h -= q * log(q);
+        }
+        entropy[r] = h;
+    }
+}
+
+/* Entropy-adaptive weight lambda_d(H_d) = beta * H_d / (H_d + C) (Appendix F), fp64. */
+void oracle_entropy_lambda(int64_t rows, const double *entropy, double beta, double c,
+                           double *lambda) {
+    for (int64_t r = 0; r < rows; ++r) lambda[r] = beta * entropy[r] / (entropy[r] + c);
 }
 
 /* ------------------------------------------------------------------------ */
@@ -367,7 +407,8 @@ static int build_beam(const seqctx *c, int32_t budget, int32_t W, int32_t root_t
 
 int oracle_build_tree(int mode, int32_t batch, int32_t depth, int32_t k, int32_t branch,
                       int32_t budget, int32_t beam_width, const int32_t *ids, const float *logprob,
-                      const float *log_rho, const float *lambda, const int32_t *root_token,
+                      const float *log_rho, const float *lambda, int32_t lambda_per_seq,
+                      const int32_t *root_token,
                       int32_t *n_nodes, int32_t *parent, int32_t *token, int32_t *depth_out,
                       int32_t *rank, float *score, uint64_t *anc) {
     if (depth < 1 || depth > MAXD || k < 1 || k > 64 || branch < 1 || branch > k || budget < 1)
@@ -387,7 +428,8 @@ int oracle_build_tree(int mode, int32_t batch, int32_t depth, int32_t k, int32_t
 #pragma omp parallel for schedule(dynamic, 1) reduction(| : err)
     for (int b = 0; b < batch; ++b) {
         seqctx c = {depth, k, branch, ids + (int64_t)b * depth * k, logprob + (int64_t)b * depth * k,
-                    log_rho ? log_rho + (int64_t)b * depth * k * k * k : NULL, lambda};
+                    log_rho ? log_rho + (int64_t)b * depth * k * k * k : NULL,
+                    lambda_per_seq ? lambda + (int64_t)b * depth : lambda};
         onode *nodes = (onode *)malloc(sizeof(onode) * (size_t)(N + 1));
         onode *pool = (onode *)malloc(sizeof(onode) * (size_t)(cap + branch));
         onode *kids = (onode *)malloc(sizeof(onode) * (size_t)branch);

@@ -27,11 +27,21 @@ int oracle_get_threads(void);
 int oracle_topk(int dtype, const void *logits, int64_t rows, int32_t vocab, int64_t row_stride,
                 int32_t k, int32_t *ids, float *logprob, float *lse);
 
+/* Softmax entropy H_d of each row (Appendix F), fp64; 0 for a row of only -inf. */
+void oracle_entropy(int dtype, const void *logits, int64_t rows, int32_t vocab, int64_t row_stride,
+                    double *entropy);
+
+/* Entropy-adaptive weight beta * H / (H + C) (Appendix F), fp64. */
+void oracle_entropy_lambda(int64_t rows, const double *entropy, double beta, double c,
+                           double *lambda);
+
 /* Prefix-aligned scoring (Eq. 9) and best-first tree construction (Sec. 4.2).
+ * lambda is [depth], or [batch, depth] when lambda_per_seq is nonzero.
  * Returns 0, or -1 on an argument the oracle cannot represent. */
 int oracle_build_tree(int mode, int32_t batch, int32_t depth, int32_t k, int32_t branch,
                       int32_t budget, int32_t beam_width, const int32_t *ids, const float *logprob,
-                      const float *log_rho, const float *lambda, const int32_t *root_token,
+                      const float *log_rho, const float *lambda, int32_t lambda_per_seq,
+                      const int32_t *root_token,
                       int32_t *n_nodes, int32_t *parent, int32_t *token, int32_t *depth_out,
                       int32_t *rank, float *score, uint64_t *anc);
 

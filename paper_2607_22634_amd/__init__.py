@@ -9,6 +9,6 @@ from ._lib import (  # noqa: F401
     EXPORTS, PRESTO_DT_BF16, PRESTO_DT_F32, PRESTO_ERR_HIP, PRESTO_ERR_INVALID_ARG,
     PRESTO_ERR_UNSUPPORTED, PRESTO_ERR_WORKSPACE, PRESTO_FLAG_NAN_DRAFTER, PRESTO_FLAG_NAN_TARGET,
     PRESTO_OK, PRESTO_TREE_BEAM, PRESTO_TREE_BEST_FIRST, PRESTO_TREE_BEST_FIRST_ALG2, AttnDesc,
-    PrestoError, TreeDesc, lib, presto_accept, presto_build_tree, presto_topk,
+    PrestoError, TreeDesc, lib, presto_accept, presto_build_tree, presto_entropy_lambda, presto_topk,
     presto_tree_attention, version,
 )

@@ -34,7 +34,8 @@ PRESTO_FLAG_NAN_DRAFTER = 1
 PRESTO_FLAG_NAN_TARGET = 2
 
 EXPORTS = (
-    "presto_topk_workspace", "presto_topk", "presto_build_tree_workspace", "presto_build_tree",
+    "presto_topk_workspace", "presto_topk", "presto_entropy_lambda", "presto_build_tree_workspace",
+    "presto_build_tree",
     "presto_tree_attention_workspace", "presto_tree_attention", "presto_accept_workspace",
     "presto_accept", "presto_status_string", "presto_last_error", "presto_version",
 )
@@ -49,7 +50,7 @@ class PrestoError(RuntimeError):
 class TreeDesc(ctypes.Structure):
     _fields_ = [("batch", ctypes.c_int32), ("depth", ctypes.c_int32), ("k", ctypes.c_int32),
                 ("branch", ctypes.c_int32), ("budget", ctypes.c_int32), ("mode", ctypes.c_int32),
-                ("beam_width", ctypes.c_int32)]
+                ("beam_width", ctypes.c_int32), ("lambda_per_seq", ctypes.c_int32)]
 
 
 class AttnDesc(ctypes.Structure):
@@ -71,8 +72,10 @@ def lib() -> ctypes.CDLL:
         L = ctypes.CDLL(LIB_PATH)
         L.presto_topk_workspace.argtypes = [_I64, _I32, _I32]
         L.presto_topk_workspace.restype = _SZ
-        L.presto_topk.argtypes = [_I32, _VP, _I64, _I32, _I64, _I32, _VP, _VP, _VP, _VP, _VP, _SZ, _VP]
+        L.presto_topk.argtypes = [_I32, _VP, _I64, _I32, _I64, _I32] + [_VP] * 6 + [_SZ, _VP]
         L.presto_topk.restype = _I32
+        L.presto_entropy_lambda.argtypes = [_I64, _VP, ctypes.c_float, ctypes.c_float, _VP, _VP]
+        L.presto_entropy_lambda.restype = _I32
         L.presto_build_tree_workspace.argtypes = [ctypes.POINTER(TreeDesc)]
         L.presto_build_tree_workspace.restype = _SZ
         L.presto_build_tree.argtypes = [ctypes.POINTER(TreeDesc)] + [_VP] * 13 + [_SZ, _VP]
@@ -140,22 +143,42 @@ def version() -> str:
     return lib().presto_version().decode()
 
 
-def presto_topk(logits: torch.Tensor, k: int, *, ids=None, logprob=None, lse=None, flags=None,
-                workspace=None, stream=None):
-    """Top-k ids, log q and LSE of every row of logits [rows, V] (bf16 or fp32)."""
+def presto_topk(logits: torch.Tensor, k: int, *, ids=None, logprob=None, lse=None, entropy=None,
+                flags=None, workspace=None, stream=None):
+    """Top-k ids, log q and LSE of every row of logits [rows, V] (bf16 or fp32).
+
+    With ``entropy`` (a [rows] fp32 tensor, or True to allocate one) the
+    softmax entropy of each row is written too and returned fourth."""
     _rows(logits)
     rows, V = logits.shape
     dev = logits.device
     ids = torch.empty(rows, k, dtype=torch.int32, device=dev) if ids is None else ids
     logprob = torch.empty(rows, k, dtype=torch.float32, device=dev) if logprob is None else logprob
     lse = torch.empty(rows, dtype=torch.float32, device=dev) if lse is None else lse
-    _dev(ids, logprob, lse, flags)
+    want_h = entropy is not None and entropy is not False
+    if entropy is True:
+        entropy = torch.empty(rows, dtype=torch.float32, device=dev)
+    h = entropy if want_h else None
+    _dev(ids, logprob, lse, h, flags)
     need = lib().presto_topk_workspace(rows, V, k)
     ws, nb = _workspace(need, dev, workspace)
     _check(lib().presto_topk(_dt(logits), _ptr(logits), rows, V, logits.stride(0), k, _ptr(ids),
-                             _ptr(logprob), _ptr(lse), _ptr(flags), _ptr(ws), nb, _stream(stream)),
+                             _ptr(logprob), _ptr(lse), _ptr(h), _ptr(flags), _ptr(ws), nb,
+                             _stream(stream)),
            "presto_topk")
-    return ids, logprob, lse
+    return (ids, logprob, lse, h) if want_h else (ids, logprob, lse)
+
+
+def presto_entropy_lambda(entropy: torch.Tensor, beta: float, c: float, *, out=None, stream=None):
+    """Entropy-adaptive weight beta * H / (H + C) of every entry of entropy."""
+    out = torch.empty_like(entropy) if out is None else out
+    _dev(entropy, out)
+    if entropy.dtype != torch.float32 or out.dtype != torch.float32 or out.shape != entropy.shape:
+        raise ValueError("entropy and out must be fp32 tensors of one shape")
+    _check(lib().presto_entropy_lambda(entropy.numel(), _ptr(entropy), float(beta), float(c),
+                                       _ptr(out), _stream(stream)),
+           "presto_entropy_lambda")
+    return out
 
 
 def presto_build_tree(ids: torch.Tensor, logprob: torch.Tensor, log_rho, lam: torch.Tensor,
@@ -163,7 +186,8 @@ def presto_build_tree(ids: torch.Tensor, logprob: torch.Tensor, log_rho, lam: to
                       branch: int | None = None, mode: int = PRESTO_TREE_BEST_FIRST, *, out=None,
                       workspace=None, stream=None, beam_width: int = 0) -> dict:
     """Draft tree per sequence (best-first, or beam search of width
-    `beam_width`): ids/logprob [b*D, k] or [b, D, k]."""
+    `beam_width`): ids/logprob [b*D, k] or [b, D, k]; lam [D], or [b, D]
+    for a weight per sequence and position."""
     branch = k if branch is None else branch
     b = root_token.shape[0]
     N = budget + 1
@@ -179,7 +203,10 @@ def presto_build_tree(ids: torch.Tensor, logprob: torch.Tensor, log_rho, lam: to
             "score": torch.empty(b, N, dtype=torch.float32, device=dev),
             "anc": torch.empty(b, N, W, dtype=torch.int64, device=dev),
         }
-    desc = TreeDesc(b, depth, k, branch, budget, mode, beam_width)
+    per_seq = lam.dim() == 2
+    if per_seq and tuple(lam.shape) != (b, depth):
+        raise ValueError("a 2-D lambda must be [batch, depth]")
+    desc = TreeDesc(b, depth, k, branch, budget, mode, beam_width, int(per_seq))
     need = lib().presto_build_tree_workspace(ctypes.byref(desc))
     ws, nb = _workspace(need, dev, workspace)
     _check(lib().presto_build_tree(

@@ -11,9 +11,11 @@
 namespace presto_host {
 
 size_t topk_workspace_bytes(int64_t rows, int32_t vocab, int32_t k);
+presto_status launch_entropy_lambda(int64_t rows, const float* entropy, float beta, float c,
+                                    float* lambda, hipStream_t stream);
 presto_status launch_topk(bool bf16, const void* logits, int64_t rows, int32_t vocab,
                           int64_t row_stride, int32_t k, int32_t* ids, float* logprob, float* lse,
-                          int32_t* flags, void* ws, hipStream_t stream);
+                          float* entropy, int32_t* flags, void* ws, hipStream_t stream);
 bool tree_build_fits(int D, int k, int branch, int N, int beam_width);
 int tree_max_depth(int k);
 presto_status launch_build_tree(const presto_tree_desc* desc, const int32_t* ids,
@@ -77,7 +79,8 @@ size_t presto_topk_workspace(int64_t rows, int32_t vocab, int32_t k) {
 
 presto_status presto_topk(presto_dtype dt, const void* logits, int64_t rows, int32_t vocab,
                           int64_t row_stride, int32_t k, int32_t* ids, float* logprob, float* lse,
-                          int32_t* flags, void* ws, size_t ws_bytes, hipStream_t stream) {
+                          float* entropy, int32_t* flags, void* ws, size_t ws_bytes,
+                          hipStream_t stream) {
     g_err[0] = 0;
     REQUIRE(valid_dtype(dt), "presto_topk: unknown dtype %d", (int)dt);
     REQUIRE(rows >= 0, "presto_topk: rows < 0");
@@ -92,7 +95,18 @@ presto_status presto_topk(presto_dtype dt, const void* logits, int64_t rows, int
     presto_status st = check_ws(ws, ws_bytes, presto_topk_workspace(rows, vocab, k));
     if (st != PRESTO_OK) return st;
     return launch_topk(dt == PRESTO_DT_BF16, logits, rows, vocab, row_stride, k, ids, logprob, lse,
-                       flags, ws, stream);
+                       entropy, flags, ws, stream);
+}
+
+presto_status presto_entropy_lambda(int64_t rows, const float* entropy, float beta, float c,
+                                    float* lambda, hipStream_t stream) {
+    g_err[0] = 0;
+    REQUIRE(rows >= 0, "presto_entropy_lambda: rows < 0");
+    REQUIRE(isfinite(beta) && beta > 0.f, "presto_entropy_lambda: beta must be positive");
+    REQUIRE(isfinite(c) && c > 0.f, "presto_entropy_lambda: C must be positive");
+    if (rows == 0) return PRESTO_OK;
+    REQUIRE(entropy && lambda, "presto_entropy_lambda: null pointer");
+    return launch_entropy_lambda(rows, entropy, beta, c, lambda, stream);
 }
 
 size_t presto_build_tree_workspace(const presto_tree_desc* desc) {

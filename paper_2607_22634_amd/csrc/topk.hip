@@ -104,11 +104,12 @@ __device__ __forceinline__ uint32_t wave_kth_largest_u32(uint32_t x, int k) {
     return t;
 }
 
-template <bool BF16, int NLOAD>
+// ENT: also the chunk's sum of exp(z - m) * (z - m), for the entropy of q.
+template <bool BF16, int NLOAD, bool ENT>
 __global__ __launch_bounds__(kTopkWavesPerBlock * kWave) void topk_partial_kernel(
     const void* __restrict__ logits, int64_t rows, int32_t vocab, int64_t row_stride, int32_t k,
     int32_t chunks, bool aligned, float2* __restrict__ part_ms, uint64_t* __restrict__ part_keys,
-    int32_t* __restrict__ flags) {
+    float* __restrict__ part_h, int32_t* __restrict__ flags) {
     constexpr int P = VecTraits<BF16>::kPerVec;  // elements per 16-byte load (a "group")
     constexpr int E = NLOAD * P;
     constexpr int64_t CH = (int64_t)kWave * E;
@@ -141,22 +142,40 @@ __global__ __launch_bounds__(kTopkWavesPerBlock * kWave) void topk_partial_kerne
 #pragma unroll
     for (int i = 1; i < NLOAD; ++i) lm = fmaxf(lm, gmax[i]);
     const float M = wave_max_f32_dpp(lm);
-    // For moderate M: exp(z - M) = exp2(fma(z, log2 e, -mo)) * 2^r with
+    // For moderate M: exp(z - M) = exp2(fma(z, log2 e, -mo)) * 2^-r with
     // mo = fl(M log2 e) and r = M log2 e - mo taken exactly by one fma (|r| is
     // below 2^-16 here), so one fma and one exp per entry.  Larger |M| takes
     // the plain form exp2((z - M) log2 e).
-    float s = 0.f;
-    float corr = 1.f;
+    // Each entry's exponent is x = fl(z log2 e - mo) = (z - M) log2 e + r, so
+    // exp(z - M) = 2^x * 2^-r (corr = 2^-r), and with ENT
+    // sum exp(z - M) (z - M) = corr * sum 2^x (x - r) / log2 e.
+    float s = 0.f, sx = 0.f;
+    float corr = 1.f, rr = 0.f;
     if (fabsf(M) < 256.f) {
         const float mo = M * kLog2eF;
-        corr = __builtin_amdgcn_exp2f(fmaf(M, kLog2eF, -mo));
+        rr = fmaf(M, kLog2eF, -mo);
+        corr = __builtin_amdgcn_exp2f(-rr);
 #pragma unroll
-        for (int e = 0; e < E; ++e) s += __builtin_amdgcn_exp2f(fmaf(v[e], kLog2eF, -mo));
+        for (int e = 0; e < E; ++e) {
+            const float x = fmaf(v[e], kLog2eF, -mo);
+            const float ex = __builtin_amdgcn_exp2f(x);
+            s += ex;
+            // a -inf entry (masked, or padding past the row end) has q = 0 and
+            // adds nothing; without the select it would add 0 * -inf
+            if constexpr (ENT) sx = fmaf(ex, ex != 0.f ? x - rr : 0.f, sx);
+        }
     } else if (M != -INFINITY) {
 #pragma unroll
-        for (int e = 0; e < E; ++e) s += __builtin_amdgcn_exp2f((v[e] - M) * kLog2eF);
+        for (int e = 0; e < E; ++e) {
+            const float x = (v[e] - M) * kLog2eF;
+            const float ex = __builtin_amdgcn_exp2f(x);
+            s += ex;
+            if constexpr (ENT) sx = fmaf(ex, ex != 0.f ? x : 0.f, sx);
+        }
     }
     const float S = wave_sum_f32_dpp(s) * corr;
+    float Hx = 0.f;  // sum over the chunk of exp(z - M) (z - M)
+    if constexpr (ENT) Hx = wave_sum_f32_dpp(sx) * corr * (1.f / kLog2eF);
     // the k-th largest lane maximum bounds the chunk's k-th value from below:
     // only groups whose maximum reaches it can hold a top-k entry
     const float thr = unord32(wave_kth_largest_u32(ord32(lm), k));
@@ -216,6 +235,7 @@ __global__ __launch_bounds__(kTopkWavesPerBlock * kWave) void topk_partial_kerne
     }
     if (lane == 0) {
         part_ms[gw] = make_float2(M, S);
+        if constexpr (ENT) part_h[gw] = Hx;
         if (!(S == S)) raise_flag(flags, PRESTO_FLAG_NAN_DRAFTER);
     }
 }
@@ -223,11 +243,14 @@ __global__ __launch_bounds__(kTopkWavesPerBlock * kWave) void topk_partial_kerne
 // One wave per row: LSE from the chunk (max, sum) pairs, then the k best of
 // the chunk keys by k rounds of wave-wide selection over keys held in
 // registers (KPL per lane; KPL == 0 re-reads them from memory).
-template <int KPL>
+// With ENT also the entropy H = -sum q log q = log S - (sum exp(z - M)(z - M)) / S
+// of the row, from the chunks' shifted sums.
+template <int KPL, bool ENT>
 __global__ __launch_bounds__(kTopkWavesPerBlock * kWave) void topk_merge_kernel(
     int64_t rows, int32_t chunks, int32_t k, const float2* __restrict__ part_ms,
-    const uint64_t* __restrict__ part_keys, int32_t* __restrict__ ids, float* __restrict__ logprob,
-    float* __restrict__ lse) {
+    const uint64_t* __restrict__ part_keys, const float* __restrict__ part_h,
+    int32_t* __restrict__ ids, float* __restrict__ logprob, float* __restrict__ lse,
+    float* __restrict__ entropy) {
     const int wave = threadIdx.x / kWave, lane = lane_id();
     const int64_t row = (int64_t)blockIdx.x * kTopkWavesPerBlock + wave;
     if (row >= rows) return;
@@ -246,14 +269,24 @@ __global__ __launch_bounds__(kTopkWavesPerBlock * kWave) void topk_merge_kernel(
     float m = -INFINITY;
     for (int c = lane; c < chunks; c += kWave) m = fmaxf(m, ms[c].x);
     const float M = wave_max_f32_dpp(m);
-    float s = 0.f;
+    float s = 0.f, hx = 0.f;
     if (M != -INFINITY)
         for (int c = lane; c < chunks; c += kWave) {
             const float2 p = ms[c];
-            s += p.x == -INFINITY ? 0.f : p.y * __expf(p.x - M);
+            if (p.x != -INFINITY) {
+                const float w = __expf(p.x - M);
+                s += p.y * w;
+                // chunk sums shift to the row max: (z - M) = (z - m_c) + (m_c - M)
+                if constexpr (ENT) hx += w * (part_h[row * chunks + c] + (p.x - M) * p.y);
+            }
         }
     const float S = wave_sum_f32_dpp(s);
-    const float L = (M == -INFINITY) ? -INFINITY : M + __logf(S);
+    const float logS = __logf(S);
+    const float L = (M == -INFINITY) ? -INFINITY : M + logS;
+    if constexpr (ENT) {
+        const float HX = wave_sum_f32_dpp(hx);
+        if (lane == 0) entropy[row] = (M == -INFINITY) ? 0.f : logS - HX / S;
+    }
 
     uint64_t last = ~0ull, mine = 0ull;
     for (int j = 0; j < k; ++j) {
@@ -272,9 +305,21 @@ __global__ __launch_bounds__(kTopkWavesPerBlock * kWave) void topk_merge_kernel(
     }
     if (lane < k) {
         ids[row * k + lane] = (int32_t)key_id(mine);
-        logprob[row * k + lane] = (L == -INFINITY) ? -INFINITY : key_value(mine) - L;
+        // (z - M) - log S rather than z - L: z - M is exact for the top
+        // entries, so large logits do not lose the ulp of L
+        logprob[row * k + lane] = (L == -INFINITY) ? -INFINITY : (key_value(mine) - M) - logS;
     }
     if (lse && lane == 0) lse[row] = L;
+}
+
+// Entropy-adaptive interpolation weight: lambda = beta * H / (H + C), per row.
+__global__ void entropy_lambda_kernel(int64_t rows, const float* __restrict__ entropy, float beta,
+                                      float c, float* __restrict__ lambda) {
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < rows) {
+        const float h = entropy[i];
+        lambda[i] = beta * (h / (h + c));
+    }
 }
 
 }  // namespace presto
@@ -293,13 +338,13 @@ static int topk_nload(bool bf16, int64_t rows, int32_t vocab) {
 size_t topk_workspace_bytes(int64_t rows, int32_t vocab, int32_t k) {
     // sized for the finest chunking any dtype may pick
     const int64_t chunks = (vocab + (int64_t)kWave * 16 - 1) / ((int64_t)kWave * 16);
-    const size_t per = (size_t)chunks * (sizeof(float2) + sizeof(uint64_t) * (size_t)k);
-    return (size_t)rows * per + 256;
+    const size_t per = (size_t)chunks * (sizeof(float2) + sizeof(uint64_t) * (size_t)k + sizeof(float));
+    return (size_t)rows * per + 512;
 }
 
 presto_status launch_topk(bool bf16, const void* logits, int64_t rows, int32_t vocab,
                           int64_t row_stride, int32_t k, int32_t* ids, float* logprob, float* lse,
-                          int32_t* flags, void* ws, hipStream_t stream) {
+                          float* entropy, int32_t* flags, void* ws, hipStream_t stream) {
     const int nload = topk_nload(bf16, rows, vocab);
     const int64_t ch = (int64_t)kWave * nload * (bf16 ? 8 : 4);
     const int64_t chunks = (vocab + ch - 1) / ch;
@@ -308,33 +353,49 @@ presto_status launch_topk(bool bf16, const void* logits, int64_t rows, int32_t v
     float2* ms = static_cast<float2*>(ws);
     uint64_t* keys = reinterpret_cast<uint64_t*>(
         (reinterpret_cast<uintptr_t>(ms + rows * chunks) + 15) & ~uintptr_t(15));
+    float* hs = reinterpret_cast<float*>(
+        (reinterpret_cast<uintptr_t>(keys + rows * chunks * k) + 15) & ~uintptr_t(15));
+    const bool ent = entropy != nullptr;
     const int64_t waves = rows * chunks;
     const dim3 block(kTopkWavesPerBlock * kWave);
     const dim3 grid((unsigned)((waves + kTopkWavesPerBlock - 1) / kTopkWavesPerBlock));
-#define PRESTO_TOPK(BF, NL)                                                                 \
-    topk_partial_kernel<BF, NL><<<grid, block, 0, stream>>>(logits, rows, vocab, row_stride, \
-                                                           k, (int32_t)chunks, aligned, ms,  \
-                                                           keys, flags)
+#define PRESTO_TOPK(BF, NL, EN)                                                              \
+    topk_partial_kernel<BF, NL, EN><<<grid, block, 0, stream>>>(logits, rows, vocab, row_stride, \
+                                                               k, (int32_t)chunks, aligned, ms,  \
+                                                               keys, hs, flags)
+#define PRESTO_TOPK2(BF, NL) \
+    if (ent) PRESTO_TOPK(BF, NL, true); else PRESTO_TOPK(BF, NL, false)
     if (bf16) {
-        if (nload == 8) PRESTO_TOPK(true, 8); else PRESTO_TOPK(true, 4);
+        if (nload == 8) { PRESTO_TOPK2(true, 8); } else { PRESTO_TOPK2(true, 4); }
     } else {
-        if (nload == 8) PRESTO_TOPK(false, 8); else PRESTO_TOPK(false, 4);
+        if (nload == 8) { PRESTO_TOPK2(false, 8); } else { PRESTO_TOPK2(false, 4); }
     }
+#undef PRESTO_TOPK2
 #undef PRESTO_TOPK
     presto_status st = check_launch("topk_partial_kernel");
     if (st != PRESTO_OK) return st;
     const dim3 mgrid((unsigned)((rows + kTopkWavesPerBlock - 1) / kTopkWavesPerBlock));
     const int64_t per_lane = (chunks * k + kWave - 1) / kWave;
-#define PRESTO_MERGE(KP)                                                                     \
-    topk_merge_kernel<KP><<<mgrid, block, 0, stream>>>(rows, (int32_t)chunks, k, ms, keys, \
-                                                       ids, logprob, lse)
-    if (per_lane <= 2) PRESTO_MERGE(2);
-    else if (per_lane <= 4) PRESTO_MERGE(4);
-    else if (per_lane <= 8) PRESTO_MERGE(8);
-    else if (per_lane <= 16) PRESTO_MERGE(16);
-    else PRESTO_MERGE(0);
+#define PRESTO_MERGE(KP, EN)                                                                    \
+    topk_merge_kernel<KP, EN><<<mgrid, block, 0, stream>>>(rows, (int32_t)chunks, k, ms, keys, hs, \
+                                                           ids, logprob, lse, entropy)
+#define PRESTO_MERGE2(KP) \
+    if (ent) PRESTO_MERGE(KP, true); else PRESTO_MERGE(KP, false)
+    if (per_lane <= 2) { PRESTO_MERGE2(2); }
+    else if (per_lane <= 4) { PRESTO_MERGE2(4); }
+    else if (per_lane <= 8) { PRESTO_MERGE2(8); }
+    else if (per_lane <= 16) { PRESTO_MERGE2(16); }
+    else { PRESTO_MERGE2(0); }
+#undef PRESTO_MERGE2
 #undef PRESTO_MERGE
     return check_launch("topk_merge_kernel");
+}
+
+presto_status launch_entropy_lambda(int64_t rows, const float* entropy, float beta, float c,
+                                    float* lambda, hipStream_t stream) {
+    entropy_lambda_kernel<<<(unsigned)((rows + 255) / 256), 256, 0, stream>>>(rows, entropy, beta, c,
+                                                                              lambda);
+    return check_launch("entropy_lambda_kernel");
 }
 
 }  // namespace presto_host

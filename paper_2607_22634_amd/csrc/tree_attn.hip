@@ -45,9 +45,8 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
 constexpr int kKeyTile = 64;      // keys per LDS tile: two 32-key blocks per barrier
 constexpr int kBlocksPerTile = kKeyTile / 32;
 constexpr int kBufs = 3;          // LDS tile buffers
-constexpr float kSlack = 8.f;
-constexpr int kMaxAncWords = 16;
-constexpr int kValuPerMfma = 4;   // VALU ops issued behind each MFMA of a key block  // ancestor words per node: n_max <= 1024     // log2 headroom before the accumulator is rescaled
+constexpr float kSlack = 8.f;     // log2 headroom before the accumulator is rescaled
+constexpr int kMaxAncWords = 16;  // ancestor words per node: n_max <= 1024
 constexpr int kRowsPerWave = 32;  // one 32-row MFMA block per wave
 // Workgroups are 8 waves, two per SIMD: one wave's softmax hides behind the
 // other's MFMAs (with one wave per SIMD the matrix cores sit idle during it).

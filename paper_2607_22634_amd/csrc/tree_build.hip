@@ -38,6 +38,7 @@ struct TreeArgs {
     const float* logprob;
     const float* log_rho;
     const float* lambda;
+    int32_t lambda_stride;  // 0: one lambda row shared by the batch, D: one per sequence
     const int32_t* root_token;
     int32_t* n_nodes;
     int32_t* parent;
@@ -135,7 +136,8 @@ __global__ __launch_bounds__(kWave) void tree_build_kernel(TreeArgs a) {
     if constexpr (RHO == 1)
         stage_words(reinterpret_cast<uint32_t*>(s_rho), reinterpret_cast<const uint32_t*>(g_rho), rho_n,
                     lane);
-    const float lam_lane = lane < D ? a.lambda[lane] : 0.f;  // lambda_d held by lane d
+    const float lam_lane =
+        lane < D ? a.lambda[(int64_t)b * a.lambda_stride + lane] : 0.f;  // lambda_d held by lane d
     __builtin_amdgcn_wave_barrier();
 
     // token score of candidate r at drafter row `row` under the trigram
@@ -556,6 +558,7 @@ presto_status launch_build_tree(const presto_tree_desc* desc, const int32_t* ids
     a.logprob = logprob;
     a.log_rho = log_rho;
     a.lambda = lambda;
+    a.lambda_stride = desc->lambda_per_seq ? desc->depth : 0;
     a.root_token = root_token;
     a.n_nodes = n_nodes;
     a.parent = parent;

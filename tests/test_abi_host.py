@@ -51,24 +51,37 @@ def _err(status):
 
 def test_topk_rejects_bad_arguments():
     lib = P.lib()
-    st, msg = _err(lib.presto_topk(0, None, 4, 1024, 1024, 0, None, None, None, None, None, 0, None))
+    st, msg = _err(lib.presto_topk(0, None, 4, 1024, 1024, 0, None, None, None, None, None, None, 0, None))
     assert st == P.PRESTO_ERR_INVALID_ARG and "k=0" in msg
-    st, _ = _err(lib.presto_topk(0, None, 4, 1024, 1000, 2, None, None, None, None, None, 0, None))
+    st, _ = _err(lib.presto_topk(0, None, 4, 1024, 1000, 2, None, None, None, None, None, None, 0, None))
     assert st == P.PRESTO_ERR_INVALID_ARG
-    st, _ = _err(lib.presto_topk(7, None, 4, 1024, 1024, 2, None, None, None, None, None, 0, None))
+    st, _ = _err(lib.presto_topk(7, None, 4, 1024, 1024, 2, None, None, None, None, None, None, 0, None))
     assert st == P.PRESTO_ERR_INVALID_ARG
-    st, _ = _err(lib.presto_topk(0, None, 4, 1024, 1024, 17, None, None, None, None, None, 0, None))
+    st, _ = _err(lib.presto_topk(0, None, 4, 1024, 1024, 17, None, None, None, None, None, None, 0, None))
     assert st == P.PRESTO_ERR_UNSUPPORTED
-    st, _ = _err(lib.presto_topk(0, None, 4, 1024, 1024, 2, None, None, None, None, None, 0, None))
+    st, _ = _err(lib.presto_topk(0, None, 4, 1024, 1024, 2, None, None, None, None, None, None, 0, None))
     assert st == P.PRESTO_ERR_INVALID_ARG  # null pointers
     # zero rows is a no-op, even without pointers
-    assert lib.presto_topk(0, None, 0, 1024, 1024, 2, None, None, None, None, None, 0, None) == 0
+    assert lib.presto_topk(0, None, 0, 1024, 1024, 2, None, None, None, None, None, None, 0, None) == 0
+
+
+def test_entropy_lambda_rejects_bad_arguments():
+    lib = P.lib()
+    fake = ctypes.c_void_p(0x1000)  # never dereferenced: the checks fail first
+    for beta, c in [(0.0, 1.0), (-1.0, 1.0), (1.0, 0.0), (float("nan"), 1.0), (1.0, float("inf"))]:
+        st, msg = _err(lib.presto_entropy_lambda(4, fake, beta, c, fake, None))
+        assert st == P.PRESTO_ERR_INVALID_ARG and ("beta" in msg or "C" in msg)
+    st, _ = _err(lib.presto_entropy_lambda(4, None, 1.0, 1.0, None, None))
+    assert st == P.PRESTO_ERR_INVALID_ARG
+    st, _ = _err(lib.presto_entropy_lambda(-1, fake, 1.0, 1.0, fake, None))
+    assert st == P.PRESTO_ERR_INVALID_ARG
+    assert lib.presto_entropy_lambda(0, None, 1.0, 1.0, None, None) == P.PRESTO_OK
 
 
 def test_topk_rejects_small_workspace():
     lib = P.lib()
     fake = ctypes.c_void_p(0x1000)  # never dereferenced: the check fails first
-    st, msg = _err(lib.presto_topk(0, fake, 4, 1024, 1024, 2, fake, fake, None, None, fake, 8, None))
+    st, msg = _err(lib.presto_topk(0, fake, 4, 1024, 1024, 2, fake, fake, None, None, None, fake, 8, None))
     assert st == P.PRESTO_ERR_WORKSPACE and "workspace" in msg
 
 

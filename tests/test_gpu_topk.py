@@ -1,5 +1,7 @@
 """GPU parity of presto_topk against the oracle (ids bit-exact, log q within
-1e-5 * max(1, |ref|)), at the five workloads' full sizes and on edge cases."""
+1e-5 * max(1, |ref|)), at the five workloads' full sizes and on edge cases;
+the entropy output and the entropy-adaptive weight (Appendix F) against the
+oracle's fp64 values."""
 import numpy as np
 import pytest
 import torch
@@ -108,3 +110,61 @@ def test_topk_workspace_reuse_keeps_results():
         again = [to_host(x) for x in P.presto_topk(t, w.k, workspace=ws)]
         for u, v in zip(first, again):
             np.testing.assert_array_equal(u, v)
+
+
+def _compare_entropy(store, dtype, h):
+    """The kernel forms H = log S - X / S with S = sum e^(z-M) and
+    X = sum e^(z-M) (z-M), M the row max.  log S is the min-entropy, so
+    0 <= log S <= H and -X / S = E_q[M - z] = H - log S lies in [0, H]: each
+    term is at most H and carries a relative error of a few hundred fp32
+    ulps after the sums over V terms, giving the bound 2e-5 * (1 + H)."""
+    rh = oracle.entropy(store, dtype)
+    h = to_host(h).astype(np.float64)
+    tol = 2e-5 * (1.0 + rh)
+    err = np.abs(h - rh)
+    assert (err <= tol).all(), (err / tol).max()
+
+
+@pytest.mark.parametrize("cfg", [1, 2, 3, 4, 5])
+def test_topk_entropy_matches_oracle_on_workload(cfg):
+    """With the entropy output on, ids/log q/LSE stay as before and H_d
+    (Appendix F) matches the oracle's fp64 entropy."""
+    w, rin = round_data(cfg)
+    logits = rin["drafter_logits"]
+    print(f"topk+entropy cfg={cfg} rows={logits.shape[0]}", flush=True)
+    ids, lp, lse, h = P.presto_topk(to_dev(logits, w.dtype), w.k, entropy=True)
+    torch.cuda.synchronize()
+    _compare(logits, w.dtype, w.k, ids, lp, lse)
+    _compare_entropy(logits, w.dtype, h)
+
+
+@pytest.mark.parametrize("dtype,V,k", EDGE)
+def test_topk_entropy_edge_rows(dtype, V, k):
+    rng = np.random.default_rng([V, k, 12])
+    x = (rng.standard_normal((8, V)) * 4).astype(np.float32)
+    x[1, :] = 1.5                                   # uniform: H = log V
+    x[2, :] = -np.inf
+    x[2, V // 2] = 3.0                              # point mass: H = 0
+    x[3, ::2] = -np.inf                             # zero-probability entries
+    x[4, :] = -np.inf                               # no distribution: H = 0
+    x[5, :] = -1e30                                 # uniform far below zero
+    x[6, :] = x[6] * 60                             # nearly one-hot
+    x[7, :] = 300.0 + x[7]                          # large offsets
+    store = sy.cast(x, dtype)
+    ids, lp, lse, h = P.presto_topk(to_dev(store, dtype), k, entropy=True)
+    torch.cuda.synchronize()
+    _compare(store, dtype, k, ids, lp, lse)
+    _compare_entropy(store, dtype, h)
+    hh = to_host(h)
+    assert hh[2] == 0.0 and hh[4] == 0.0
+
+
+def test_entropy_lambda_matches_oracle():
+    rng = np.random.default_rng(21)
+    h = np.concatenate([[0.0, 1e-30, 1.5, 12.0, 1e6], rng.uniform(0, 12, 4091)]).astype(np.float32)
+    for beta, c in [(1.0, 1.0), (0.35, 2.5), (4.0, 0.01)]:
+        lam = to_host(P.presto_entropy_lambda(to_dev(h), beta, c))
+        want = oracle.entropy_lambda(h.astype(np.float64), np.float32(beta), np.float32(c))
+        # three fp32 roundings (H + C, the quotient, the product)
+        np.testing.assert_allclose(lam, want, rtol=4e-7, atol=0)
+        assert lam[0] == 0.0

@@ -113,3 +113,30 @@ def test_beam_tree_matches_oracle_random(D, k, branch, B, W, quant):
         g, o = _gpu_and_oracle(ids, lp, rho, lam, root, D, k, B, branch=branch, beam_width=W)
         _assert_same(g, o)
 
+
+
+@pytest.mark.parametrize("cfg,beam_width", [(2, 0), (3, 0), (4, 0), (3, 4)])
+def test_tree_with_entropy_adaptive_lambda(cfg, beam_width):
+    """Per-sequence, per-position weights lambda_d(H_d) (Appendix F): the
+    weights come from the oracle's entropies and enter both sides as the
+    same fp32 [batch, depth] table."""
+    w, rin = round_data(cfg)
+    print(f"tree entropy-lambda cfg={cfg} W={beam_width}", flush=True)
+    ids, lp, _ = P.presto_topk(to_dev(rin["drafter_logits"], w.dtype), w.k)
+    ids = to_host(ids).reshape(w.batch, w.depth, w.k)
+    lp = to_host(lp).reshape(w.batch, w.depth, w.k)
+    h = oracle.entropy(rin["drafter_logits"], w.dtype)
+    lam = oracle.entropy_lambda(h, 0.6, 2.0).astype(np.float32).reshape(w.batch, w.depth)
+    assert np.ptp(lam) > 0  # the weights really vary
+    g, o = _gpu_and_oracle(ids, lp, rin["rho"], lam, rin["root_token"], w.depth, w.k, w.budget,
+                           beam_width=beam_width)
+    _assert_same(g, o)
+
+
+def test_tree_per_sequence_lambda_random():
+    D, k, B, b = 12, 5, 130, 24
+    ids, lp, R, root = _random_batch([D, k, B, 77], b, D, k, False)
+    lam = np.random.default_rng(3).uniform(0, 1.5, (b, D)).astype(np.float32)
+    lam[::5] = 0.0
+    g, o = _gpu_and_oracle(ids, lp, R, lam, root, D, k, B, branch=4)
+    _assert_same(g, o)

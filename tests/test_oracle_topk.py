@@ -49,6 +49,17 @@ def test_topk_negative_zero_ties_positive_zero():
     assert ids.tolist() == [[5, 0, 1]]
 
 
+@pytest.mark.parametrize("offset", [-1e30, -3e8, 1e20, 300.0])
+def test_topk_constant_row_far_from_zero(offset):
+    """A constant row is uniform whatever its offset: log q = -log V exactly,
+    even where fp64 cannot hold offset + log V."""
+    V = 1000
+    x = np.full((1, V), offset, np.float32)
+    ids, lp, lse, _ = oracle.topk(x, 3, "f32")
+    assert ids.tolist() == [[0, 1, 2]]
+    np.testing.assert_array_equal(lp, np.float32(-np.log(V)))
+
+
 def test_topk_all_neg_inf_row():
     x = np.full((1, 16), -np.inf, np.float32)
     ids, lp, lse, _ = oracle.topk(x, 2, "f32")
