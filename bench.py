@@ -210,9 +210,11 @@ def main() -> int:
     roof["frac"] = round(roof["achieved"] / roof["peak"], 4)
     roof["traffic"] = None
 
+    extra = measure_next_rows(P, sy, w, R, reps, timed, topk_out, topk_ws, tree_out, rin, dev)
+
     cpu = None
     if not args.no_cpu_baseline:
-        cpu = cpu_baseline(w, rin, layers, th, target, args.cpu_seconds)
+        cpu = cpu_baseline(w, rin, layers, args.cpu_seconds)
 
     line = {
         "metric": METRIC, "value": round(1e3 / ms_per_step, 2), "unit": "rounds/s", "n_gpus": 1,
@@ -224,7 +226,7 @@ def main() -> int:
                                f"ctx {w.ctx[0]}-{w.ctx[1]}, {w.layers} layer(s)",
                    "global_batch": w.batch, "replicas": reps},
         "sequence_rounds_per_s": round(w.batch * 1e3 / ms_per_step, 2),
-        "stages": stages, "roofline": roof, "cpu_baseline": cpu,
+        "stages": stages, "roofline": roof, "cpu_baseline": cpu, "next_rows": extra,
         "accept_len": acc_out["accept_len"].cpu().tolist(),
         "gen_seconds": round(gen_s, 1),
     }
@@ -232,7 +234,64 @@ def main() -> int:
     return 0
 
 
-def cpu_baseline(w, rin, layers, th, target, seconds):
+def measure_next_rows(P, sy, w, R, reps, timed, topk_out, topk_ws, tree_out, rin, dev):
+    """Per-launch times of the parts adjacent to the round (not in the step):
+    top-k with the entropy output, the entropy-adaptive weight, the trigram
+    lattice gather (and the one-time table build), beam-search trees."""
+    import torch
+
+    rows = w.batch * w.depth
+    e = 2 if w.dtype == "bf16" else 4
+    n = 20
+    ent = torch.empty(rows, dtype=torch.float32, device=dev)
+    lam_t = torch.empty(rows, dtype=torch.float32, device=dev)
+    out = {}
+
+    def topk_ent(r):
+        P.presto_topk(R[r]["drafter"], w.k, ids=topk_out[0], logprob=topk_out[1], lse=topk_out[2],
+                      entropy=ent, workspace=topk_ws)
+
+    us = timed(topk_ent, n, 0) * 1e3
+    out["topk_entropy"] = {"us": round(us, 2),
+                           "GB/s": round((rows * w.vocab * e + rows * (8 * w.k + 8)) / (us * 1e3), 1)}
+    out["entropy_lambda"] = {"us": round(timed(lambda r: P.presto_entropy_lambda(ent, 0.6, 2.0,
+                                                                                 out=lam_t), n, 0)
+                                         * 1e3, 2)}
+
+    # trigram table: walks through this round's candidates plus 1M background trigrams
+    ids_h = topk_out[0].view(w.batch, w.depth, w.k).cpu().numpy()
+    t2, t1, t, lr = sy.trigram_entries(w, ids_h, 64, 1_000_000)
+    cap = 1 << max(6, int(np.ceil(np.log2(2 * len(t)))))
+    table = torch.empty(P.presto_ngram_table_bytes(cap), dtype=torch.uint8, device=dev)
+    cols = [torch.from_numpy(x).to(dev) for x in (t2, t1, t, lr)]
+    flags = torch.zeros(1, dtype=torch.int32, device=dev)
+
+    def build(r):
+        P.presto_ngram_clear(table, cap)
+        P.presto_ngram_insert(table, cap, *cols, flags=flags)
+
+    build_ms = timed(build, 3, 0)
+    assert int(flags.item()) == 0, "trigram table build flagged an entry"
+    prev = torch.from_numpy(sy.prev_tokens(w)).to(dev)
+    root = torch.from_numpy(rin["root_token"]).to(dev)
+    lat = torch.empty(w.batch, w.depth, w.k, w.k, w.k, dtype=torch.float32, device=dev)
+    us = timed(lambda r: P.presto_ngram_gather(table, cap, float(np.log(1e-4)), topk_out[0], prev,
+                                               root, w.depth, w.k, out=lat), n, 0) * 1e3
+    out["ngram_gather"] = {"us": round(us, 2), "lattice_entries": int(lat.numel()),
+                           "table_entries": int(len(t)), "table_slots": cap,
+                           "table_build_ms": round(build_ms, 3)}
+
+    lam = torch.from_numpy(rin["lam"]).to(dev)
+    rho = torch.from_numpy(rin["rho"]).to(dev)
+    beam_out = {k: torch.empty_like(v) for k, v in tree_out.items()}
+    us = timed(lambda r: P.presto_build_tree(topk_out[0], topk_out[1], rho, lam, root, w.depth,
+                                             w.k, w.budget, mode=P.PRESTO_TREE_BEAM,
+                                             beam_width=10, out=beam_out), n, 0) * 1e3
+    out["build_tree_beam10"] = {"us": round(us, 2)}
+    return out
+
+
+def cpu_baseline(w, rin, layers, seconds):
     """The oracle, as it stands, on whole rounds of the same workload for ~`seconds`."""
     import oracle
 
@@ -244,9 +303,15 @@ def cpu_baseline(w, rin, layers, th, target, seconds):
         t = t.detach().cpu()
         return t.view(torch.int16).numpy().view(np.uint16) if t.dtype == torch.bfloat16 else t.numpy()
 
+    import synthetic as sy
+
     att = [{k: host(v) for k, v in L.items()} for L in layers]
-    T = host(target)
     D, k = w.depth, w.k
+    # the target rows follow the oracle's own tree (input synthesis, untimed)
+    ids0, lp0, _, _ = oracle.topk(rin["drafter_logits"], k, w.dtype)
+    tr0 = oracle.build_tree(ids0.reshape(w.batch, D, k), lp0.reshape(w.batch, D, k), rin["rho"],
+                            rin["lam"], rin["root_token"], D, k, w.budget)
+    T = sy.target_logits(w, rin["field"], tr0["parent"], tr0["rank"], tr0["n_nodes"])
     n = 0
     t0 = time.time()
     while True:

@@ -66,7 +66,9 @@ typedef enum {
 /* Bits ORed into the optional `flags` word. */
 enum {
     PRESTO_FLAG_NAN_DRAFTER = 1, /* a drafter logit row held a NaN (or +inf)   */
-    PRESTO_FLAG_NAN_TARGET = 2   /* a live target logit row held a NaN         */
+    PRESTO_FLAG_NAN_TARGET = 2,  /* a live target logit row held a NaN         */
+    PRESTO_FLAG_NGRAM_BAD = 4,   /* an n-gram entry was invalid and skipped    */
+    PRESTO_FLAG_NGRAM_FULL = 8   /* an n-gram entry found no free table slot   */
 };
 
 /* ------------------------------------------------------------------------ */
@@ -108,6 +110,48 @@ presto_status presto_topk(presto_dtype dt, const void *logits, int64_t rows, int
  */
 presto_status presto_entropy_lambda(int64_t rows, const float *entropy, float beta, float c,
                                     float *lambda, hipStream_t stream);
+
+/* ------------------------------------------------------------------------ */
+/* Prefix-aligned signal from a trigram model (Sec. 5.1: rho is an n-gram
+ * model with n = 3).  The table is built once (off the per-round path) and
+ * each round gathers the lattice log_rho[b, d, r2, r1, r] that
+ * presto_build_tree reads, so the tree search itself never probes it.
+ *
+ * Table: caller device memory of presto_ngram_table_bytes(capacity) bytes,
+ * 8-byte aligned, capacity a power of two in 64 .. 2^32 (an open-addressing
+ * hash table; keep it at most about half full for short probes).  Tokens
+ * must lie in [0, 2^21).
+ *
+ * presto_ngram_clear   empties the table (must precede the first insert).
+ * presto_ngram_insert  adds n entries log rho(t[i] | t2[i], t1[i]) (device
+ *   arrays, t2 the older context token).  log rho must be finite and <= 0;
+ *   -0.0 is stored as +0.0.  A key inserted more than once keeps its
+ *   largest value, in any order of insertion.  Invalid entries are skipped
+ *   with PRESTO_FLAG_NGRAM_BAD, entries finding no free slot with
+ *   PRESTO_FLAG_NGRAM_FULL (flags may be NULL).  Calls may be repeated to
+ *   add more entries; concurrent inserts and gathers on one table race.
+ * presto_ngram_gather  fills log_rho [batch, depth, k, k, k] fp32 from
+ *   ids [batch, depth, k] (presto_topk's candidates), prev_token [batch]
+ *   (the committed token before the root, or -1 if none) and root_token
+ *   [batch]: entry (b, d, r2, r1, r) is log rho(t | t2, t1) with
+ *     t  = ids[b, d, r],
+ *     t1 = ids[b, d-1, r1] for d >= 1, else the root token,
+ *     t2 = ids[b, d-2, r2] for d >= 2, the root token for d = 1, else
+ *          prev_token[b],
+ *   or floor_log_rho (finite, <= 0) when that trigram is absent or a token
+ *   lies outside [0, 2^21).  This is the rank-slot convention of
+ *   presto_build_tree (slot 0 for a token outside the block); slots a depth
+ *   does not read repeat slot 0.  Limits: depth 1 .. 32, k 1 .. 16.
+ */
+size_t presto_ngram_table_bytes(int64_t capacity); /* 0 for an invalid capacity */
+presto_status presto_ngram_clear(void *table, int64_t capacity, hipStream_t stream);
+presto_status presto_ngram_insert(void *table, int64_t capacity, int64_t n, const int32_t *t2,
+                                  const int32_t *t1, const int32_t *t, const float *log_rho,
+                                  int32_t *flags, hipStream_t stream);
+presto_status presto_ngram_gather(const void *table, int64_t capacity, float floor_log_rho,
+                                  int32_t batch, int32_t depth, int32_t k, const int32_t *ids,
+                                  const int32_t *prev_token, const int32_t *root_token,
+                                  float *log_rho, hipStream_t stream);
 
 /* ------------------------------------------------------------------------ */
 /* Stage 2: prefix-aligned scoring and best-first tree construction.

@@ -89,6 +89,56 @@ def entropy_lambda(h, beta: float, c: float) -> np.ndarray:
     return out
 
 
+NGRAM_TOKEN_LIMIT = 1 << 21
+
+
+def ngram_table(t2, t1, t, log_rho) -> dict:
+    """Trigram model (Sec. 5.1: rho is an n-gram model with n = 3) as a
+    dictionary (t2, t1, t) -> log rho(t | t2, t1).  Entries with a token
+    outside [0, 2^21) or a log rho that is not finite and <= 0 are ignored;
+    a key given more than once keeps its largest value; -0.0 reads as +0.0."""
+    table = {}
+    for a, b, c, v in zip(np.asarray(t2).tolist(), np.asarray(t1).tolist(),
+                          np.asarray(t).tolist(), np.asarray(log_rho, np.float32).tolist()):
+        if not all(0 <= x < NGRAM_TOKEN_LIMIT for x in (a, b, c)):
+            continue
+        if not (np.isfinite(v) and v <= 0.0):
+            continue
+        v = v + 0.0
+        key = (a, b, c)
+        if key not in table or v > table[key]:
+            table[key] = v
+    return table
+
+
+def ngram_lattice(table: dict, floor: float, ids, prev_token, root_token) -> np.ndarray:
+    """log_rho lattice [b, D, k, k, k] for the tree stage (Eq. 9): entry
+    (b, d, r2, r1, r) is log rho(t | t2, t1) of candidate t = ids[b, d, r]
+    after the two tokens before it on a path: the parent t1 = ids[b, d-1, r1]
+    (the root token at d = 0) and the grandparent t2 = ids[b, d-2, r2] (the
+    root token at d = 1, the token before the root at d = 0); `floor` when
+    the table lacks the trigram."""
+    ids = np.asarray(ids)
+    B, D, k = ids.shape
+    out = np.empty((B, D, k, k, k), np.float32)
+    for b in range(B):
+        root, prev = int(root_token[b]), int(prev_token[b])
+        for d in range(D):
+            for r2 in range(k):
+                for r1 in range(k):
+                    parent = int(ids[b, d - 1, r1]) if d >= 1 else root
+                    if d >= 2:
+                        grand = int(ids[b, d - 2, r2])
+                    elif d == 1:
+                        grand = root
+                    else:
+                        grand = prev
+                    for r in range(k):
+                        out[b, d, r2, r1, r] = table.get((grand, parent, int(ids[b, d, r])),
+                                                         floor)
+    return out
+
+
 def build_tree(ids, logprob, rho, lam, root_token, depth: int, k: int, budget: int,
                branch: int | None = None, mode: int = BEST_FIRST, beam_width: int = 0) -> dict:
     """Tree per sequence (best-first, literal Alg. 2, or beam search with beam

@@ -8,7 +8,9 @@ functions carry the C names.
 from ._lib import (  # noqa: F401
     EXPORTS, PRESTO_DT_BF16, PRESTO_DT_F32, PRESTO_ERR_HIP, PRESTO_ERR_INVALID_ARG,
     PRESTO_ERR_UNSUPPORTED, PRESTO_ERR_WORKSPACE, PRESTO_FLAG_NAN_DRAFTER, PRESTO_FLAG_NAN_TARGET,
+    PRESTO_FLAG_NGRAM_BAD, PRESTO_FLAG_NGRAM_FULL,
     PRESTO_OK, PRESTO_TREE_BEAM, PRESTO_TREE_BEST_FIRST, PRESTO_TREE_BEST_FIRST_ALG2, AttnDesc,
-    PrestoError, TreeDesc, lib, presto_accept, presto_build_tree, presto_entropy_lambda, presto_topk,
+    PrestoError, TreeDesc, lib, presto_accept, presto_build_tree, presto_entropy_lambda, presto_ngram_clear,
+    presto_ngram_gather, presto_ngram_insert, presto_ngram_table_bytes, presto_topk,
     presto_tree_attention, version,
 )

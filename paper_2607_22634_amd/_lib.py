@@ -32,9 +32,12 @@ PRESTO_TREE_BEAM = 2
 
 PRESTO_FLAG_NAN_DRAFTER = 1
 PRESTO_FLAG_NAN_TARGET = 2
+PRESTO_FLAG_NGRAM_BAD = 4
+PRESTO_FLAG_NGRAM_FULL = 8
 
 EXPORTS = (
-    "presto_topk_workspace", "presto_topk", "presto_entropy_lambda", "presto_build_tree_workspace",
+    "presto_topk_workspace", "presto_topk", "presto_entropy_lambda", "presto_ngram_table_bytes",
+    "presto_ngram_clear", "presto_ngram_insert", "presto_ngram_gather", "presto_build_tree_workspace",
     "presto_build_tree",
     "presto_tree_attention_workspace", "presto_tree_attention", "presto_accept_workspace",
     "presto_accept", "presto_status_string", "presto_last_error", "presto_version",
@@ -76,6 +79,15 @@ def lib() -> ctypes.CDLL:
         L.presto_topk.restype = _I32
         L.presto_entropy_lambda.argtypes = [_I64, _VP, ctypes.c_float, ctypes.c_float, _VP, _VP]
         L.presto_entropy_lambda.restype = _I32
+        L.presto_ngram_table_bytes.argtypes = [_I64]
+        L.presto_ngram_table_bytes.restype = _SZ
+        L.presto_ngram_clear.argtypes = [_VP, _I64, _VP]
+        L.presto_ngram_clear.restype = _I32
+        L.presto_ngram_insert.argtypes = [_VP, _I64, _I64, _VP, _VP, _VP, _VP, _VP, _VP]
+        L.presto_ngram_insert.restype = _I32
+        L.presto_ngram_gather.argtypes = [_VP, _I64, ctypes.c_float, _I32, _I32, _I32, _VP, _VP,
+                                          _VP, _VP, _VP]
+        L.presto_ngram_gather.restype = _I32
         L.presto_build_tree_workspace.argtypes = [ctypes.POINTER(TreeDesc)]
         L.presto_build_tree_workspace.restype = _SZ
         L.presto_build_tree.argtypes = [ctypes.POINTER(TreeDesc)] + [_VP] * 13 + [_SZ, _VP]
@@ -178,6 +190,45 @@ def presto_entropy_lambda(entropy: torch.Tensor, beta: float, c: float, *, out=N
     _check(lib().presto_entropy_lambda(entropy.numel(), _ptr(entropy), float(beta), float(c),
                                        _ptr(out), _stream(stream)),
            "presto_entropy_lambda")
+    return out
+
+
+def presto_ngram_table_bytes(capacity: int) -> int:
+    """Bytes of device memory a trigram table of `capacity` slots needs."""
+    return int(lib().presto_ngram_table_bytes(capacity))
+
+
+def presto_ngram_clear(table: torch.Tensor, capacity: int, *, stream=None) -> None:
+    """Empty the trigram table held in `table` (a device byte tensor)."""
+    _dev(table)
+    _check(lib().presto_ngram_clear(_ptr(table), capacity, _stream(stream)), "presto_ngram_clear")
+
+
+def presto_ngram_insert(table: torch.Tensor, capacity: int, t2: torch.Tensor, t1: torch.Tensor,
+                        t: torch.Tensor, log_rho: torch.Tensor, *, flags=None, stream=None) -> None:
+    """Add entries log rho(t | t2, t1) (int32 / fp32 device vectors of one length)."""
+    _dev(table, t2, t1, t, log_rho, flags)
+    n = t.numel()
+    if not (t2.numel() == t1.numel() == log_rho.numel() == n):
+        raise ValueError("t2, t1, t and log_rho must have one length")
+    _check(lib().presto_ngram_insert(_ptr(table), capacity, n, _ptr(t2), _ptr(t1), _ptr(t),
+                                     _ptr(log_rho), _ptr(flags), _stream(stream)),
+           "presto_ngram_insert")
+
+
+def presto_ngram_gather(table: torch.Tensor, capacity: int, floor_log_rho: float,
+                        ids: torch.Tensor, prev_token: torch.Tensor, root_token: torch.Tensor,
+                        depth: int, k: int, *, out=None, stream=None) -> torch.Tensor:
+    """log_rho lattice [b, depth, k, k, k] for the candidates ids [b*depth, k]
+    or [b, depth, k]."""
+    b = root_token.shape[0]
+    out = torch.empty(b, depth, k, k, k, dtype=torch.float32, device=ids.device) if out is None \
+        else out
+    _dev(table, ids, prev_token, root_token, out)
+    _check(lib().presto_ngram_gather(_ptr(table), capacity, float(floor_log_rho), b, depth, k,
+                                     _ptr(ids), _ptr(prev_token), _ptr(root_token), _ptr(out),
+                                     _stream(stream)),
+           "presto_ngram_gather")
     return out
 
 

@@ -29,6 +29,14 @@ presto_status launch_tree_attention(const presto_attn_desc* d, const void* q, co
                                     const void* k_tree, const void* v_tree, const uint64_t* anc,
                                     const int32_t* n_nodes, void* out, void* ws,
                                     hipStream_t stream);
+presto_status launch_ngram_clear(void* table, int64_t capacity, hipStream_t stream);
+presto_status launch_ngram_insert(void* table, int64_t capacity, int64_t n, const int32_t* t2,
+                                  const int32_t* t1, const int32_t* t, const float* log_rho,
+                                  int32_t* flags, hipStream_t stream);
+presto_status launch_ngram_gather(const void* table, int64_t capacity, float floor_v,
+                                  int32_t batch, int32_t D, int32_t k, const int32_t* ids,
+                                  const int32_t* prev_token, const int32_t* root_token,
+                                  float* log_rho, hipStream_t stream);
 size_t accept_workspace_bytes(int32_t batch, int32_t n_max, int32_t vocab);
 presto_status launch_accept(bool bf16, const void* logits, int32_t vocab, int64_t row_stride,
                             int32_t batch, int32_t n_max, int32_t depth, const int32_t* parent,
@@ -107,6 +115,60 @@ presto_status presto_entropy_lambda(int64_t rows, const float* entropy, float be
     if (rows == 0) return PRESTO_OK;
     REQUIRE(entropy && lambda, "presto_entropy_lambda: null pointer");
     return launch_entropy_lambda(rows, entropy, beta, c, lambda, stream);
+}
+
+static bool ngram_capacity_ok(int64_t capacity) {
+    return capacity >= 64 && capacity <= ((int64_t)1 << 32) && (capacity & (capacity - 1)) == 0;
+}
+
+size_t presto_ngram_table_bytes(int64_t capacity) {
+    if (!ngram_capacity_ok(capacity)) return 0;
+    return (size_t)capacity * (sizeof(uint64_t) + sizeof(uint32_t));
+}
+
+presto_status presto_ngram_clear(void* table, int64_t capacity, hipStream_t stream) {
+    g_err[0] = 0;
+    REQUIRE(ngram_capacity_ok(capacity),
+            "presto_ngram_clear: capacity %lld is not a power of two in 64 .. 2^32",
+            (long long)capacity);
+    REQUIRE(table, "presto_ngram_clear: null table");
+    REQUIRE((uintptr_t)table % 8 == 0, "presto_ngram_clear: table not 8-byte aligned");
+    return launch_ngram_clear(table, capacity, stream);
+}
+
+presto_status presto_ngram_insert(void* table, int64_t capacity, int64_t n, const int32_t* t2,
+                                  const int32_t* t1, const int32_t* t, const float* log_rho,
+                                  int32_t* flags, hipStream_t stream) {
+    g_err[0] = 0;
+    REQUIRE(ngram_capacity_ok(capacity),
+            "presto_ngram_insert: capacity %lld is not a power of two in 64 .. 2^32",
+            (long long)capacity);
+    REQUIRE(n >= 0 && n <= ((int64_t)1 << 32), "presto_ngram_insert: n outside 0 .. 2^32");
+    if (n == 0) return PRESTO_OK;
+    REQUIRE(table && t2 && t1 && t && log_rho, "presto_ngram_insert: null pointer");
+    REQUIRE((uintptr_t)table % 8 == 0, "presto_ngram_insert: table not 8-byte aligned");
+    return launch_ngram_insert(table, capacity, n, t2, t1, t, log_rho, flags, stream);
+}
+
+presto_status presto_ngram_gather(const void* table, int64_t capacity, float floor_log_rho,
+                                  int32_t batch, int32_t depth, int32_t k, const int32_t* ids,
+                                  const int32_t* prev_token, const int32_t* root_token,
+                                  float* log_rho, hipStream_t stream) {
+    g_err[0] = 0;
+    REQUIRE(ngram_capacity_ok(capacity),
+            "presto_ngram_gather: capacity %lld is not a power of two in 64 .. 2^32",
+            (long long)capacity);
+    REQUIRE(isfinite(floor_log_rho) && floor_log_rho <= 0.f,
+            "presto_ngram_gather: floor must be finite and <= 0");
+    REQUIRE(batch >= 0, "presto_ngram_gather: batch < 0");
+    REQUIRE(depth >= 1 && depth <= 32, "presto_ngram_gather: depth=%d outside 1..32", depth);
+    REQUIRE(k >= 1 && k <= 16, "presto_ngram_gather: k=%d outside 1..16", k);
+    if (batch == 0) return PRESTO_OK;
+    REQUIRE(table && ids && prev_token && root_token && log_rho,
+            "presto_ngram_gather: null pointer");
+    REQUIRE((uintptr_t)table % 8 == 0, "presto_ngram_gather: table not 8-byte aligned");
+    return launch_ngram_gather(table, capacity, floor_log_rho, batch, depth, k, ids, prev_token,
+                               root_token, log_rho, stream);
 }
 
 size_t presto_build_tree_workspace(const presto_tree_desc* desc) {

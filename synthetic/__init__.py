@@ -30,6 +30,11 @@ even on the bit pattern when the workload is bf16):
   floor ``ln(1e-4)``, otherwise ``ln(u)`` with ``u ~ U(1e-3, 1)``.
 * Q, K, V ~ N(0, 1), independent per layer; the KV cache is packed
   varlen ``[sum ctx, Hkv, d]`` with ``ctx_offsets[b+1]``.
+* Trigram table entries (the n-gram rho of Sec. 5.1, whose training corpus
+  is not available): the trigrams of random walks that start from the
+  two committed tokens (the token before the root, the root) and pick one
+  of the k candidate tokens at each drafter position, plus uniformly random
+  background trigrams; each distinct trigram gets ln(u), u ~ U(1e-3, 1).
 """
 from __future__ import annotations
 
@@ -41,7 +46,7 @@ from dataclasses import dataclass, field as dc_field
 import numpy as np
 
 # Stream identifiers: one per tensor kind.
-S_FIELD, S_PEAKS, S_TNOISE, S_RHO, S_Q, S_K, S_V, S_KT, S_VT, S_CTX, S_TOKENS = range(1, 12)
+S_FIELD, S_PEAKS, S_TNOISE, S_RHO, S_Q, S_K, S_V, S_KT, S_VT, S_CTX, S_TOKENS, S_NGRAM = range(1, 13)
 
 # Positions of the KV cache drawn from one generator call.
 _KV_CHUNK = 1024
@@ -203,6 +208,36 @@ def lambdas(w: Workload) -> np.ndarray:
 def root_tokens(w: Workload) -> np.ndarray:
     return np.array([int(_rng(w, s, 0, S_TOKENS).integers(0, w.vocab)) for s in range(w.batch)],
                     np.int32)
+
+
+def prev_tokens(w: Workload) -> np.ndarray:
+    """The committed token before the root, per sequence."""
+    return np.array([int(_rng(w, s, 0, S_TOKENS, 2).integers(0, w.vocab)) for s in range(w.batch)],
+                    np.int32)
+
+
+def trigram_entries(w: Workload, ids: np.ndarray, n_walks: int, n_background: int) -> tuple:
+    """Trigram table entries (t2, t1, t, log rho) as four arrays: the
+    trigrams along n_walks random walks per sequence through its candidate
+    rows ids [b, D, k] after (prev token, root token), and n_background
+    random trigrams over the vocabulary."""
+    rng = np.random.default_rng([w.seed, 7, S_NGRAM])
+    prev, root = prev_tokens(w), root_tokens(w)
+    B, D, k = ids.shape
+    walks = []
+    for b in range(B):
+        pick = rng.integers(0, k, (n_walks, D))
+        toks = np.take_along_axis(np.broadcast_to(ids[b], (n_walks, D, k)), pick[:, :, None],
+                                  axis=2)[:, :, 0]
+        seq = np.concatenate([np.full((n_walks, 1), prev[b]), np.full((n_walks, 1), root[b]), toks],
+                             axis=1)
+        walks.append(np.stack([seq[:, :-2], seq[:, 1:-1], seq[:, 2:]], axis=2).reshape(-1, 3))
+    bg = rng.integers(0, w.vocab, (n_background, 3))
+    tri = np.unique(np.concatenate(walks + [bg]).astype(np.int64), axis=0)
+    tri = tri[rng.permutation(len(tri))]
+    logp = np.log(rng.uniform(1e-3, 1.0, len(tri))).astype(np.float32)
+    return (tri[:, 0].astype(np.int32), tri[:, 1].astype(np.int32), tri[:, 2].astype(np.int32),
+            logp)
 
 
 def ctx_lengths(w: Workload) -> np.ndarray:

@@ -41,6 +41,33 @@ def round_data(cfg: int, **over) -> tuple:
 
 
 @functools.lru_cache(maxsize=2)
+def oracle_candidates(cfg: int) -> tuple:
+    """The oracle's top-k of a workload's drafter logits, [b, D, k] each.
+    Stages after top-k are fed these on both sides, so no oracle input ever
+    comes from the GPU."""
+    import oracle
+
+    w, rin = round_data(cfg)
+    ids, lp, _, _ = oracle.topk(rin["drafter_logits"], w.k, w.dtype)
+    return ids.reshape(w.batch, w.depth, w.k), lp.reshape(w.batch, w.depth, w.k)
+
+
+@functools.lru_cache(maxsize=2)
+def oracle_tree(cfg: int) -> dict:
+    """The oracle's tree of a workload (from oracle_candidates)."""
+    import oracle
+
+    w, rin = round_data(cfg)
+    ids, lp = oracle_candidates(cfg)
+    return oracle.build_tree(ids, lp, rin["rho"], rin["lam"], rin["root_token"], w.depth, w.k,
+                             w.budget)
+
+
+def tree_to_dev(tree: dict) -> dict:
+    return {k: to_dev(v) for k, v in tree.items()}
+
+
+@functools.lru_cache(maxsize=2)
 def attn_data(cfg: int, layer: int = 0) -> tuple:
     w = sy.workload(cfg)
     return w, sy.attention_inputs(w, layer)

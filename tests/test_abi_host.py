@@ -131,3 +131,26 @@ def test_accept_rejects_bad_arguments():
     assert lib.presto_accept(0, None, 1024, 1024, 1, 9, 0, *args, 0, None) == P.PRESTO_ERR_INVALID_ARG
     assert lib.presto_accept(0, None, 1024, 1024, 1, 9, 4, *args, 0, None) == P.PRESTO_ERR_INVALID_ARG
     assert lib.presto_accept(0, None, 1024, 1024, 0, 9, 4, *args, 0, None) == P.PRESTO_OK
+
+
+def test_ngram_entry_points_validate_on_the_host():
+    lib = P.lib()
+    fake = ctypes.c_void_p(0x1000)  # never dereferenced: the checks fail first
+    assert lib.presto_ngram_table_bytes(1024) == 1024 * 12
+    for bad_cap in (0, 32, 100, 3 << 20):
+        assert lib.presto_ngram_table_bytes(bad_cap) == 0
+        st, msg = _err(lib.presto_ngram_clear(fake, bad_cap, None))
+        assert st == P.PRESTO_ERR_INVALID_ARG and "capacity" in msg
+    st, _ = _err(lib.presto_ngram_clear(None, 1024, None))
+    assert st == P.PRESTO_ERR_INVALID_ARG
+    st, _ = _err(lib.presto_ngram_insert(fake, 1024, -1, fake, fake, fake, fake, None, None))
+    assert st == P.PRESTO_ERR_INVALID_ARG
+    assert lib.presto_ngram_insert(None, 1024, 0, None, None, None, None, None, None) == P.PRESTO_OK
+    g = lib.presto_ngram_gather
+    for floor, depth, k in [(0.5, 4, 4), (float("nan"), 4, 4), (-1.0, 0, 4), (-1.0, 33, 4),
+                            (-1.0, 4, 0), (-1.0, 4, 17)]:
+        st, _ = _err(g(fake, 1024, floor, 1, depth, k, fake, fake, fake, fake, None))
+        assert st == P.PRESTO_ERR_INVALID_ARG, (floor, depth, k)
+    st, _ = _err(g(ctypes.c_void_p(0x1004), 1024, -1.0, 1, 4, 4, fake, fake, fake, fake, None))
+    assert st == P.PRESTO_ERR_INVALID_ARG  # misaligned table
+    assert g(None, 1024, -1.0, 0, 4, 4, None, None, None, None, None) == P.PRESTO_OK

@@ -1,5 +1,6 @@
 """GPU parity of presto_accept: per-node target argmax, accepted length,
-path and bonus token equal the oracle's exactly."""
+path and bonus token equal the oracle's exactly (both sides take the
+oracle's tree of the workload, or random trees)."""
 import json
 import os
 
@@ -10,7 +11,7 @@ import torch
 import oracle
 import paper_2607_22634_amd as P
 import synthetic as sy
-from gpu_util import round_data, to_dev, to_host, tree_to_host
+from gpu_util import oracle_tree, round_data, to_dev, to_host, tree_to_dev, tree_to_host
 
 pytestmark = pytest.mark.gpu
 GOLD = os.path.join(os.path.dirname(__file__), "golden")
@@ -32,12 +33,9 @@ def _check(w, T_store, th, tree_dev):
 def test_accept_matches_oracle_on_workload(cfg):
     w, rin = round_data(cfg)
     print(f"accept cfg={cfg}", flush=True)
-    ids, lp, _ = P.presto_topk(to_dev(rin["drafter_logits"], w.dtype), w.k)
-    t = P.presto_build_tree(ids, lp, to_dev(rin["rho"]), to_dev(rin["lam"]),
-                            to_dev(rin["root_token"]), w.depth, w.k, w.budget)
-    th = tree_to_host(t)
+    th = oracle_tree(cfg)
     T = sy.target_logits(w, rin["field"], th["parent"], th["rank"], th["n_nodes"])
-    o = _check(w, T, th, t)
+    o = _check(w, T, th, tree_to_dev(th))
     print("accept_len", o["accept_len"].tolist(), flush=True)
 
 

@@ -14,17 +14,15 @@ import oracle
 import paper_2607_22634_amd as P
 import synthetic as sy
 from brute import anc_from_parent
-from gpu_util import attn_data, round_data, to_dev, to_host, tree_to_host
+from gpu_util import attn_data, oracle_tree, round_data, to_dev, to_host, tree_to_dev, tree_to_host
 
 pytestmark = pytest.mark.gpu
 
 
 def _tree_for(cfg):
-    w, rin = round_data(cfg)
-    ids, lp, _ = P.presto_topk(to_dev(rin["drafter_logits"], w.dtype), w.k)
-    t = P.presto_build_tree(ids, lp, to_dev(rin["rho"]), to_dev(rin["lam"]),
-                            to_dev(rin["root_token"]), w.depth, w.k, w.budget)
-    return w, t
+    """The oracle's tree of the workload, on the device (both sides use it)."""
+    w, _ = round_data(cfg)
+    return w, tree_to_dev(oracle_tree(cfg))
 
 
 def _run(w, att, tree_dev):

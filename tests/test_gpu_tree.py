@@ -1,6 +1,7 @@
-"""GPU parity of presto_build_tree: fed the same candidate tables, the GPU
-tree equals the oracle's bit for bit (topology, tokens, depths, ranks,
-fp32 scores, ancestor masks, node counts)."""
+"""GPU parity of presto_build_tree: fed the same candidate tables (the
+oracle's top-k of the workload, or random tables), the GPU tree equals the
+oracle's bit for bit (topology, tokens, depths, ranks, fp32 scores, ancestor
+masks, node counts)."""
 import numpy as np
 import pytest
 import torch
@@ -8,7 +9,7 @@ import torch
 import oracle
 import paper_2607_22634_amd as P
 import synthetic as sy
-from gpu_util import round_data, to_dev, to_host, tree_to_host
+from gpu_util import oracle_candidates, round_data, to_dev, to_host, tree_to_host
 
 pytestmark = pytest.mark.gpu
 
@@ -41,9 +42,7 @@ def test_tree_matches_oracle_on_workload(cfg, lam):
     over = {} if lam is None else {"lam": lam}
     w, rin = round_data(cfg, **over)
     print(f"tree cfg={cfg} batch={w.batch} B={w.budget} k={w.k}", flush=True)
-    ids, lp, _ = P.presto_topk(to_dev(rin["drafter_logits"], w.dtype), w.k)
-    ids = to_host(ids).reshape(w.batch, w.depth, w.k)
-    lp = to_host(lp).reshape(w.batch, w.depth, w.k)
+    ids, lp = oracle_candidates(cfg)
     g, o = _gpu_and_oracle(ids, lp, rin["rho"], rin["lam"], rin["root_token"], w.depth, w.k,
                            w.budget)
     _assert_same(g, o)
@@ -93,9 +92,7 @@ def test_tree_is_deterministic():
 def test_beam_tree_matches_oracle_on_workload(cfg, W):
     w, rin = round_data(cfg)
     print(f"beam cfg={cfg} W={W}", flush=True)
-    ids, lp, _ = P.presto_topk(to_dev(rin["drafter_logits"], w.dtype), w.k)
-    ids = to_host(ids).reshape(w.batch, w.depth, w.k)
-    lp = to_host(lp).reshape(w.batch, w.depth, w.k)
+    ids, lp = oracle_candidates(cfg)
     g, o = _gpu_and_oracle(ids, lp, rin["rho"], rin["lam"], rin["root_token"], w.depth, w.k,
                            w.budget, beam_width=W)
     _assert_same(g, o)
@@ -122,9 +119,7 @@ def test_tree_with_entropy_adaptive_lambda(cfg, beam_width):
     same fp32 [batch, depth] table."""
     w, rin = round_data(cfg)
     print(f"tree entropy-lambda cfg={cfg} W={beam_width}", flush=True)
-    ids, lp, _ = P.presto_topk(to_dev(rin["drafter_logits"], w.dtype), w.k)
-    ids = to_host(ids).reshape(w.batch, w.depth, w.k)
-    lp = to_host(lp).reshape(w.batch, w.depth, w.k)
+    ids, lp = oracle_candidates(cfg)
     h = oracle.entropy(rin["drafter_logits"], w.dtype)
     lam = oracle.entropy_lambda(h, 0.6, 2.0).astype(np.float32).reshape(w.batch, w.depth)
     assert np.ptp(lam) > 0  # the weights really vary
