@@ -288,6 +288,55 @@ def measure_next_rows(P, sy, w, R, reps, timed, topk_out, topk_ws, tree_out, rin
                                              w.k, w.budget, mode=P.PRESTO_TREE_BEAM,
                                              beam_width=10, out=beam_out), n, 0) * 1e3
     out["build_tree_beam10"] = {"us": round(us, 2)}
+
+    # bookkeeping after accept: commit the accepted path into a slotted cache
+    L0 = R[0]["layers"][0]
+    ctx_h = rin["ctx"].astype(np.int64)
+    room = 32 * (w.depth + 1)
+    starts = np.concatenate([[0], np.cumsum(ctx_h + room)[:-1]])
+    rows_total = int((ctx_h + room).sum())
+    kc = torch.zeros((rows_total,) + tuple(L0["k_cache"].shape[1:]), dtype=L0["k_cache"].dtype,
+                     device=dev)
+    vc = torch.zeros_like(kc)
+    ctx0 = torch.from_numpy(np.stack([starts, ctx_h], 1).astype(np.int32)).to(dev)
+    ctx_t = ctx0.clone()
+    cap = torch.from_numpy((ctx_h + room).astype(np.int32)).to(dev)
+    acc = P.presto_accept(R[0]["target"], tree_out["parent"], tree_out["token"], tree_out["n_nodes"],
+                          w.depth)
+    flags = torch.zeros(1, dtype=torch.int32, device=dev)
+    us = timed(lambda r: P.presto_commit_kv(L0["k_tree"], L0["v_tree"], acc["path"],
+                                            acc["accept_len"], kc, vc, ctx_t, cap, flags=flags),
+               n, 0) * 1e3
+    assert int(flags.item()) == 0, "commit flagged a sequence"
+    m = int(acc["accept_len"].sum().item()) + w.batch
+    row_b = w.hkv * w.head_dim * e
+    out["commit_kv"] = {"us": round(us, 2), "rows": m, "GB/s": round(4 * m * row_b / (us * 1e3), 1)}
+
+    # quadratic self-speculation: slot selection + in-place top-k, flattening
+    S = max(1, min(1024 // w.n_max - 1, w.depth, (2 << 30) // (w.batch * w.n_max * w.vocab * e)))
+    slot_rows = w.batch * w.n_max * S
+    slot_logits = torch.empty(slot_rows, w.vocab, dtype=R[0]["drafter"].dtype, device=dev)
+    slot_logits.copy_(R[0]["drafter"][torch.arange(slot_rows, device=dev) % rows])
+    sel = P.presto_select_slots(acc["path"], acc["accept_len"], w.n_max, S, 1)
+    nrows = sel.numel()
+    sws = torch.zeros(max(1, P.lib().presto_topk_workspace(nrows, w.vocab, w.k)), dtype=torch.uint8,
+                      device=dev)
+    sel_out = (torch.empty(nrows, w.k, dtype=torch.int32, device=dev),
+               torch.empty(nrows, w.k, dtype=torch.float32, device=dev),
+               torch.empty(nrows, dtype=torch.float32, device=dev))
+
+    def select_topk(r):
+        P.presto_select_slots(acc["path"], acc["accept_len"], w.n_max, S, 1, out=sel)
+        P.presto_topk_rows(slot_logits, sel.view(-1), w.k, ids=sel_out[0], logprob=sel_out[1],
+                           lse=sel_out[2], workspace=sws)
+
+    us = timed(select_topk, n, 0) * 1e3
+    out["select_slots_topk"] = {"us": round(us, 2), "slots": S, "rows": nrows,
+                                "GB/s": round(nrows * w.vocab * e / (us * 1e3), 1)}
+    root_pos = torch.from_numpy(rin["ctx"].astype(np.int32)).to(dev)
+    us = timed(lambda r: P.presto_flatten_slots(tree_out["depth"], tree_out["anc"],
+                                                tree_out["n_nodes"], root_pos, S), n, 0) * 1e3
+    out["flatten_slots"] = {"us": round(us, 2), "rows": w.n_max * (1 + S)}
     return out
 
 

@@ -68,7 +68,10 @@ enum {
     PRESTO_FLAG_NAN_DRAFTER = 1, /* a drafter logit row held a NaN (or +inf)   */
     PRESTO_FLAG_NAN_TARGET = 2,  /* a live target logit row held a NaN         */
     PRESTO_FLAG_NGRAM_BAD = 4,   /* an n-gram entry was invalid and skipped    */
-    PRESTO_FLAG_NGRAM_FULL = 8   /* an n-gram entry found no free table slot   */
+    PRESTO_FLAG_NGRAM_FULL = 8,  /* an n-gram entry found no free table slot   */
+    PRESTO_FLAG_BAD_INDEX = 16,  /* presto_topk_rows: a row index outside the logits */
+    PRESTO_FLAG_KV_COMMIT = 32   /* round bookkeeping: a sequence's slot, length or
+                                    path was invalid; that sequence was skipped */
 };
 
 /* ------------------------------------------------------------------------ */
@@ -99,6 +102,19 @@ presto_status presto_topk(presto_dtype dt, const void *logits, int64_t rows, int
                           int64_t row_stride, int32_t k, int32_t *ids, float *logprob, float *lse,
                           float *entropy, int32_t *flags, void *ws, size_t ws_bytes,
                           hipStream_t stream);
+
+/* The same on gathered rows: output row r reads logits row row_index[r]
+ * (int64 device, [rows]) of logits [logits_rows, row_stride].  An index
+ * outside [0, logits_rows) reads as a row of only -inf and raises
+ * PRESTO_FLAG_BAD_INDEX.  Used with presto_select_slots to read the next
+ * round's drafter rows in place from a slot-logit matrix.  Same limits and
+ * workspace as presto_topk (presto_topk_workspace(rows, vocab, k)).
+ */
+presto_status presto_topk_rows(presto_dtype dt, const void *logits, int64_t logits_rows,
+                               const int64_t *row_index, int64_t rows, int32_t vocab,
+                               int64_t row_stride, int32_t k, int32_t *ids, float *logprob,
+                               float *lse, float *entropy, int32_t *flags, void *ws,
+                               size_t ws_bytes, hipStream_t stream);
 
 /* Entropy-adaptive prefix weight (Appendix F):
  *   lambda[r] = beta * H[r] / (H[r] + C), fp32, H from presto_topk's
@@ -229,10 +245,15 @@ presto_status presto_build_tree(const presto_tree_desc *desc, const int32_t *ids
  * Rows n >= n_nodes[b] are written as zeros.
  *
  * q        [batch, n_max, hq, head_dim]
- * k_cache, v_cache [sum_b ctx_b, hkv, head_dim], packed: sequence b owns
- *          positions ctx_offsets[b] .. ctx_offsets[b+1]-1
- * ctx_offsets [batch + 1] int32 device, non-decreasing, ctx_offsets[0] = 0,
- *          every ctx_b <= max_ctx (ctx_b = 0 is allowed)
+ * k_cache, v_cache [cache_rows, hkv, head_dim]
+ * ctx_offsets, by desc->ctx_layout:
+ *   PRESTO_CTX_PACKED: [batch + 1] int32 device, non-decreasing,
+ *          ctx_offsets[0] = 0; sequence b owns cache rows
+ *          ctx_offsets[b] .. ctx_offsets[b+1]-1 (ctx_b = their count)
+ *   PRESTO_CTX_SLOTS: [batch, 2] int32 device (start_b, ctx_b); sequence b
+ *          owns rows start_b .. start_b + ctx_b - 1, with room after them
+ *          for presto_commit_kv to append to
+ *   every ctx_b <= max_ctx (ctx_b = 0 is allowed)
  * k_tree, v_tree [batch, n_max, hkv, head_dim]: K/V of the tree nodes
  * anc      [batch, n_max, ceil(n_max/64)] from presto_build_tree
  * n_nodes  [batch] int32 device, 1 .. n_max
@@ -241,10 +262,13 @@ presto_status presto_build_tree(const presto_tree_desc *desc, const int32_t *ids
  * fp32 softmax; fp32 inputs use fp32 throughout.
  * Limits: head_dim in {64, 128}; hq % hkv == 0; n_max <= 1024.
  */
+typedef enum { PRESTO_CTX_PACKED = 0, PRESTO_CTX_SLOTS = 1 } presto_ctx_layout;
+
 typedef struct {
     int32_t batch, n_max, hq, hkv, head_dim, max_ctx;
     float scale; /* usually 1/sqrt(head_dim) */
     presto_dtype dt;
+    int32_t ctx_layout; /* presto_ctx_layout */
 } presto_attn_desc;
 
 size_t presto_tree_attention_workspace(const presto_attn_desc *desc);
@@ -283,6 +307,75 @@ presto_status presto_accept(presto_dtype dt, const void *target_logits, int32_t 
                             int32_t *accept_len, int32_t *path, int32_t *bonus,
                             int32_t *target_argmax, int32_t *flags, void *ws, size_t ws_bytes,
                             hipStream_t stream);
+
+/* ------------------------------------------------------------------------ */
+/* Bookkeeping between rounds.
+ *
+ * presto_commit_kv (Appendix C stage I: the accepted tokens join the
+ * committed prefix for the next round): for every sequence b, the tree K/V
+ * rows of path[b, 0 .. accept_len[b]] (the root, then the accepted draft
+ * nodes, as written by presto_accept) are appended in that order to the
+ * cache after its ctx_b rows, and ctx_b grows by accept_len[b] + 1.
+ *   k_tree, v_tree [batch, n_max, hkv, head_dim] (dtype dt), as given to
+ *                  presto_tree_attention
+ *   path, accept_len from presto_accept ([batch, depth + 1], [batch])
+ *   k_cache, v_cache [cache_rows, hkv, head_dim] in PRESTO_CTX_SLOTS layout
+ *   ctx [batch, 2] int32 device (start_b, ctx_b), updated in place
+ *   ctx_cap [batch] int32 device: sequence b owns rows start_b ..
+ *                  start_b + ctx_cap[b] - 1
+ * A sequence whose slot lies outside the cache, would overflow its
+ * capacity, or whose path is invalid is left unchanged and raises
+ * PRESTO_FLAG_KV_COMMIT.  16-byte aligned tensors.  The tree rows of the
+ * next round's root (the bonus token) are the caller's: its K/V come from
+ * the next verification forward.
+ */
+typedef struct {
+    int32_t batch, n_max, hkv, head_dim, depth;
+    presto_dtype dt;
+} presto_commit_desc;
+
+presto_status presto_commit_kv(const presto_commit_desc *desc, const void *k_tree,
+                               const void *v_tree, const int32_t *path, const int32_t *accept_len,
+                               void *k_cache, void *v_cache, int64_t cache_rows, int32_t *ctx,
+                               const int32_t *ctx_cap, int32_t *flags, hipStream_t stream);
+
+/* Quadratic self-speculation (Appendix E).  The verification forward also
+ * denoises `slots` mask positions after every tree node; slot j (1-based)
+ * of node n stands for the position j places after n.  Their logits form
+ * the matrix [batch, n_max, slots, V] (row (b, n, j - 1)).
+ *
+ * presto_select_slots (Appendix E (II)): only the block of the last accepted
+ * node a = path[b, accept_len[b]] feeds the next round.  Writes row_index
+ * [batch, slots - first_slot] int64: next drafter row d of sequence b reads
+ * slot first_slot + d + 1 of a, i.e. matrix row
+ * (b * n_max + a) * slots + first_slot + d.  With first_slot = 1 the first
+ * slot, whose position the bonus token (the next root) fills, is skipped.
+ * An invalid path raises PRESTO_FLAG_KV_COMMIT and reads the root's block.
+ * Limits: 0 <= first_slot < slots <= 64.
+ *
+ * presto_flatten_slots (Appendix E (IV)): the next forward's input puts a
+ * block of `slots` mask slots after every tree node: composite row
+ * r = n * (1 + slots) + j is node n (j = 0) or its slot j.  Writes
+ *   pos_out [batch, R] int32, R = n_max * (1 + slots): root_pos[b] +
+ *          depth(n) + j for live rows, -1 for rows of nodes n >= n_nodes
+ *   anc_out [batch, R, ceil(R / 64)] uint64: a node row sees the node rows of
+ *          its root path (itself included); a slot row sees the same node
+ *          rows and every slot of its own block; dead rows see nothing
+ *   n_rows  [batch] int32: n_nodes[b] * (1 + slots), the live prefix
+ * from depth, anc [batch, n_max, ceil(n_max / 64)], n_nodes of
+ * presto_build_tree and root_pos [batch] (the position of the root).  The
+ * result is a valid presto_tree_attention mask when R <= 1024.
+ * Limits: 1 <= slots <= 64, R <= 65536.
+ */
+presto_status presto_select_slots(int32_t batch, int32_t n_max, int32_t depth, int32_t slots,
+                                  int32_t first_slot, const int32_t *path,
+                                  const int32_t *accept_len, int64_t *row_index, int32_t *flags,
+                                  hipStream_t stream);
+presto_status presto_flatten_slots(int32_t batch, int32_t n_max, int32_t slots,
+                                   const int32_t *depth, const uint64_t *anc,
+                                   const int32_t *n_nodes, const int32_t *root_pos,
+                                   int32_t *pos_out, uint64_t *anc_out, int32_t *n_rows,
+                                   hipStream_t stream);
 
 /* ------------------------------------------------------------------------ */
 const char *presto_status_string(presto_status s);

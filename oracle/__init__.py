@@ -232,3 +232,84 @@ def accept(dtype, target_logits, parent, token, n_nodes, depth: int) -> dict:
                  _p(out["target_argmax"]))
     out["nan_rows"] = int(nan_rows)
     return out
+
+
+# ----------------------------------------------------------------------------
+# Bookkeeping between rounds (Appendix C stage I; Appendix E)
+
+def commit_kv(k_tree, v_tree, path, accept_len, k_cache, v_cache, ctx, ctx_cap):
+    """The root and the accepted draft tokens join the committed prefix
+    (Appendix C stage I): for each sequence, the tree K/V rows of its path
+    (root first, as the accept stage lists it) are appended after its cache
+    rows, and its length grows by their count.  ctx [b, 2] = (start, len),
+    ctx_cap [b] = rows the sequence owns.  A sequence that would overflow
+    its rows, lies outside the cache, or has an invalid path is left as it
+    is.  Returns (k_cache, v_cache, ctx, skipped) as new arrays."""
+    kc, vc, cx = k_cache.copy(), v_cache.copy(), np.array(ctx, np.int32, copy=True)
+    B, N = k_tree.shape[:2]
+    depth = path.shape[1] - 1
+    skipped = np.zeros(B, bool)
+    for b in range(B):
+        start, length, cap = int(cx[b, 0]), int(cx[b, 1]), int(ctx_cap[b])
+        al = int(accept_len[b])
+        nodes = [int(x) for x in path[b, :al + 1]] if 0 <= al <= depth else []
+        ok = (0 <= al <= depth and start >= 0 and length >= 0 and cap >= 0
+              and start + cap <= kc.shape[0] and length + al + 1 <= cap
+              and nodes[0] == 0 and all(0 <= x < N for x in nodes))
+        if not ok:
+            skipped[b] = True
+            continue
+        for i, node in enumerate(nodes):
+            kc[start + length + i] = k_tree[b, node]
+            vc[start + length + i] = v_tree[b, node]
+        cx[b, 1] = length + len(nodes)
+    return kc, vc, cx, skipped
+
+
+def select_slots(path, accept_len, n_max: int, slots: int, first_slot: int = 1) -> np.ndarray:
+    """Rows of the next round's drafter positions in the slot-logit matrix
+    [b * n_max * slots, V] (Appendix E (II)): only the mask slots after the
+    last accepted node are used, from slot first_slot + 1 (1-based) on."""
+    B = len(accept_len)
+    out = np.empty((B, slots - first_slot), np.int64)
+    for b in range(B):
+        last = int(path[b, int(accept_len[b])])
+        for d in range(slots - first_slot):
+            out[b, d] = (b * n_max + last) * slots + first_slot + d
+    return out
+
+
+def flatten_slots(parent, depth, n_nodes, root_pos, slots: int) -> dict:
+    """Composite input of the next forward (Appendix E (IV)): every tree node
+    is followed by a block of `slots` mask slots; row n * (1 + slots) + j is
+    node n (j = 0) or its slot j.  A node row attends to the node rows on its
+    root path (itself included), a slot row to those same node rows and to
+    its whole block; positions are root_pos + depth(n) + j.  Built from
+    parent pointers."""
+    B, N = parent.shape
+    blk = 1 + slots
+    R = N * blk
+    WO = (R + 63) // 64
+    pos = np.full((B, R), -1, np.int32)
+    anc = np.zeros((B, R, WO), np.uint64)
+    n_rows = np.zeros(B, np.int32)
+
+    def setbit(b, r, c):
+        anc[b, r, c // 64] |= np.uint64(1) << np.uint64(c % 64)
+
+    for b in range(B):
+        nn = int(n_nodes[b])
+        n_rows[b] = nn * blk
+        for n in range(nn):
+            chain = [n]
+            while chain[-1] != 0:
+                chain.append(int(parent[b, chain[-1]]))
+            for j in range(blk):
+                r = n * blk + j
+                pos[b, r] = int(root_pos[b]) + int(depth[b, n]) + j
+                for m in chain:
+                    setbit(b, r, m * blk)
+                if j > 0:
+                    for jj in range(1, blk):
+                        setbit(b, r, n * blk + jj)
+    return {"pos": pos, "anc": anc, "n_rows": n_rows}

@@ -34,13 +34,18 @@ PRESTO_FLAG_NAN_DRAFTER = 1
 PRESTO_FLAG_NAN_TARGET = 2
 PRESTO_FLAG_NGRAM_BAD = 4
 PRESTO_FLAG_NGRAM_FULL = 8
+PRESTO_FLAG_BAD_INDEX = 16
+PRESTO_FLAG_KV_COMMIT = 32
+PRESTO_CTX_PACKED = 0
+PRESTO_CTX_SLOTS = 1
 
 EXPORTS = (
     "presto_topk_workspace", "presto_topk", "presto_entropy_lambda", "presto_ngram_table_bytes",
     "presto_ngram_clear", "presto_ngram_insert", "presto_ngram_gather", "presto_build_tree_workspace",
     "presto_build_tree",
     "presto_tree_attention_workspace", "presto_tree_attention", "presto_accept_workspace",
-    "presto_accept", "presto_status_string", "presto_last_error", "presto_version",
+    "presto_accept", "presto_topk_rows", "presto_commit_kv", "presto_select_slots",
+    "presto_flatten_slots", "presto_status_string", "presto_last_error", "presto_version",
 )
 
 
@@ -59,7 +64,12 @@ class TreeDesc(ctypes.Structure):
 class AttnDesc(ctypes.Structure):
     _fields_ = [("batch", ctypes.c_int32), ("n_max", ctypes.c_int32), ("hq", ctypes.c_int32),
                 ("hkv", ctypes.c_int32), ("head_dim", ctypes.c_int32), ("max_ctx", ctypes.c_int32),
-                ("scale", ctypes.c_float), ("dt", ctypes.c_int32)]
+                ("scale", ctypes.c_float), ("dt", ctypes.c_int32), ("ctx_layout", ctypes.c_int32)]
+
+
+class CommitDesc(ctypes.Structure):
+    _fields_ = [("batch", ctypes.c_int32), ("n_max", ctypes.c_int32), ("hkv", ctypes.c_int32),
+                ("head_dim", ctypes.c_int32), ("depth", ctypes.c_int32), ("dt", ctypes.c_int32)]
 
 
 _VP, _I32, _I64, _SZ = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
@@ -100,6 +110,16 @@ def lib() -> ctypes.CDLL:
         L.presto_accept_workspace.restype = _SZ
         L.presto_accept.argtypes = [_I32, _VP, _I32, _I64, _I32, _I32, _I32] + [_VP] * 9 + [_SZ, _VP]
         L.presto_accept.restype = _I32
+        L.presto_topk_rows.argtypes = [_I32, _VP, _I64, _VP, _I64, _I32, _I64, _I32] + [_VP] * 6 \
+            + [_SZ, _VP]
+        L.presto_topk_rows.restype = _I32
+        L.presto_commit_kv.argtypes = [ctypes.POINTER(CommitDesc)] + [_VP] * 6 + [_I64] + \
+            [_VP] * 4
+        L.presto_commit_kv.restype = _I32
+        L.presto_select_slots.argtypes = [_I32, _I32, _I32, _I32, _I32] + [_VP] * 5
+        L.presto_select_slots.restype = _I32
+        L.presto_flatten_slots.argtypes = [_I32, _I32, _I32] + [_VP] * 8
+        L.presto_flatten_slots.restype = _I32
         L.presto_status_string.argtypes = [_I32]
         L.presto_status_string.restype = ctypes.c_char_p
         L.presto_last_error.restype = ctypes.c_char_p
@@ -271,15 +291,18 @@ def presto_build_tree(ids: torch.Tensor, logprob: torch.Tensor, log_rho, lam: to
 def presto_tree_attention(q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.Tensor,
                           ctx_offsets: torch.Tensor, k_tree: torch.Tensor, v_tree: torch.Tensor,
                           anc: torch.Tensor, n_nodes: torch.Tensor, max_ctx: int,
-                          scale: float | None = None, *, out=None, workspace=None, stream=None):
-    """Tree-masked attention of q [b, N, Hq, d] over [cache ; ancestors]."""
+                          scale: float | None = None, *, out=None, workspace=None, stream=None,
+                          ctx_layout: int = PRESTO_CTX_PACKED):
+    """Tree-masked attention of q [b, N, Hq, d] over [cache ; ancestors].
+    ctx_offsets: [b + 1] packed offsets, or [b, 2] (start, len) pairs with
+    ctx_layout=PRESTO_CTX_SLOTS."""
     b, N, hq, d = q.shape
     hkv = k_tree.shape[2]
     scale = d ** -0.5 if scale is None else scale
     _dev(q, k_cache, v_cache, ctx_offsets, k_tree, v_tree, anc, n_nodes)
     out = torch.empty_like(q) if out is None else out
     _dev(out)
-    desc = AttnDesc(b, N, hq, hkv, d, int(max_ctx), float(scale), _dt(q))
+    desc = AttnDesc(b, N, hq, hkv, d, int(max_ctx), float(scale), _dt(q), int(ctx_layout))
     need = lib().presto_tree_attention_workspace(ctypes.byref(desc))
     ws, nb = _workspace(need, q.device, workspace)
     _check(lib().presto_tree_attention(
@@ -309,4 +332,80 @@ def presto_accept(target_logits: torch.Tensor, parent: torch.Tensor, token: torc
         _ptr(parent), _ptr(token), _ptr(n_nodes), _ptr(out["accept_len"]), _ptr(out["path"]),
         _ptr(out["bonus"]), _ptr(out.get("target_argmax")), _ptr(flags), _ptr(ws), nb,
         _stream(stream)), "presto_accept")
+    return out
+
+
+def presto_topk_rows(logits: torch.Tensor, row_index: torch.Tensor, k: int, *, ids=None,
+                     logprob=None, lse=None, entropy=None, flags=None, workspace=None, stream=None):
+    """presto_topk on the rows logits[row_index] (int64 device indices), read in place."""
+    _rows(logits)
+    _dev(row_index)
+    if row_index.dtype != torch.int64:
+        raise TypeError("row_index must be int64")
+    rows = row_index.numel()
+    L, V = logits.shape
+    dev = logits.device
+    ids = torch.empty(rows, k, dtype=torch.int32, device=dev) if ids is None else ids
+    logprob = torch.empty(rows, k, dtype=torch.float32, device=dev) if logprob is None else logprob
+    lse = torch.empty(rows, dtype=torch.float32, device=dev) if lse is None else lse
+    want_h = entropy is not None and entropy is not False
+    if entropy is True:
+        entropy = torch.empty(rows, dtype=torch.float32, device=dev)
+    h = entropy if want_h else None
+    _dev(ids, logprob, lse, h, flags)
+    need = lib().presto_topk_workspace(rows, V, k)
+    ws, nb = _workspace(need, dev, workspace)
+    _check(lib().presto_topk_rows(_dt(logits), _ptr(logits), L, _ptr(row_index), rows, V,
+                                  logits.stride(0), k, _ptr(ids), _ptr(logprob), _ptr(lse), _ptr(h),
+                                  _ptr(flags), _ptr(ws), nb, _stream(stream)),
+           "presto_topk_rows")
+    return (ids, logprob, lse, h) if want_h else (ids, logprob, lse)
+
+
+def presto_commit_kv(k_tree: torch.Tensor, v_tree: torch.Tensor, path: torch.Tensor,
+                     accept_len: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.Tensor,
+                     ctx: torch.Tensor, ctx_cap: torch.Tensor, *, flags=None, stream=None) -> None:
+    """Append each sequence's root and accepted tree K/V rows to its cache
+    slot; ctx [b, 2] (start, len) is advanced in place."""
+    b, N, hkv, d = k_tree.shape
+    depth = path.shape[1] - 1
+    _dev(k_tree, v_tree, path, accept_len, k_cache, v_cache, ctx, ctx_cap, flags)
+    desc = CommitDesc(b, N, hkv, d, depth, _dt(k_tree))
+    _check(lib().presto_commit_kv(ctypes.byref(desc), _ptr(k_tree), _ptr(v_tree), _ptr(path),
+                                  _ptr(accept_len), _ptr(k_cache), _ptr(v_cache),
+                                  k_cache.shape[0], _ptr(ctx), _ptr(ctx_cap), _ptr(flags),
+                                  _stream(stream)),
+           "presto_commit_kv")
+
+
+def presto_select_slots(path: torch.Tensor, accept_len: torch.Tensor, n_max: int, slots: int,
+                        first_slot: int = 1, *, out=None, flags=None, stream=None) -> torch.Tensor:
+    """Row indices [b, slots - first_slot] of the next drafter rows in the
+    slot-logit matrix [b * n_max * slots, V]."""
+    b = accept_len.shape[0]
+    depth = path.shape[1] - 1
+    out = torch.empty(b, slots - first_slot, dtype=torch.int64, device=path.device) \
+        if out is None else out
+    _dev(path, accept_len, out, flags)
+    _check(lib().presto_select_slots(b, n_max, depth, slots, first_slot, _ptr(path),
+                                     _ptr(accept_len), _ptr(out), _ptr(flags), _stream(stream)),
+           "presto_select_slots")
+    return out
+
+
+def presto_flatten_slots(depth: torch.Tensor, anc: torch.Tensor, n_nodes: torch.Tensor,
+                         root_pos: torch.Tensor, slots: int, *, stream=None) -> dict:
+    """Composite layout of a tree with `slots` mask slots after every node:
+    pos [b, R], anc [b, R, ceil(R/64)], n_rows [b] with R = N * (1 + slots)."""
+    b, N = depth.shape
+    R = N * (1 + slots)
+    dev = depth.device
+    out = {"pos": torch.empty(b, R, dtype=torch.int32, device=dev),
+           "anc": torch.empty(b, R, (R + 63) // 64, dtype=torch.int64, device=dev),
+           "n_rows": torch.empty(b, dtype=torch.int32, device=dev)}
+    _dev(depth, anc, n_nodes, root_pos)
+    _check(lib().presto_flatten_slots(b, N, slots, _ptr(depth), _ptr(anc), _ptr(n_nodes),
+                                      _ptr(root_pos), _ptr(out["pos"]), _ptr(out["anc"]),
+                                      _ptr(out["n_rows"]), _stream(stream)),
+           "presto_flatten_slots")
     return out

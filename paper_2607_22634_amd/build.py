@@ -11,7 +11,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libpresto.so")
-SOURCES = ["api.hip", "topk.hip", "ngram.hip", "tree_build.hip", "tree_attn.hip", "accept.hip"]
+SOURCES = ["api.hip", "topk.hip", "ngram.hip", "round.hip", "tree_build.hip", "tree_attn.hip", "accept.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [

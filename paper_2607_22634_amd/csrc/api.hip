@@ -13,9 +13,23 @@ namespace presto_host {
 size_t topk_workspace_bytes(int64_t rows, int32_t vocab, int32_t k);
 presto_status launch_entropy_lambda(int64_t rows, const float* entropy, float beta, float c,
                                     float* lambda, hipStream_t stream);
-presto_status launch_topk(bool bf16, const void* logits, int64_t rows, int32_t vocab,
-                          int64_t row_stride, int32_t k, int32_t* ids, float* logprob, float* lse,
-                          float* entropy, int32_t* flags, void* ws, hipStream_t stream);
+presto_status launch_topk(bool bf16, const void* logits, const int64_t* row_index,
+                          int64_t logits_rows, int64_t rows, int32_t vocab, int64_t row_stride,
+                          int32_t k, int32_t* ids, float* logprob, float* lse, float* entropy,
+                          int32_t* flags, void* ws, hipStream_t stream);
+presto_status launch_commit_kv(const presto_commit_desc* d, const void* k_tree, const void* v_tree,
+                               const int32_t* path, const int32_t* accept_len, void* k_cache,
+                               void* v_cache, int64_t cache_rows, int32_t* ctx,
+                               const int32_t* ctx_cap, int32_t* flags, hipStream_t stream);
+presto_status launch_select_slots(int32_t batch, int32_t n_max, int32_t depth, int32_t slots,
+                                  int32_t first_slot, const int32_t* path,
+                                  const int32_t* accept_len, int64_t* row_index, int32_t* flags,
+                                  hipStream_t stream);
+presto_status launch_flatten_slots(int32_t batch, int32_t n_max, int32_t slots,
+                                   const int32_t* depth, const uint64_t* anc,
+                                   const int32_t* n_nodes, const int32_t* root_pos,
+                                   int32_t* pos_out, uint64_t* anc_out, int32_t* n_rows,
+                                   hipStream_t stream);
 bool tree_build_fits(int D, int k, int branch, int N, int beam_width);
 int tree_max_depth(int k);
 presto_status launch_build_tree(const presto_tree_desc* desc, const int32_t* ids,
@@ -102,8 +116,31 @@ presto_status presto_topk(presto_dtype dt, const void* logits, int64_t rows, int
             "presto_topk: too many rows");
     presto_status st = check_ws(ws, ws_bytes, presto_topk_workspace(rows, vocab, k));
     if (st != PRESTO_OK) return st;
-    return launch_topk(dt == PRESTO_DT_BF16, logits, rows, vocab, row_stride, k, ids, logprob, lse,
-                       entropy, flags, ws, stream);
+    return launch_topk(dt == PRESTO_DT_BF16, logits, nullptr, rows, rows, vocab, row_stride, k, ids,
+                       logprob, lse, entropy, flags, ws, stream);
+}
+
+presto_status presto_topk_rows(presto_dtype dt, const void* logits, int64_t logits_rows,
+                               const int64_t* row_index, int64_t rows, int32_t vocab,
+                               int64_t row_stride, int32_t k, int32_t* ids, float* logprob,
+                               float* lse, float* entropy, int32_t* flags, void* ws,
+                               size_t ws_bytes, hipStream_t stream) {
+    g_err[0] = 0;
+    REQUIRE(valid_dtype(dt), "presto_topk_rows: unknown dtype %d", (int)dt);
+    REQUIRE(rows >= 0 && logits_rows >= 0, "presto_topk_rows: negative row count");
+    REQUIRE(vocab >= 1, "presto_topk_rows: vocab < 1");
+    REQUIRE(k >= 1 && k <= vocab, "presto_topk_rows: k=%d outside 1..vocab", k);
+    REQUIRE(row_stride >= vocab, "presto_topk_rows: row_stride < vocab");
+    if (k > 16) return set_error(PRESTO_ERR_UNSUPPORTED, "presto_topk_rows: k=%d > 16", k);
+    if (rows == 0) return PRESTO_OK;
+    REQUIRE(logits && row_index && ids && logprob, "presto_topk_rows: null pointer");
+    REQUIRE(logits_rows >= 1, "presto_topk_rows: no logits rows");
+    REQUIRE(rows * (int64_t)((vocab + 1023) / 1024) < (int64_t)1 << 31,
+            "presto_topk_rows: too many rows");
+    presto_status st = check_ws(ws, ws_bytes, presto_topk_workspace(rows, vocab, k));
+    if (st != PRESTO_OK) return st;
+    return launch_topk(dt == PRESTO_DT_BF16, logits, row_index, logits_rows, rows, vocab,
+                       row_stride, k, ids, logprob, lse, entropy, flags, ws, stream);
 }
 
 presto_status presto_entropy_lambda(int64_t rows, const float* entropy, float beta, float c,
@@ -241,6 +278,8 @@ presto_status presto_tree_attention(const presto_attn_desc* desc, const void* q,
     REQUIRE(d.head_dim == 64 || d.head_dim == 128, "presto_tree_attention: head_dim %d",
             d.head_dim);
     REQUIRE(d.max_ctx >= 0, "presto_tree_attention: max_ctx < 0");
+    REQUIRE(d.ctx_layout == PRESTO_CTX_PACKED || d.ctx_layout == PRESTO_CTX_SLOTS,
+            "presto_tree_attention: unknown ctx_layout %d", d.ctx_layout);
     REQUIRE(isfinite(d.scale) && d.scale > 0.f, "presto_tree_attention: scale must be positive");
     REQUIRE((int64_t)d.max_ctx + d.n_max < ((int64_t)1 << 30), "presto_tree_attention: too long");
     if (d.batch == 0) return PRESTO_OK;
@@ -287,6 +326,64 @@ presto_status presto_accept(presto_dtype dt, const void* target_logits, int32_t 
     return launch_accept(dt == PRESTO_DT_BF16, target_logits, vocab, row_stride, batch, n_max, depth,
                          parent, token, n_nodes, accept_len, path, bonus, target_argmax, flags, ws,
                          stream);
+}
+
+presto_status presto_commit_kv(const presto_commit_desc* desc, const void* k_tree,
+                               const void* v_tree, const int32_t* path, const int32_t* accept_len,
+                               void* k_cache, void* v_cache, int64_t cache_rows, int32_t* ctx,
+                               const int32_t* ctx_cap, int32_t* flags, hipStream_t stream) {
+    g_err[0] = 0;
+    REQUIRE(desc, "presto_commit_kv: null descriptor");
+    const presto_commit_desc d = *desc;
+    REQUIRE(valid_dtype(d.dt), "presto_commit_kv: unknown dtype %d", (int)d.dt);
+    REQUIRE(d.batch >= 0, "presto_commit_kv: batch < 0");
+    REQUIRE(d.n_max >= 1 && d.n_max <= 1024, "presto_commit_kv: n_max outside 1..1024");
+    REQUIRE(d.depth >= 1 && d.depth <= 1024, "presto_commit_kv: depth outside 1..1024");
+    REQUIRE(d.hkv >= 1 && (d.head_dim == 64 || d.head_dim == 128),
+            "presto_commit_kv: hkv >= 1 and head_dim in {64, 128}");
+    REQUIRE(cache_rows >= 0, "presto_commit_kv: cache_rows < 0");
+    if (d.batch == 0) return PRESTO_OK;
+    REQUIRE(k_tree && v_tree && path && accept_len && k_cache && v_cache && ctx && ctx_cap,
+            "presto_commit_kv: null pointer");
+    const uintptr_t al = (uintptr_t)k_tree | (uintptr_t)v_tree | (uintptr_t)k_cache |
+                         (uintptr_t)v_cache;
+    REQUIRE(al % 16 == 0, "presto_commit_kv: K/V tensors must be 16-byte aligned");
+    return launch_commit_kv(&d, k_tree, v_tree, path, accept_len, k_cache, v_cache, cache_rows,
+                            ctx, ctx_cap, flags, stream);
+}
+
+presto_status presto_select_slots(int32_t batch, int32_t n_max, int32_t depth, int32_t slots,
+                                  int32_t first_slot, const int32_t* path,
+                                  const int32_t* accept_len, int64_t* row_index, int32_t* flags,
+                                  hipStream_t stream) {
+    g_err[0] = 0;
+    REQUIRE(batch >= 0, "presto_select_slots: batch < 0");
+    REQUIRE(n_max >= 1 && n_max <= 1024, "presto_select_slots: n_max outside 1..1024");
+    REQUIRE(depth >= 1, "presto_select_slots: depth < 1");
+    REQUIRE(slots >= 1 && slots <= 64, "presto_select_slots: slots outside 1..64");
+    REQUIRE(first_slot >= 0 && first_slot < slots,
+            "presto_select_slots: first_slot outside 0..slots-1");
+    if (batch == 0) return PRESTO_OK;
+    REQUIRE(path && accept_len && row_index, "presto_select_slots: null pointer");
+    return launch_select_slots(batch, n_max, depth, slots, first_slot, path, accept_len, row_index,
+                               flags, stream);
+}
+
+presto_status presto_flatten_slots(int32_t batch, int32_t n_max, int32_t slots,
+                                   const int32_t* depth, const uint64_t* anc,
+                                   const int32_t* n_nodes, const int32_t* root_pos,
+                                   int32_t* pos_out, uint64_t* anc_out, int32_t* n_rows,
+                                   hipStream_t stream) {
+    g_err[0] = 0;
+    REQUIRE(batch >= 0, "presto_flatten_slots: batch < 0");
+    REQUIRE(n_max >= 1 && n_max <= 1024, "presto_flatten_slots: n_max outside 1..1024");
+    REQUIRE(slots >= 1 && slots <= 64, "presto_flatten_slots: slots outside 1..64");
+    REQUIRE((int64_t)n_max * (1 + slots) <= 65536, "presto_flatten_slots: more than 65536 rows");
+    if (batch == 0) return PRESTO_OK;
+    REQUIRE(depth && anc && n_nodes && root_pos && pos_out && anc_out && n_rows,
+            "presto_flatten_slots: null pointer");
+    return launch_flatten_slots(batch, n_max, slots, depth, anc, n_nodes, root_pos, pos_out,
+                                anc_out, n_rows, stream);
 }
 
 const char* presto_status_string(presto_status s) {

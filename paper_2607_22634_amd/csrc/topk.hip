@@ -108,8 +108,9 @@ __device__ __forceinline__ uint32_t wave_kth_largest_u32(uint32_t x, int k) {
 template <bool BF16, int NLOAD, bool ENT>
 __global__ __launch_bounds__(kTopkWavesPerBlock * kWave) void topk_partial_kernel(
     const void* __restrict__ logits, int64_t rows, int32_t vocab, int64_t row_stride, int32_t k,
-    int32_t chunks, bool aligned, float2* __restrict__ part_ms, uint64_t* __restrict__ part_keys,
-    float* __restrict__ part_h, int32_t* __restrict__ flags) {
+    int32_t chunks, bool aligned, const int64_t* __restrict__ row_index, int64_t logits_rows,
+    float2* __restrict__ part_ms, uint64_t* __restrict__ part_keys, float* __restrict__ part_h,
+    int32_t* __restrict__ flags) {
     constexpr int P = VecTraits<BF16>::kPerVec;  // elements per 16-byte load (a "group")
     constexpr int E = NLOAD * P;
     constexpr int64_t CH = (int64_t)kWave * E;
@@ -123,7 +124,18 @@ __global__ __launch_bounds__(kTopkWavesPerBlock * kWave) void topk_partial_kerne
     const int64_t row = gw / chunks;
     const int32_t chunk = (int32_t)(gw % chunks);
     const int64_t c0 = (int64_t)chunk * CH;
-    const char* rowp = static_cast<const char*>(logits) + row * row_stride * (BF16 ? 2 : 4);
+    // with a row index, output row `row` reads logits row row_index[row]; an
+    // index outside the logits reads as an empty row (and is flagged)
+    int64_t src = row;
+    if (row_index) {
+        src = row_index[row];
+        if (src < 0 || src >= logits_rows) {
+            if (chunk == 0 && lane_id() == 0) raise_flag(flags, PRESTO_FLAG_BAD_INDEX);
+            src = 0;
+            vocab = 0;
+        }
+    }
+    const char* rowp = static_cast<const char*>(logits) + src * row_stride * (BF16 ? 2 : 4);
     const bool full = aligned && (c0 + CH <= vocab);
 
     float v[E];
@@ -342,9 +354,10 @@ size_t topk_workspace_bytes(int64_t rows, int32_t vocab, int32_t k) {
     return (size_t)rows * per + 512;
 }
 
-presto_status launch_topk(bool bf16, const void* logits, int64_t rows, int32_t vocab,
-                          int64_t row_stride, int32_t k, int32_t* ids, float* logprob, float* lse,
-                          float* entropy, int32_t* flags, void* ws, hipStream_t stream) {
+presto_status launch_topk(bool bf16, const void* logits, const int64_t* row_index,
+                          int64_t logits_rows, int64_t rows, int32_t vocab, int64_t row_stride,
+                          int32_t k, int32_t* ids, float* logprob, float* lse, float* entropy,
+                          int32_t* flags, void* ws, hipStream_t stream) {
     const int nload = topk_nload(bf16, rows, vocab);
     const int64_t ch = (int64_t)kWave * nload * (bf16 ? 8 : 4);
     const int64_t chunks = (vocab + ch - 1) / ch;
@@ -361,8 +374,9 @@ presto_status launch_topk(bool bf16, const void* logits, int64_t rows, int32_t v
     const dim3 grid((unsigned)((waves + kTopkWavesPerBlock - 1) / kTopkWavesPerBlock));
 #define PRESTO_TOPK(BF, NL, EN)                                                              \
     topk_partial_kernel<BF, NL, EN><<<grid, block, 0, stream>>>(logits, rows, vocab, row_stride, \
-                                                               k, (int32_t)chunks, aligned, ms,  \
-                                                               keys, hs, flags)
+                                                               k, (int32_t)chunks, aligned,      \
+                                                               row_index, logits_rows, ms, keys, \
+                                                               hs, flags)
 #define PRESTO_TOPK2(BF, NL) \
     if (ent) PRESTO_TOPK(BF, NL, true); else PRESTO_TOPK(BF, NL, false)
     if (bf16) {

@@ -62,6 +62,7 @@ struct AttnArgs {
     const uint16_t* kc;
     const uint16_t* vc;
     const int32_t* ctx_off;
+    int32_t ctx_slots;  // 0: ctx_off is [batch + 1] offsets; 1: (start, len) pairs
     const uint16_t* kt;
     const uint16_t* vt;
     const uint64_t* anc;
@@ -73,6 +74,16 @@ struct AttnArgs {
     int32_t n_tasks, n_blocks;
     float scale_log2;  // scale * log2(e)
 };
+
+// Cache rows of sequence b: start c0 and length ctx, from packed offsets
+// [batch + 1] or from (start, len) pairs [batch, 2].
+struct CtxSpan {
+    int c0, ctx;
+};
+__device__ __forceinline__ CtxSpan ctx_span(const int32_t* off, int b, int slots) {
+    if (slots) return {off[2 * b], off[2 * b + 1]};
+    return {off[b], off[b + 1] - off[b]};
+}
 
 __device__ __forceinline__ int clamp_nodes(int nn, int n_max) {
     return nn < 1 ? 1 : (nn > n_max ? n_max : nn);
@@ -143,8 +154,8 @@ __global__ __launch_bounds__(NW * kWave) void tree_attn_bf16_kernel(AttnArgs a) 
     const int g = (task / a.row_tiles / a.splits) % a.hkv;
     const int b = task / a.row_tiles / a.splits / a.hkv;
 
-    const int c0 = a.ctx_off[b];
-    const int ctx = a.ctx_off[b + 1] - c0;
+    const CtxSpan cs = ctx_span(a.ctx_off, b, a.ctx_slots);
+    const int c0 = cs.c0, ctx = cs.ctx;
     const int nn = clamp_nodes(a.n_nodes[b], a.n_max);
     const int keys = ctx + nn;
     const int k_begin = split * a.split_len;
@@ -463,7 +474,7 @@ __global__ __launch_bounds__(256) void tree_attn_merge_kernel(AttnArgs a) {
 #pragma unroll
     for (int e = 0; e < PER; ++e) acc[e] = 0.f;
     if (rho < a.G * nn) {
-        const int keys = a.ctx_off[b + 1] - a.ctx_off[b] + nn;
+        const int keys = ctx_span(a.ctx_off, b, a.ctx_slots).ctx + nn;
         const int nsplit = min(a.splits, (keys + a.split_len - 1) / a.split_len);
         const float* pp = a.part + (((int64_t)b * a.hkv + g) * a.rows_pad + rho) * a.splits * (D + 2);
         float ms = -INFINITY, ls = 0.f;
@@ -506,7 +517,7 @@ __global__ __launch_bounds__(256) void tree_attn_merge_kernel(AttnArgs a) {
 template <int D>
 __global__ __launch_bounds__(kWave) void tree_attn_f32_kernel(
     const float* __restrict__ q, const float* __restrict__ kc, const float* __restrict__ vc,
-    const int32_t* __restrict__ ctx_off, const float* __restrict__ kt,
+    const int32_t* __restrict__ ctx_off, int32_t ctx_slots, const float* __restrict__ kt,
     const float* __restrict__ vt, const uint64_t* __restrict__ anc,
     const int32_t* __restrict__ n_nodes, float* __restrict__ out, int32_t n_max, int32_t hq,
     int32_t hkv, float scale) {
@@ -523,7 +534,8 @@ __global__ __launch_bounds__(kWave) void tree_attn_f32_kernel(
         for (int e = lane; e < D; e += kWave) op[e] = 0.f;
         return;
     }
-    const int c0 = ctx_off[b], ctx = ctx_off[b + 1] - c0;
+    const CtxSpan cs = ctx_span(ctx_off, b, ctx_slots);
+    const int c0 = cs.c0, ctx = cs.ctx;
     const float* qp = q + (((int64_t)b * n_max + n) * hq + h) * D;
     const uint64_t* arow = anc + ((int64_t)b * n_max + n) * W;
     float qv[D];
@@ -640,6 +652,7 @@ presto_status launch_tree_attention(const presto_attn_desc* d, const void* q, co
 #define PRESTO_F32(DD)                                                                           \
     tree_attn_f32_kernel<DD><<<grid, kWave, 0, stream>>>(                                        \
         (const float*)q, (const float*)k_cache, (const float*)v_cache, ctx_offsets,              \
+        d->ctx_layout == PRESTO_CTX_SLOTS,                                                       \
         (const float*)k_tree, (const float*)v_tree, anc, n_nodes, (float*)out, d->n_max, d->hq, \
         d->hkv, d->scale)
         if (d->head_dim == 64) PRESTO_F32(64); else PRESTO_F32(128);
@@ -652,6 +665,7 @@ presto_status launch_tree_attention(const presto_attn_desc* d, const void* q, co
     a.kc = (const uint16_t*)k_cache;
     a.vc = (const uint16_t*)v_cache;
     a.ctx_off = ctx_offsets;
+    a.ctx_slots = d->ctx_layout == PRESTO_CTX_SLOTS;
     a.kt = (const uint16_t*)k_tree;
     a.vt = (const uint16_t*)v_tree;
     a.anc = anc;
