@@ -98,33 +98,38 @@ __global__ __launch_bounds__(kArgmaxWavesPerBlock * kWave) void argmax_partial_k
 // path is the chain of nodes whose whole root path is good.  Pointer jumping
 // (ceil(log2(depth + 1)) rounds) gives every node that property and its
 // depth at once; the accepted nodes then write themselves into the path.
+// Every global load (node count, parents, tokens, chunk keys) is issued
+// before the first one is used: the kernel waits for memory once.
 __global__ __launch_bounds__(kWalkThreads) void accept_walk_kernel(
     int32_t n_max, int32_t depth, int32_t chunks, const uint64_t* __restrict__ part,
     const int32_t* __restrict__ parent, const int32_t* __restrict__ token,
     const int32_t* __restrict__ n_nodes, int32_t* __restrict__ accept_len,
     int32_t* __restrict__ path, int32_t* __restrict__ bonus, int32_t* __restrict__ target_argmax) {
     __shared__ int32_t s_a[kMaxNodes];
-    __shared__ int32_t s_par[kMaxNodes];
     __shared__ int32_t s_jmp[2][kMaxNodes];
     __shared__ int32_t s_dep[2][kMaxNodes];  // edges to the jump target; -1: a bad node on the way
     __shared__ int32_t s_len;
     const int b = blockIdx.x;
-    const int nn = min(max(n_nodes[b], 1), n_max);
-    const int wave = threadIdx.x / kWave, lane = lane_id();
+    const int tid = threadIdx.x;
+    const int wave = tid / kWave, lane = lane_id();
     const int nwaves = blockDim.x / kWave;
     const int64_t rb = (int64_t)b * n_max;
-    if (threadIdx.x == 0) s_len = 0;
-    for (int n = threadIdx.x; n < nn; n += blockDim.x) s_par[n] = n == 0 ? 0 : parent[rb + n];
+    // node tid's parent and token (blockDim.x >= n_max), and the node count
+    const int my_par = tid < n_max ? parent[rb + tid] : 0;
+    const int my_tok = tid < n_max ? token[rb + tid] : 0;
+    const int nn_raw = n_nodes[b];
+    if (tid == 0) s_len = 0;
     // each wave reduces the chunk keys of kNodesPerWave nodes at a time (all
-    // their loads in flight before the first reduction)
-    for (int n0 = wave * kNodesPerWave; n0 < nn; n0 += nwaves * kNodesPerWave) {
+    // their loads in flight before the first reduction); rows of padding
+    // nodes are reduced too (never written in this call; ignored below)
+    for (int n0 = wave * kNodesPerWave; n0 < n_max; n0 += nwaves * kNodesPerWave) {
         uint64_t best[kNodesPerWave];
 #pragma unroll
         for (int u = 0; u < kNodesPerWave; ++u) best[u] = 0ull;
         for (int c = lane; c < chunks; c += kWave) {
 #pragma unroll
             for (int u = 0; u < kNodesPerWave; ++u) {
-                if (n0 + u < nn) {
+                if (n0 + u < n_max) {
                     const uint64_t x = part[(rb + n0 + u) * chunks + c];
                     best[u] = x > best[u] ? x : best[u];
                 }
@@ -133,47 +138,48 @@ __global__ __launch_bounds__(kWalkThreads) void accept_walk_kernel(
 #pragma unroll
         for (int u = 0; u < kNodesPerWave; ++u) {
             const uint64_t m = wave_max_u64_dpp(best[u]);
-            if (lane == 0 && n0 + u < nn) s_a[n0 + u] = (int32_t)key_id(m);
+            if (lane == 0 && n0 + u < n_max) s_a[n0 + u] = (int32_t)key_id(m);
         }
     }
+    const int nn = min(max(nn_raw, 1), n_max);
     __syncthreads();
-    for (int n = threadIdx.x; n < n_max; n += blockDim.x) {
-        if (target_argmax) target_argmax[rb + n] = n < nn ? s_a[n] : -1;
-        if (n < nn) {
-            const int p = s_par[n];
-            const bool good = n == 0 || token[rb + n] == s_a[p];
-            s_jmp[0][n] = p;
-            s_dep[0][n] = good ? (n == 0 ? 0 : 1) : -1;
+    if (tid < n_max) {
+        if (target_argmax) target_argmax[rb + tid] = tid < nn ? s_a[tid] : -1;
+        if (tid < nn) {
+            // (a parent outside 0 .. nn-1 can only come from a malformed tree:
+            // clamped, so that it costs a wrong answer, never a bad access)
+            const int p = tid == 0 ? 0 : min(max(my_par, 0), nn - 1);
+            const bool good = tid == 0 || my_tok == s_a[p];
+            s_jmp[0][tid] = p;
+            s_dep[0][tid] = good ? (tid == 0 ? 0 : 1) : -1;
         }
     }
     __syncthreads();
     int cur = 0;
     for (int reach = 1; reach < depth + 1; reach *= 2) {
-        for (int n = threadIdx.x; n < nn; n += blockDim.x) {
-            const int j = s_jmp[cur][n], dn = s_dep[cur][n], dj = s_dep[cur][j];
-            s_jmp[cur ^ 1][n] = s_jmp[cur][j];
-            s_dep[cur ^ 1][n] = (dn < 0 || dj < 0) ? -1 : dn + dj;
+        if (tid < nn) {
+            const int j = s_jmp[cur][tid], dn = s_dep[cur][tid], dj = s_dep[cur][j];
+            s_jmp[cur ^ 1][tid] = s_jmp[cur][j];
+            s_dep[cur ^ 1][tid] = (dn < 0 || dj < 0) ? -1 : dn + dj;
         }
         cur ^= 1;
         __syncthreads();
     }
     // accepted nodes: a good root path no longer than `depth` moves
     int32_t* pth = path + (int64_t)b * (depth + 1);
-    for (int n = threadIdx.x; n < nn; n += blockDim.x) {
-        const int dn = s_dep[cur][n];
+    if (tid < nn) {
+        const int dn = s_dep[cur][tid];
         if (dn >= 0 && dn <= depth) {
-            pth[dn] = n;
+            pth[dn] = tid;
             atomicMax(&s_len, dn);
         }
     }
     __syncthreads();
     const int L = s_len;
-    for (int i = L + 1 + threadIdx.x; i <= depth; i += blockDim.x) pth[i] = -1;
-    for (int n = threadIdx.x; n < nn; n += blockDim.x) {
-        if (s_dep[cur][n] == L) {
-            accept_len[b] = L;
-            bonus[b] = s_a[n];
-        }
+    for (int i = L + 1 + tid; i <= depth; i += blockDim.x) pth[i] = -1;
+    if (tid < nn && s_dep[cur][tid] == L) {
+        accept_len[b] = L;
+        bonus[b] = s_a[tid];
     }
 }
 
@@ -220,8 +226,8 @@ presto_status launch_accept(bool bf16, const void* logits, int32_t vocab, int64_
 #undef PRESTO_ARGMAX
     presto_status st = check_launch("argmax_partial_kernel");
     if (st != PRESTO_OK) return st;
-    const int threads = n_max >= 64 ? kWalkThreads : 256;
-    accept_walk_kernel<<<batch, threads, 0, stream>>>(n_max, depth, (int32_t)chunks, part, parent,
+    // one thread per node (n_max <= 1024), at least 16 waves for the key reduction
+    accept_walk_kernel<<<batch, kWalkThreads, 0, stream>>>(n_max, depth, (int32_t)chunks, part, parent,
                                                       token, n_nodes, accept_len, path, bonus,
                                                       target_argmax);
     return check_launch("accept_walk_kernel");
