@@ -57,6 +57,9 @@ def main() -> int:
     ap.add_argument("--replicas", type=int, default=0, help="input copies cycled (0 = auto)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--traffic-run", action="store_true",
+                    help="only the workload's tree attention (5 calls) and a 256 MiB device copy "
+                         "(3 calls), for rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE runs")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py runs on exactly one GPU: the round is independent per sequence and this "
@@ -95,6 +98,9 @@ def main() -> int:
     th = {k: v.cpu().numpy() for k, v in tree.items()}
     target = dv(sy.target_logits(w, rin["field"], th["parent"], th["rank"], th["n_nodes"]), w.dtype)
     gen_s = time.time() - t_gen
+
+    if args.traffic_run:
+        return traffic_run(P, w, layers, tree, max_ctx, dev)
 
     work = algorithmic_work(w, ctx, th["n_nodes"], th["depth"])
     step_bytes = (work["topk_bytes"] + work["argmax_bytes"] + w.layers * work["attn_bytes_per_layer"])
@@ -208,7 +214,7 @@ def main() -> int:
         roof = {"bound": "hbm", "achieved": stages[dom]["GB/s"], "peak": HBM_PEAK_GBS, "unit": "GB/s"}
     roof["kernel"] = dom
     roof["frac"] = round(roof["achieved"] / roof["peak"], 4)
-    roof["traffic"] = None
+    roof["traffic"] = measured_traffic(dom, w)
 
     extra = measure_next_rows(P, sy, w, R, reps, timed, topk_out, topk_ws, tree_out, rin, dev)
 
@@ -231,6 +237,51 @@ def main() -> int:
         "gen_seconds": round(gen_s, 1),
     }
     print(json.dumps(line), flush=True)
+    return 0
+
+
+TRAFFIC_PROFILE = {"tree_attention": ("profiles/traffic_tree_attention_qwen3-8b-single.md",
+                                      "paper_2607_22634_amd/csrc/tree_attn.hip")}
+
+
+def measured_traffic(kernel: str, w):
+    """HBM bytes per launch of `kernel` from the committed FETCH_SIZE /
+    WRITE_SIZE summary, when that summary is for this workload and for the
+    kernel source as it is now (its sha256 is recorded there); else None."""
+    import hashlib
+
+    if kernel not in TRAFFIC_PROFILE or w.name != "qwen3-8b-single":
+        return None
+    summary, source = (os.path.join(ROOT, x) for x in TRAFFIC_PROFILE[kernel])
+    if not os.path.exists(summary):
+        return None
+    fields = {}
+    for line in open(summary):
+        if line.startswith("- ") and ":" in line:
+            key, val = line[2:].split(":", 1)
+            fields[key.strip()] = val.strip().strip("`")
+    digest = hashlib.sha256(open(source, "rb").read()).hexdigest()
+    if fields.get("source sha256") != digest or "bytes per launch" not in fields:
+        return None
+    return int(fields["bytes per launch"])
+
+
+def traffic_run(P, w, layers, tree, max_ctx, dev) -> int:
+    """A short process for counter runs: 5 tree-attention calls of the
+    workload, then 3 plain copies of 256 MiB (the calibration kernel)."""
+    import torch
+
+    L = layers[0]
+    out = torch.empty_like(L["q"])
+    for _ in range(5):
+        P.presto_tree_attention(L["q"], L["k_cache"], L["v_cache"], L["ctx_offsets"], L["k_tree"],
+                                L["v_tree"], tree["anc"], tree["n_nodes"], max_ctx, w.scale, out=out)
+    src = torch.ones(64 << 20, dtype=torch.float32, device=dev)
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print("traffic run done: 5 tree-attention calls, 3 copies of 256 MiB", flush=True)
     return 0
 
 
