@@ -57,6 +57,8 @@ def main() -> int:
     ap.add_argument("--replicas", type=int, default=0, help="input copies cycled (0 = auto)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-at-scale", action="store_true",
+                    help="skip the kernels timed at the larger workloads' shapes")
     ap.add_argument("--traffic-run", action="store_true",
                     help="only the workload's tree attention (5 calls) and a 256 MiB device copy "
                          "(3 calls), for rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE runs")
@@ -217,6 +219,7 @@ def main() -> int:
     roof["traffic"] = measured_traffic(dom, w)
 
     extra = measure_next_rows(P, sy, w, R, reps, timed, topk_out, topk_ws, tree_out, rin, dev)
+    at_scale = None if args.no_at_scale else measure_at_scale(P, sy, dev)
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -233,6 +236,7 @@ def main() -> int:
                    "global_batch": w.batch, "replicas": reps},
         "sequence_rounds_per_s": round(w.batch * 1e3 / ms_per_step, 2),
         "stages": stages, "roofline": roof, "cpu_baseline": cpu, "next_rows": extra,
+        "at_scale": at_scale,
         "accept_len": acc_out["accept_len"].cpu().tolist(),
         "gen_seconds": round(gen_s, 1),
     }
@@ -283,6 +287,102 @@ def traffic_run(P, w, layers, tree, max_ctx, dev) -> int:
     torch.cuda.synchronize()
     print("traffic run done: 5 tree-attention calls, 3 copies of 256 MiB", flush=True)
     return 0
+
+
+def measure_at_scale(P, sy, dev):
+    """The data-parallel kernels at the larger workloads' shapes, each against
+    its roofline: top-k and the accept argmax over workload 5's rows (1024
+    drafter rows, 4128 node rows), tree attention at workload 3 (16 ragged
+    contexts, HBM-bound) and workload 4 (4 x 32768 keys, MFMA-bound).  Inputs
+    are N(0, 1) device draws of those shapes (scaled like the workloads'
+    logits); trees come from the GPU stages on them.  Timing only: parity at
+    these shapes is covered by the tests."""
+    import torch
+
+    def time_us(fn, n=10):
+        fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        st = torch.cuda.current_stream()
+        e0.record(st)
+        for _ in range(n):
+            fn()
+        e1.record(st)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) * 1e3 / n
+
+    def roof(bytes_, flops, us):
+        gbs = bytes_ / (us * 1e3)
+        tfs = flops / (us * 1e6)
+        t_hbm = bytes_ / (HBM_PEAK_GBS * 1e3)
+        t_mfma = flops / (MFMA_BF16_TFLOPS * 1e6)
+        if t_mfma > t_hbm:
+            return {"us": round(us, 2), "bound": "mfma", "TFLOP/s": round(tfs, 1), "GB/s": round(gbs, 1),
+                    "frac": round(tfs / MFMA_BF16_TFLOPS, 4)}
+        return {"us": round(us, 2), "bound": "hbm", "GB/s": round(gbs, 1), "TFLOP/s": round(tfs, 1),
+                "frac": round(gbs / HBM_PEAK_GBS, 4)}
+
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(1234)
+    out = {}
+    # top-k and argmax over workload 5's rows
+    w5 = sy.workload(5)
+    rows = w5.batch * w5.depth
+    logits = (torch.randn(rows, w5.vocab, device=dev, generator=gen) * 4).to(torch.bfloat16)
+    ws = torch.zeros(P.lib().presto_topk_workspace(rows, w5.vocab, w5.k), dtype=torch.uint8, device=dev)
+    o = (torch.empty(rows, w5.k, dtype=torch.int32, device=dev),
+         torch.empty(rows, w5.k, dtype=torch.float32, device=dev),
+         torch.empty(rows, dtype=torch.float32, device=dev))
+    us = time_us(lambda: P.presto_topk(logits, w5.k, ids=o[0], logprob=o[1], lse=o[2], workspace=ws))
+    out["topk_1024_rows"] = roof(rows * w5.vocab * 2 + rows * (8 * w5.k + 4), 0, us)
+    del logits
+    lam = torch.full((w5.depth,), 0.2, dtype=torch.float32, device=dev)
+    root = torch.zeros(w5.batch, dtype=torch.int32, device=dev)
+    lp = torch.log_softmax(torch.randn(rows, 64, device=dev, generator=gen) * 4, dim=1)
+    lp, ids = torch.topk(lp, w5.k, dim=1)
+    tree = P.presto_build_tree(ids.to(torch.int32).contiguous(), lp.contiguous(), None, lam, root,
+                               w5.depth, w5.k, w5.budget)
+    target = (torch.randn(w5.batch * w5.n_max, w5.vocab, device=dev, generator=gen) * 4).to(torch.bfloat16)
+    aws = torch.zeros(P.lib().presto_accept_workspace(w5.batch, w5.n_max, w5.vocab), dtype=torch.uint8,
+                      device=dev)
+    us = time_us(lambda: P.presto_accept(target, tree["parent"], tree["token"], tree["n_nodes"], w5.depth,
+                                         workspace=aws))
+    live = int(tree["n_nodes"].sum().item())
+    out["accept_4128_rows"] = roof(live * w5.vocab * 2, 0, us)
+    del target
+    # tree attention at workloads 3 and 4
+    for cfg in (3, 4):
+        w = sy.workload(cfg)
+        ctx = sy.ctx_lengths(w).astype(np.int64)
+        offs = torch.from_numpy(np.concatenate([[0], np.cumsum(ctx)]).astype(np.int32)).to(dev)
+        total = int(ctx.sum())
+        rows = w.batch * w.depth
+        lp = torch.log_softmax(torch.randn(rows, 64, device=dev, generator=gen) * 4, dim=1)
+        lp, ids = torch.topk(lp, w.k, dim=1)
+        lamw = torch.full((w.depth,), 0.2, dtype=torch.float32, device=dev)
+        rootw = torch.zeros(w.batch, dtype=torch.int32, device=dev)
+        tr = P.presto_build_tree(ids.to(torch.int32).contiguous(), lp.contiguous(), None, lamw, rootw,
+                                 w.depth, w.k, w.budget)
+        bf = dict(device=dev, dtype=torch.bfloat16)
+        q = torch.randn(w.batch, w.n_max, w.hq, w.head_dim, device=dev, generator=gen).to(torch.bfloat16)
+        kc = torch.randn(total, w.hkv, w.head_dim, device=dev, generator=gen).to(torch.bfloat16)
+        vc = torch.randn(total, w.hkv, w.head_dim, device=dev, generator=gen).to(torch.bfloat16)
+        kt = torch.randn(w.batch, w.n_max, w.hkv, w.head_dim, device=dev, generator=gen).to(torch.bfloat16)
+        vt = torch.randn(w.batch, w.n_max, w.hkv, w.head_dim, device=dev, generator=gen).to(torch.bfloat16)
+        ao = torch.empty_like(q)
+        desc = P.AttnDesc(w.batch, w.n_max, w.hq, w.hkv, w.head_dim, int(ctx.max()), w.scale,
+                          P.PRESTO_DT_BF16)
+        import ctypes
+        nws = P.lib().presto_tree_attention_workspace(ctypes.byref(desc))
+        aw = torch.zeros(max(1, nws), dtype=torch.uint8, device=dev) if nws else None
+        us = time_us(lambda: P.presto_tree_attention(q, kc, vc, offs, kt, vt, tr["anc"], tr["n_nodes"],
+                                                     int(ctx.max()), w.scale, out=ao, workspace=aw))
+        nn = tr["n_nodes"].cpu().numpy()
+        dep = tr["depth"].cpu().numpy()
+        ww = algorithmic_work(w, ctx, nn, dep)
+        out[f"tree_attention_{w.name}"] = roof(ww["attn_bytes_per_layer"], ww["attn_flops_per_layer"], us)
+        del q, kc, vc, kt, vt, ao, aw
+    return out
 
 
 def measure_next_rows(P, sy, w, R, reps, timed, topk_out, topk_ws, tree_out, rin, dev):
