@@ -68,7 +68,10 @@ struct AttnArgs {
     const uint64_t* anc;
     const int32_t* n_nodes;
     uint16_t* out;
-    float* part;  // [batch, hkv, rows_pad, splits, D + 2] when splits > 1
+    // split partials when splits > 1, per query row (b, g, rho < G n_max) and
+    // split: the normalised output as bf16 [.., splits, D] and (m, l) fp32
+    uint16_t* part_o;
+    float2* part_ml;
     int32_t batch, n_max, hq, hkv, G, W;
     int32_t row_tiles, rows_pad, splits, split_len;
     int32_t n_tasks, n_blocks;
@@ -199,7 +202,29 @@ __global__ __launch_bounds__(NW * kWave) void tree_attn_bf16_kernel(AttnArgs a) 
     // ---- K/V staging: global -> registers -> LDS, three buffers: while tile t
     // is consumed, tile t+1 is already in LDS (the last block of a tile scores
     // the first block of the next one) and tile t+2 is in flight.
+    // A tile wholly inside the context is read at a uniform base plus a
+    // per-thread 32-bit byte offset fixed for the whole loop (no per-tile
+    // address arithmetic); other tiles take the general path.
+    const int fast_end = min(ctx, k_end);
+    uint32_t piece_off[PT];
+#pragma unroll
+    for (int i = 0; i < PT; ++i) {
+        const int p = tid + i * NT;
+        piece_off[i] = (uint32_t)(((p / (D / 8)) * a.hkv * D + (p % (D / 8)) * 8) * 2);
+    }
     auto fetch = [&](int t0) {
+        if (t0 + kKeyTile <= fast_end) {
+            const int64_t row = ((int64_t)(c0 + t0) * a.hkv + g) * D;
+            const char* kb = reinterpret_cast<const char*>(a.kc + row);
+            const char* vb = reinterpret_cast<const char*>(a.vc + row);
+            TilePieces<PT> r;
+#pragma unroll
+            for (int i = 0; i < PT; ++i) {
+                r.k[i] = *reinterpret_cast<const uint4*>(kb + piece_off[i]);
+                r.v[i] = *reinterpret_cast<const uint4*>(vb + piece_off[i]);
+            }
+            return r;
+        }
         return fetch_tile<D, PT, NT>(a.kc, a.vc, a.kt, a.vt, tid, t0, k_end, ctx, c0, a.hkv, g,
                                      (int64_t)b * a.n_max);
     };
@@ -436,27 +461,30 @@ __global__ __launch_bounds__(NW * kWave) void tree_attn_bf16_kernel(AttnArgs a) 
                                    pack_bf16x2(o[rb][db][4 * q4 + 2] * inv, o[rb][db][4 * q4 + 3] * inv));
                 }
         } else {
-            float* pp =
-                a.part + ((((int64_t)b * a.hkv + g) * a.rows_pad + rho[rb]) * a.splits + split) * (D + 2);
+            // normalised here, so bf16 holds it to the output's own precision
+            const int64_t pr = (((int64_t)b * a.hkv + g) * all_rows + rho[rb]) * a.splits + split;
+            uint16_t* po = a.part_o + pr * D;
+            const float inv = l > 0.f ? 1.f / l : 0.f;
 #pragma unroll
             for (int db = 0; db < DB; ++db)
 #pragma unroll
                 for (int q4 = 0; q4 < 4; ++q4) {
                     const int dd = db * 32 + 8 * q4 + 4 * h;
-                    *reinterpret_cast<float4*>(pp + dd) =
-                        make_float4(o[rb][db][4 * q4], o[rb][db][4 * q4 + 1], o[rb][db][4 * q4 + 2],
-                                    o[rb][db][4 * q4 + 3]);
+                    *reinterpret_cast<uint2*>(po + dd) =
+                        make_uint2(pack_bf16x2(o[rb][db][4 * q4] * inv, o[rb][db][4 * q4 + 1] * inv),
+                                   pack_bf16x2(o[rb][db][4 * q4 + 2] * inv, o[rb][db][4 * q4 + 3] * inv));
                 }
-            if (h == 0) {
-                pp[D] = m_run[rb];
-                pp[D + 1] = l;
-            }
+            if (h == 0) a.part_ml[pr] = make_float2(m_run[rb], l);
         }
     }
 }
 
-// Merge of the split partials: one wave per query row; lanes first read the
-// splits' (max, sum), then each lane combines its D/64 output dimensions.
+// Merge of the split partials: one wave per query row.  Lane s reads the
+// (m, l) pair of split s (at most 64 splits) and forms its weight
+// l exp2(m - M); the splits' normalised outputs are then read in groups of
+// kMergeUnroll with every load of a group issued before the first is used,
+// so a row costs two memory round trips rather than one per split.
+constexpr int kMergeUnroll = 8;
 template <int D>
 __global__ __launch_bounds__(256) void tree_attn_merge_kernel(AttnArgs a) {
     constexpr int PER = D / kWave;  // output dims per lane
@@ -476,27 +504,34 @@ __global__ __launch_bounds__(256) void tree_attn_merge_kernel(AttnArgs a) {
     if (rho < a.G * nn) {
         const int keys = ctx_span(a.ctx_off, b, a.ctx_slots).ctx + nn;
         const int nsplit = min(a.splits, (keys + a.split_len - 1) / a.split_len);
-        const float* pp = a.part + (((int64_t)b * a.hkv + g) * a.rows_pad + rho) * a.splits * (D + 2);
-        float ms = -INFINITY, ls = 0.f;
-        for (int s = lane; s < nsplit; s += kWave) {
-            ms = fmaxf(ms, pp[s * (D + 2) + D]);
-        }
-        const float M = wave_max_f32_dpp(ms);
-        float wl = 0.f;  // this lane's split weight (lane s holds split s, s < 64)
-        for (int s = lane; s < nsplit; s += kWave) {
-            const float m = pp[s * (D + 2) + D];
-            const float w = m == -INFINITY ? 0.f : exp2f(m - M);
-            ls += w * pp[s * (D + 2) + D + 1];
-            if (s < kWave) wl = w;
-        }
-        const float L = wave_sum_f32_dpp(ls);
-        for (int s = 0; s < nsplit; ++s) {
-            const float* ps = pp + s * (D + 2);
-            const float m = ps[D];
-            const float w = s < kWave ? __int_as_float(__builtin_amdgcn_readlane(__float_as_int(wl), s))
-                                      : (m == -INFINITY ? 0.f : exp2f(m - M));
+        const int64_t pr = (((int64_t)b * a.hkv + g) * a.G * a.n_max + rho) * a.splits;
+        const uint16_t* po = a.part_o + pr * D + lane * PER;
+        float2 ml = make_float2(-INFINITY, 0.f);
+        if (lane < nsplit) ml = a.part_ml[pr + lane];
+        const float M = wave_max_f32_dpp(ml.x);
+        const float wl = ml.x == -INFINITY ? 0.f : exp2f(ml.x - M) * ml.y;  // weight of split `lane`
+        const float L = wave_sum_f32_dpp(wl);
+        for (int s0 = 0; s0 < nsplit; s0 += kMergeUnroll) {
+            float v[kMergeUnroll][PER];
 #pragma unroll
-            for (int e = 0; e < PER; ++e) acc[e] += w * ps[lane * PER + e];
+            for (int u = 0; u < kMergeUnroll; ++u) {
+                const int s = min(s0 + u, nsplit - 1);
+                if constexpr (PER == 1) {
+                    v[u][0] = bf16_to_f(po[(int64_t)s * D]);
+                } else {
+                    const uint32_t w2 = *reinterpret_cast<const uint32_t*>(po + (int64_t)s * D);
+                    v[u][0] = bf16_to_f((uint16_t)(w2 & 0xffffu));
+                    v[u][1] = bf16_to_f((uint16_t)(w2 >> 16));
+                }
+            }
+#pragma unroll
+            for (int u = 0; u < kMergeUnroll; ++u) {
+                if (s0 + u < nsplit) {
+                    const float w = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(wl), s0 + u));
+#pragma unroll
+                    for (int e = 0; e < PER; ++e) acc[e] += w * v[u][e];
+                }
+            }
         }
         const float inv = L > 0.f ? 1.f / L : 0.f;
 #pragma unroll
@@ -609,20 +644,21 @@ static AttnPlan attn_plan(const presto_attn_desc* d) {
     // context splits: one workgroup per CU, so the time in key-block units
     // (about 0.85 us each) is (rounds of workgroups) x (key blocks per split
     // + about 3 for a workgroup's prologue) plus the merge, whose partials
-    // (written and read back, about 4 MB per key-block time) grow with the
-    // split count
+    // (2 D + 8 bytes per query row and split, written and read back, about
+    // 4 MB per key-block time) grow with the split count
     const int64_t base = (int64_t)d->batch * d->hkv * p.row_tiles;
     const int keys = d->max_ctx + d->n_max;
     const int max_splits = (keys + 127) / 128;
     double best_cost = 1e30;
     p.splits = 1;
     p.split_len = (keys + kKeyTile - 1) / kKeyTile * kKeyTile;
-    for (int s = 1; s <= 64 && s <= max_splits; ++s) {
+    for (int s = 1; s <= kWave && s <= max_splits; ++s) {  // the merge gives each split a lane
         int len = (keys + s - 1) / s;
         len = (len + kKeyTile - 1) / kKeyTile * kKeyTile;
         const int se = (keys + len - 1) / len;
         const double rounds = (double)((base * se + 255) / 256);
-        const double merge_bytes = se > 1 ? 2.0 * base * p.rows_per_tile * se * (d->head_dim + 2) * 4.0 : 0.0;
+        const double merge_bytes =
+            se > 1 ? 2.0 * d->batch * d->hkv * p.rows * se * (2.0 * d->head_dim + 8.0) : 0.0;
         const double cost = rounds * ((len + 31) / 32 + 3) + merge_bytes / 4.0e6;
         if (cost < best_cost - 1e-9) {
             best_cost = cost;
@@ -639,7 +675,8 @@ size_t attn_workspace_bytes(const presto_attn_desc* d) {
     if (d->dt != PRESTO_DT_BF16) return 0;
     const AttnPlan p = attn_plan(d);
     if (p.splits <= 1) return 0;
-    return (size_t)d->batch * d->hkv * p.rows_pad * p.splits * (d->head_dim + 2) * sizeof(float) + 256;
+    const size_t prs = (size_t)d->batch * d->hkv * p.G * d->n_max * p.splits;
+    return ((prs * d->head_dim * sizeof(uint16_t) + 255) & ~(size_t)255) + prs * sizeof(float2) + 256;
 }
 
 presto_status launch_tree_attention(const presto_attn_desc* d, const void* q, const void* k_cache,
@@ -671,7 +708,11 @@ presto_status launch_tree_attention(const presto_attn_desc* d, const void* q, co
     a.anc = anc;
     a.n_nodes = n_nodes;
     a.out = (uint16_t*)out;
-    a.part = (float*)ws;
+    {
+        const size_t prs = (size_t)d->batch * d->hkv * p.G * d->n_max * p.splits;
+        a.part_o = (uint16_t*)ws;
+        a.part_ml = (float2*)((char*)ws + ((prs * d->head_dim * sizeof(uint16_t) + 255) & ~(size_t)255));
+    }
     a.batch = d->batch;
     a.n_max = d->n_max;
     a.hq = d->hq;
