@@ -167,7 +167,7 @@ def _workspace(nbytes: int, device, ws):
         return None, 0
     if ws is not None:
         return ws, ws.numel() * ws.element_size()
-    t = torch.zeros(nbytes, dtype=torch.uint8, device=device)  # workspaces start zeroed
+    t = torch.empty(nbytes, dtype=torch.uint8, device=device)  # contents on entry are ignored
     return t, nbytes
 
 
