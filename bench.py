@@ -4,7 +4,8 @@
 One step = one whole round on one batch of synthetic inputs already resident
 in HBM: presto_topk -> presto_build_tree -> presto_tree_attention (every
 layer of the workload) -> presto_accept, enqueued on one stream with no host
-synchronisation inside.  Inputs are replicated in device memory and the steps
+synchronisation inside (--launch graph replays each round from a HIP graph
+captured once per input replica instead).  Inputs are replicated in device memory and the steps
 cycle through the replicas, so that every step reads data that has been
 pushed out of the 256 MB last-level cache by the steps in between (the
 numbers are DRAM numbers, not cache numbers).
@@ -59,6 +60,9 @@ def main() -> int:
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-at-scale", action="store_true",
                     help="skip the kernels timed at the larger workloads' shapes")
+    ap.add_argument("--launch", choices=["stream", "graph"], default="stream",
+                    help="timed rounds: every kernel launched on the stream (default), or one "
+                         "captured HIP graph per input replica, replayed (measured slower)")
     ap.add_argument("--traffic-run", action="store_true",
                     help="only the workload's tree attention (5 calls) and a 256 MiB device copy "
                          "(3 calls), for rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE runs")
@@ -180,8 +184,37 @@ def main() -> int:
     for i in range(args.warmup):
         step(i % reps)
     torch.cuda.synchronize()
-    # the timed region: K whole rounds back to back
-    ms_per_step = timed(step, args.steps, args.warmup)
+    # K whole rounds back to back, every kernel launched on the stream
+    ms_stream = timed(step, args.steps, args.warmup)
+    ms_per_step = ms_stream
+    if args.launch == "graph":
+        # The same rounds as HIP graphs: one capture per replica (the library
+        # only launches kernels), checked bit for bit against the eager round
+        # of replica 0 before timing.
+        def outputs():
+            t = [topk_out[0], topk_out[1], tree_out["parent"], tree_out["token"], tree_out["anc"],
+                 tree_out["n_nodes"], acc_out["path"], acc_out["accept_len"], acc_out["bonus"]]
+            return [x.detach().clone() for x in t + attn_out]
+
+        step(0)
+        torch.cuda.synchronize()
+        ref = outputs()
+        graphs = []
+        side = torch.cuda.Stream()
+        for r in range(reps):
+            g = torch.cuda.CUDAGraph()
+            side.wait_stream(stream)
+            with torch.cuda.graph(g, stream=side):
+                step(r)
+            stream.wait_stream(side)
+            graphs.append(g)
+        torch.cuda.synchronize()
+        step(1 % reps)
+        graphs[0].replay()
+        torch.cuda.synchronize()
+        for a, b in zip(outputs(), ref):
+            assert torch.equal(a, b), "graph replay differs from the eager round"
+        ms_per_step = timed(lambda r: graphs[r].replay(), args.steps, args.warmup)
     # per-stage averages (each stage alone, same replica cycling), for the rooflines
     stage_ms = np.array([timed(f, args.steps, 0) for f in stage_fns])
     assert int(flags.item()) == 0, "device flagged NaN inputs"
@@ -229,6 +262,7 @@ def main() -> int:
         "metric": METRIC, "value": round(1e3 / ms_per_step, 2), "unit": "rounds/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 5),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": w.dtype,
+        "launch": "hip-graph" if args.launch == "graph" else "stream",
         "data": "synthetic",
         "config": {"workload": f"{w.name}: batch {w.batch}, block {w.depth}, vocab {w.vocab}, "
                                f"top-{w.k}, budget {w.budget}, GQA {w.hq}q/{w.hkv}kv d{w.head_dim}, "
@@ -240,6 +274,8 @@ def main() -> int:
         "accept_len": acc_out["accept_len"].cpu().tolist(),
         "gen_seconds": round(gen_s, 1),
     }
+    if args.launch == "graph":
+        line["ms_per_step_stream"] = round(ms_stream, 5)
     print(json.dumps(line), flush=True)
     return 0
 
