@@ -63,6 +63,8 @@ def main() -> int:
     ap.add_argument("--launch", choices=["stream", "graph"], default="stream",
                     help="timed rounds: every kernel launched on the stream (default), or one "
                          "captured HIP graph per input replica, replayed (measured slower)")
+    ap.add_argument("--at-scale-run", action="store_true",
+                    help="only the at-scale kernels (printed as JSON), for rocprofv3 counter runs")
     ap.add_argument("--traffic-run", action="store_true",
                     help="only the workload's tree attention (5 calls) and a 256 MiB device copy "
                          "(3 calls), for rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE runs")
@@ -79,6 +81,9 @@ def main() -> int:
 
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+    if args.at_scale_run:
+        print(json.dumps(measure_at_scale(P, sy, dev)), flush=True)
+        return 0
     w = sy.workload(args.workload)
     t_gen = time.time()
     rin = sy.round_inputs(w)
@@ -215,6 +220,22 @@ def main() -> int:
         for a, b in zip(outputs(), ref):
             assert torch.equal(a, b), "graph replay differs from the eager round"
         ms_per_step = timed(lambda r: graphs[r].replay(), args.steps, args.warmup)
+    # distribution of single rounds (each bracketed by its own event pair, still
+    # back to back with no host synchronisation), and the warm-cache rate with
+    # one replica repeated (labelled; every other figure is cold, DRAM)
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    for i, (a0, a1) in enumerate(ev):
+        a0.record(stream)
+        if args.launch == "graph":
+            graphs[(args.warmup + i) % reps].replay()
+        else:
+            step((args.warmup + i) % reps)
+        a1.record(stream)
+    torch.cuda.synchronize()
+    per_round_us = np.array([a0.elapsed_time(a1) * 1e3 for a0, a1 in ev])
+    warm_ms = timed(lambda r: step(0), args.steps, 0)
     # per-stage averages (each stage alone, same replica cycling), for the rooflines
     stage_ms = np.array([timed(f, args.steps, 0) for f in stage_fns])
     assert int(flags.item()) == 0, "device flagged NaN inputs"
@@ -269,6 +290,11 @@ def main() -> int:
                                f"ctx {w.ctx[0]}-{w.ctx[1]}, {w.layers} layer(s)",
                    "global_batch": w.batch, "replicas": reps},
         "sequence_rounds_per_s": round(w.batch * 1e3 / ms_per_step, 2),
+        "round_us": {"p10": round(float(np.percentile(per_round_us, 10)), 2),
+                     "p50": round(float(np.percentile(per_round_us, 50)), 2),
+                     "p90": round(float(np.percentile(per_round_us, 90)), 2),
+                     "rounds": int(per_round_us.size)},
+        "warm_rounds_per_s": round(1e3 / warm_ms, 2),
         "stages": stages, "roofline": roof, "cpu_baseline": cpu, "next_rows": extra,
         "at_scale": at_scale,
         "accept_len": acc_out["accept_len"].cpu().tolist(),
@@ -562,8 +588,28 @@ def cpu_baseline(w, rin, layers, seconds):
         if time.time() - t0 >= seconds:
             break
     el = time.time() - t0
-    return {"value": round(n / el, 4), "unit": "rounds/s", "cores": oracle.get_threads(),
-            "kind": "oracle", "sample": f"{n} whole round(s) of the same workload ({el:.1f} s)"}
+    cores = oracle.get_threads()
+    # the two sequential stages on one thread as well (one call each)
+    oracle.set_threads(1)
+    t1 = time.time()
+    ids, lp, _, _ = oracle.topk(rin["drafter_logits"], k, w.dtype)
+    t2 = time.time()
+    oracle.build_tree(ids.reshape(w.batch, D, k), lp.reshape(w.batch, D, k), rin["rho"], rin["lam"],
+                      rin["root_token"], D, k, w.budget)
+    t3 = time.time()
+    oracle.set_threads(threads)
+    model = ""
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    return {"value": round(n / el, 4), "unit": "rounds/s", "cores": cores,
+            "kind": "oracle", "sample": f"{n} whole round(s) of the same workload ({el:.1f} s)",
+            "cpu_model": model,
+            "one_thread_ms": {"topk": round((t2 - t1) * 1e3, 2), "build_tree": round((t3 - t2) * 1e3, 2)}}
 
 
 if __name__ == "__main__":

@@ -68,26 +68,28 @@ __global__ __launch_bounds__(kArgmaxWavesPerBlock * kWave) void argmax_partial_k
             v[e] = x;
         }
     }
-    float lm = -INFINITY, sum = 0.f;
+    // lane maximum with NaN propagation (a NaN anywhere in the lane makes it
+    // NaN, which is how NaN rows are detected)
+    float lm = v[0];
 #pragma unroll
-    for (int e = 0; e < E; ++e) {
-        lm = fmaxf(lm, v[e]);
-        sum += v[e];  // only to detect NaN
-    }
-    const float M = wave_max_f32_dpp(lm);
-    // lowest vocabulary id holding the chunk maximum
+    for (int e = 1; e < E; ++e) lm = __builtin_elementwise_maximum(lm, v[e]);
+    const bool nan_lane = !(lm == lm);
+    const float M = wave_max_f32_dpp(nan_lane ? -INFINITY : lm);
+    // lowest vocabulary id holding the chunk maximum: a lane's elements
+    // ascend in id, so its candidate is its first element equal to M
+    int first = E;
+#pragma unroll
+    for (int e = E - 1; e >= 0; --e) first = v[e] == M ? e : first;
     uint32_t best = 0xffffffffu;
-#pragma unroll
-    for (int e = 0; e < E; ++e) {
-        const int64_t idx = c0 + (int64_t)((e / P) * kWave + lane) * P + (e % P);
-        const bool hit = (v[e] == M) && (full || idx < vocab);
-        best = (hit && (uint32_t)idx < best) ? (uint32_t)idx : best;
+    if (first < E) {
+        const int64_t idx = c0 + (int64_t)((first / P) * kWave + lane) * P + (first % P);
+        if (full || idx < vocab) best = (uint32_t)idx;
     }
     best = wave_min_u32_dpp(best);
-    const float tot = wave_sum_f32_dpp(sum);
+    const bool any_nan = __ballot(nan_lane) != 0ull;
     if (lane == 0) {
         part[gw] = vocab_key(M, best);
-        if (!(tot == tot)) raise_flag(flags, PRESTO_FLAG_NAN_TARGET);
+        if (any_nan) raise_flag(flags, PRESTO_FLAG_NAN_TARGET);
     }
 }
 

@@ -115,7 +115,10 @@ __global__ __launch_bounds__(kTopkWavesPerBlock * kWave) void topk_partial_kerne
     constexpr int E = NLOAD * P;
     constexpr int64_t CH = (int64_t)kWave * E;
     constexpr int kGroupCap = kCandCap / P;      // candidate groups a wave list holds
-    __shared__ uint64_t cand[kTopkWavesPerBlock][kCandCap];
+    // per-wave candidate list: the values of up to kGroupCap groups and the
+    // vocabulary index of each group's first element
+    __shared__ __align__(16) float cand_v[kTopkWavesPerBlock][kCandCap];
+    __shared__ int32_t cand_i[kTopkWavesPerBlock][kGroupCap];
     __shared__ uint32_t cand_n[kTopkWavesPerBlock];
 
     const int wave = threadIdx.x / kWave, lane = lane_id();
@@ -192,20 +195,28 @@ __global__ __launch_bounds__(kTopkWavesPerBlock * kWave) void topk_partial_kerne
     // only groups whose maximum reaches it can hold a top-k entry
     const float thr = unord32(wave_kth_largest_u32(ord32(lm), k));
 
+    // A lane appends its candidate groups (values as they are) with one LDS
+    // atomic for all of them; the keys are formed afterwards, one candidate
+    // per lane, so the divergent part stays a few stores per group.
     if (lane == 0) cand_n[wave] = 0u;
     __builtin_amdgcn_wave_barrier();
+    uint32_t npass = 0u;
+#pragma unroll
+    for (int i = 0; i < NLOAD; ++i) npass += gmax[i] >= thr ? 1u : 0u;
+    uint32_t q = 0u;
+    if (npass != 0u) q = atomicAdd(&cand_n[wave], npass);
 #pragma unroll
     for (int i = 0; i < NLOAD; ++i) {
         if (gmax[i] >= thr) {
-            const uint32_t slot = atomicAdd(&cand_n[wave], 1u);
-            if (slot < (uint32_t)kGroupCap) {
+            if (q < (uint32_t)kGroupCap) {
+                float4* dst = reinterpret_cast<float4*>(&cand_v[wave][q * P]);
 #pragma unroll
-                for (int j = 0; j < P; ++j) {
-                    const int64_t idx = c0 + (int64_t)(i * kWave + lane) * P + j;
-                    const bool ok = (full || idx < vocab) && v[i * P + j] >= thr;
-                    cand[wave][slot * P + j] = ok ? vocab_key(v[i * P + j], (uint32_t)idx) : 0ull;
-                }
+                for (int j = 0; j < P / 4; ++j)
+                    dst[j] = make_float4(v[i * P + 4 * j], v[i * P + 4 * j + 1], v[i * P + 4 * j + 2],
+                                         v[i * P + 4 * j + 3]);
+                cand_i[wave][q] = (int32_t)(c0 + (int64_t)(i * kWave + lane) * P);
             }
+            ++q;
         }
     }
     __builtin_amdgcn_wave_barrier();
@@ -213,10 +224,15 @@ __global__ __launch_bounds__(kTopkWavesPerBlock * kWave) void topk_partial_kerne
     uint64_t* out = part_keys + gw * k;
 
     if (ngroups <= (uint32_t)kGroupCap) {
-        // one candidate key per lane (keys are unique); k rounds of wave max,
+        // one candidate per lane (keys are unique); k rounds of wave max,
         // retiring the lane that held it (0 past the last valid entry)
         const int total = (int)ngroups * P;
-        uint64_t x = lane < total ? cand[wave][lane] : 0ull;
+        uint64_t x = 0ull;
+        if (lane < total) {
+            const float xv = cand_v[wave][lane];
+            const int64_t idx = (int64_t)cand_i[wave][lane / P] + lane % P;
+            if ((full || idx < vocab) && xv >= thr) x = vocab_key(xv, (uint32_t)idx);
+        }
         uint64_t mine = 0ull;
         for (int j = 0; j < k; ++j) {
             const uint64_t m = wave_max_u64_dpp(x);
