@@ -17,6 +17,7 @@ constexpr int kArgmaxWavesPerBlock = 4;
 constexpr int kWalkThreads = 1024;
 constexpr int kMaxNodes = 1024;
 constexpr int kNodesPerWave = 8;
+constexpr int kKeyCols = 3;  // chunk keys per lane and node loaded at once
 
 template <bool BF16, int NLOAD>
 __global__ __launch_bounds__(kArgmaxWavesPerBlock * kWave) void argmax_partial_kernel(
@@ -121,21 +122,28 @@ __global__ __launch_bounds__(kWalkThreads) void accept_walk_kernel(
     const int my_tok = tid < n_max ? token[rb + tid] : 0;
     const int nn_raw = n_nodes[b];
     if (tid == 0) s_len = 0;
-    // each wave reduces the chunk keys of kNodesPerWave nodes at a time (all
-    // their loads in flight before the first reduction); rows of padding
-    // nodes are reduced too (never written in this call; ignored below)
+    // each wave reduces the chunk keys of kNodesPerWave nodes at a time, up to
+    // kKeyCols chunk keys per lane and node with every load in flight before
+    // the first reduction (one memory round trip for a 151936-entry bf16 row);
+    // rows of padding nodes are reduced too (never written in this call;
+    // ignored below)
     for (int n0 = wave * kNodesPerWave; n0 < n_max; n0 += nwaves * kNodesPerWave) {
         uint64_t best[kNodesPerWave];
 #pragma unroll
         for (int u = 0; u < kNodesPerWave; ++u) best[u] = 0ull;
-        for (int c = lane; c < chunks; c += kWave) {
+        for (int c0 = 0; c0 < chunks; c0 += kKeyCols * kWave) {
+            uint64_t x[kKeyCols][kNodesPerWave];
 #pragma unroll
-            for (int u = 0; u < kNodesPerWave; ++u) {
-                if (n0 + u < n_max) {
-                    const uint64_t x = part[(rb + n0 + u) * chunks + c];
-                    best[u] = x > best[u] ? x : best[u];
-                }
+            for (int t = 0; t < kKeyCols; ++t) {
+                const int c = c0 + t * kWave + lane;
+#pragma unroll
+                for (int u = 0; u < kNodesPerWave; ++u)
+                    x[t][u] = (c < chunks && n0 + u < n_max) ? part[(rb + n0 + u) * chunks + c] : 0ull;
             }
+#pragma unroll
+            for (int t = 0; t < kKeyCols; ++t)
+#pragma unroll
+                for (int u = 0; u < kNodesPerWave; ++u) best[u] = x[t][u] > best[u] ? x[t][u] : best[u];
         }
 #pragma unroll
         for (int u = 0; u < kNodesPerWave; ++u) {

@@ -166,27 +166,21 @@ __device__ __forceinline__ uint32_t wave_min_u32_dpp(uint32_t v) {
     return (uint32_t)__builtin_amdgcn_readlane((int)v, 63);
 }
 
-// Unsigned 64-bit max / min over the whole wave.
+// Unsigned 64-bit max / min over the whole wave, as two 32-bit reductions:
+// the high words first, then the low words of the lanes holding that high
+// word (each stage is one fused DPP max/min per step).
 __device__ __forceinline__ uint64_t wave_max_u64_dpp(uint64_t v) {
-    uint64_t t;
-    t = dpp_u64<0xb1>(0ull, v); v = t > v ? t : v;
-    t = dpp_u64<0x4e>(0ull, v); v = t > v ? t : v;
-    t = dpp_u64<0x114>(0ull, v); v = t > v ? t : v;
-    t = dpp_u64<0x118>(0ull, v); v = t > v ? t : v;
-    t = dpp_u64<0x142, 0xa>(0ull, v); v = t > v ? t : v;
-    t = dpp_u64<0x143, 0xc>(0ull, v); v = t > v ? t : v;
-    return readlane_u64(v, 63);
+    const uint32_t hi = (uint32_t)(v >> 32);
+    const uint32_t H = wave_max_u32_dpp(hi);
+    const uint32_t L = wave_max_u32_dpp(hi == H ? (uint32_t)v : 0u);
+    return ((uint64_t)H << 32) | L;
 }
 
 __device__ __forceinline__ uint64_t wave_min_u64_dpp(uint64_t v) {
-    uint64_t t;
-    t = dpp_u64<0xb1>(~0ull, v); v = t < v ? t : v;
-    t = dpp_u64<0x4e>(~0ull, v); v = t < v ? t : v;
-    t = dpp_u64<0x114>(~0ull, v); v = t < v ? t : v;
-    t = dpp_u64<0x118>(~0ull, v); v = t < v ? t : v;
-    t = dpp_u64<0x142, 0xa>(~0ull, v); v = t < v ? t : v;
-    t = dpp_u64<0x143, 0xc>(~0ull, v); v = t < v ? t : v;
-    return readlane_u64(v, 63);
+    const uint32_t hi = (uint32_t)(v >> 32);
+    const uint32_t H = wave_min_u32_dpp(hi);
+    const uint32_t L = wave_min_u32_dpp(hi == H ? (uint32_t)v : ~0u);
+    return ((uint64_t)H << 32) | L;
 }
 
 // Unsigned 64-bit max over lanes 0..15 (row 0), returned to every lane.
