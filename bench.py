@@ -137,8 +137,10 @@ def main() -> int:
     N = w.n_max
     tree_out = {k: torch.empty_like(v) for k, v in tree.items()}
     attn_out = [torch.empty_like(L["q"]) for L in layers]
+    total_ctx = int(np.asarray(ctx).sum())
     desc = P.AttnDesc(w.batch, N, w.hq, w.hkv, w.head_dim, max_ctx, w.scale,
-                      P.PRESTO_DT_BF16 if w.dtype == "bf16" else P.PRESTO_DT_F32)
+                      P.PRESTO_DT_BF16 if w.dtype == "bf16" else P.PRESTO_DT_F32,
+                      P.PRESTO_CTX_PACKED, total_ctx)
     import ctypes
     attn_ws_n = P.lib().presto_tree_attention_workspace(ctypes.byref(desc))
     attn_ws = torch.zeros(max(1, attn_ws_n), dtype=torch.uint8, device=dev) if attn_ws_n else None
@@ -162,7 +164,8 @@ def main() -> int:
         for li, L in enumerate(R[r]["layers"]):
             P.presto_tree_attention(L["q"], L["k_cache"], L["v_cache"], L["ctx_offsets"],
                                     L["k_tree"], L["v_tree"], tree_out["anc"], tree_out["n_nodes"],
-                                    max_ctx, w.scale, out=attn_out[li], workspace=attn_ws)
+                                    max_ctx, w.scale, out=attn_out[li], workspace=attn_ws,
+                                    total_ctx=total_ctx)
 
     def st_accept(r):
         P.presto_accept(R[r]["target"], tree_out["parent"], tree_out["token"], tree_out["n_nodes"],
@@ -433,12 +436,13 @@ def measure_at_scale(P, sy, dev):
         vt = torch.randn(w.batch, w.n_max, w.hkv, w.head_dim, device=dev, generator=gen).to(torch.bfloat16)
         ao = torch.empty_like(q)
         desc = P.AttnDesc(w.batch, w.n_max, w.hq, w.hkv, w.head_dim, int(ctx.max()), w.scale,
-                          P.PRESTO_DT_BF16)
+                          P.PRESTO_DT_BF16, P.PRESTO_CTX_PACKED, total)
         import ctypes
         nws = P.lib().presto_tree_attention_workspace(ctypes.byref(desc))
         aw = torch.zeros(max(1, nws), dtype=torch.uint8, device=dev) if nws else None
         us = time_us(lambda: P.presto_tree_attention(q, kc, vc, offs, kt, vt, tr["anc"], tr["n_nodes"],
-                                                     int(ctx.max()), w.scale, out=ao, workspace=aw))
+                                                     int(ctx.max()), w.scale, out=ao, workspace=aw,
+                                                     total_ctx=total))
         nn = tr["n_nodes"].cpu().numpy()
         dep = tr["depth"].cpu().numpy()
         ww = algorithmic_work(w, ctx, nn, dep)

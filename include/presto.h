@@ -269,6 +269,12 @@ typedef struct {
     float scale; /* usually 1/sqrt(head_dim) */
     presto_dtype dt;
     int32_t ctx_layout; /* presto_ctx_layout */
+    /* Sum of ctx_b over the batch, or 0 when the caller does not know it.
+     * A scheduling hint only: the result is the same for any value.  With
+     * ragged contexts it lets the context be split by the actual total, and
+     * the workgroups be dealt over the splits each sequence really has,
+     * instead of assuming batch x max_ctx. */
+    int64_t total_ctx;
 } presto_attn_desc;
 
 size_t presto_tree_attention_workspace(const presto_attn_desc *desc);

@@ -64,7 +64,8 @@ class TreeDesc(ctypes.Structure):
 class AttnDesc(ctypes.Structure):
     _fields_ = [("batch", ctypes.c_int32), ("n_max", ctypes.c_int32), ("hq", ctypes.c_int32),
                 ("hkv", ctypes.c_int32), ("head_dim", ctypes.c_int32), ("max_ctx", ctypes.c_int32),
-                ("scale", ctypes.c_float), ("dt", ctypes.c_int32), ("ctx_layout", ctypes.c_int32)]
+                ("scale", ctypes.c_float), ("dt", ctypes.c_int32), ("ctx_layout", ctypes.c_int32),
+                ("total_ctx", ctypes.c_int64)]
 
 
 class CommitDesc(ctypes.Structure):
@@ -292,17 +293,20 @@ def presto_tree_attention(q: torch.Tensor, k_cache: torch.Tensor, v_cache: torch
                           ctx_offsets: torch.Tensor, k_tree: torch.Tensor, v_tree: torch.Tensor,
                           anc: torch.Tensor, n_nodes: torch.Tensor, max_ctx: int,
                           scale: float | None = None, *, out=None, workspace=None, stream=None,
-                          ctx_layout: int = PRESTO_CTX_PACKED):
+                          ctx_layout: int = PRESTO_CTX_PACKED, total_ctx: int = 0):
     """Tree-masked attention of q [b, N, Hq, d] over [cache ; ancestors].
     ctx_offsets: [b + 1] packed offsets, or [b, 2] (start, len) pairs with
-    ctx_layout=PRESTO_CTX_SLOTS."""
+    ctx_layout=PRESTO_CTX_SLOTS.  total_ctx: the sum of the context lengths
+    when the caller knows it (a scheduling hint for ragged batches; 0 =
+    unknown); a workspace passed in must be sized for the same hint."""
     b, N, hq, d = q.shape
     hkv = k_tree.shape[2]
     scale = d ** -0.5 if scale is None else scale
     _dev(q, k_cache, v_cache, ctx_offsets, k_tree, v_tree, anc, n_nodes)
     out = torch.empty_like(q) if out is None else out
     _dev(out)
-    desc = AttnDesc(b, N, hq, hkv, d, int(max_ctx), float(scale), _dt(q), int(ctx_layout))
+    desc = AttnDesc(b, N, hq, hkv, d, int(max_ctx), float(scale), _dt(q), int(ctx_layout),
+                    int(total_ctx))
     need = lib().presto_tree_attention_workspace(ctypes.byref(desc))
     ws, nb = _workspace(need, q.device, workspace)
     _check(lib().presto_tree_attention(

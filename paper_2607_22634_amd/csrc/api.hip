@@ -256,7 +256,7 @@ presto_status presto_build_tree(const presto_tree_desc* desc, const int32_t* ids
 
 size_t presto_tree_attention_workspace(const presto_attn_desc* desc) {
     if (!desc || desc->batch <= 0 || desc->n_max <= 0 || desc->hkv <= 0 || desc->hq <= 0 ||
-        desc->hq % desc->hkv != 0 || desc->max_ctx < 0)
+        desc->hq % desc->hkv != 0 || desc->max_ctx < 0 || desc->total_ctx < 0)
         return 0;
     return attn_workspace_bytes(desc);
 }
@@ -278,6 +278,7 @@ presto_status presto_tree_attention(const presto_attn_desc* desc, const void* q,
     REQUIRE(d.head_dim == 64 || d.head_dim == 128, "presto_tree_attention: head_dim %d",
             d.head_dim);
     REQUIRE(d.max_ctx >= 0, "presto_tree_attention: max_ctx < 0");
+    REQUIRE(d.total_ctx >= 0, "presto_tree_attention: total_ctx < 0");
     REQUIRE(d.ctx_layout == PRESTO_CTX_PACKED || d.ctx_layout == PRESTO_CTX_SLOTS,
             "presto_tree_attention: unknown ctx_layout %d", d.ctx_layout);
     REQUIRE(isfinite(d.scale) && d.scale > 0.f, "presto_tree_attention: scale must be positive");

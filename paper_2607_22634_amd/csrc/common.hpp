@@ -166,6 +166,17 @@ __device__ __forceinline__ uint32_t wave_min_u32_dpp(uint32_t v) {
     return (uint32_t)__builtin_amdgcn_readlane((int)v, 63);
 }
 
+// Inclusive prefix sum over the lanes of a wave.
+__device__ __forceinline__ int wave_prefix_sum_i32(int v) {
+    const int lane = lane_id();
+#pragma unroll
+    for (int d = 1; d < kWave; d <<= 1) {
+        const int t = __shfl_up(v, d);
+        if (lane >= d) v += t;
+    }
+    return v;
+}
+
 // Unsigned 64-bit max / min over the whole wave, as two 32-bit reductions:
 // the high words first, then the low words of the lanes holding that high
 // word (each stage is one fused DPP max/min per step).

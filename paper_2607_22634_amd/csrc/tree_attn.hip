@@ -75,6 +75,7 @@ struct AttnArgs {
     int32_t batch, n_max, hq, hkv, G, W;
     int32_t row_tiles, rows_pad, splits, split_len;
     int32_t n_tasks, n_blocks;
+    int32_t compact;  // tasks dealt over the (sequence, split) pairs that hold keys
     float scale_log2;  // scale * log2(e)
 };
 
@@ -150,12 +151,55 @@ __global__ __launch_bounds__(NW * kWave) void tree_attn_bf16_kernel(AttnArgs a) 
     __shared__ __align__(16) uint16_t sV[kBufs * VBUF];
     __shared__ uint64_t s_anc[(ROWS + 1) * kMaxAncWords];  // ancestor rows of this tile's nodes
 
-    const int task = xcd_task(blockIdx.x, a.n_blocks);
-    if (task >= a.n_tasks) return;
+    int task, split, g, b;
+    if (a.compact) {
+        // task = ((pair * hkv) + g) * row_tiles + rt, pair = the index of
+        // (sequence b, split) among the splits the sequences actually have,
+        // in sequence order.  Every wave counts the pairs itself, then deals
+        // the tasks over the XCDs as in the dense case, but over the tasks
+        // that exist (the grid is an upper bound).
+        const int lane0 = lane_id();
+        auto splits_of = [&](int bb) {
+            if (bb >= a.batch) return 0;
+            const int kb = ctx_span(a.ctx_off, bb, a.ctx_slots).ctx + clamp_nodes(a.n_nodes[bb], a.n_max);
+            return (kb + a.split_len - 1) / a.split_len;
+        };
+        int pairs = 0;
+        for (int b0 = 0; b0 < a.batch; b0 += kWave) {
+            const int incl = wave_prefix_sum_i32(splits_of(b0 + lane0));
+            pairs += __builtin_amdgcn_readlane(incl, kWave - 1);
+        }
+        const int n_tasks = pairs * a.hkv * a.row_tiles;
+        const int n_blocks = (n_tasks + 7) / 8 * 8;
+        if ((int)blockIdx.x >= n_blocks) return;
+        task = xcd_task(blockIdx.x, n_blocks);
+        if (task >= n_tasks) return;
+        g = (task / a.row_tiles) % a.hkv;
+        const int item = task / a.row_tiles / a.hkv;
+        b = -1;
+        split = 0;
+        int base = 0;
+        for (int b0 = 0; b0 < a.batch; b0 += kWave) {
+            const int ns = splits_of(b0 + lane0);
+            const int incl = wave_prefix_sum_i32(ns);
+            const uint64_t hit = __ballot(ns > 0 && item >= base + incl - ns && item < base + incl);
+            if (hit) {
+                const int l = __ffsll((unsigned long long)hit) - 1;
+                b = b0 + l;
+                split = item - base - (__builtin_amdgcn_readlane(incl, l) - __builtin_amdgcn_readlane(ns, l));
+                break;
+            }
+            base += __builtin_amdgcn_readlane(incl, kWave - 1);
+        }
+        if (b < 0) return;
+    } else {
+        task = xcd_task(blockIdx.x, a.n_blocks);
+        if (task >= a.n_tasks) return;
+        split = (task / a.row_tiles) % a.splits;
+        g = (task / a.row_tiles / a.splits) % a.hkv;
+        b = task / a.row_tiles / a.splits / a.hkv;
+    }
     const int rt = task % a.row_tiles;
-    const int split = (task / a.row_tiles) % a.splits;
-    const int g = (task / a.row_tiles / a.splits) % a.hkv;
-    const int b = task / a.row_tiles / a.splits / a.hkv;
 
     const CtxSpan cs = ctx_span(a.ctx_off, b, a.ctx_slots);
     const int c0 = cs.c0, ctx = cs.ctx;
@@ -627,6 +671,7 @@ using namespace presto;
 
 struct AttnPlan {
     int G, rows, row_tiles, rows_per_tile, rows_pad, waves, rb, splits, split_len;
+    bool compact;
     int64_t tasks, blocks;
 };
 
@@ -646,8 +691,13 @@ static AttnPlan attn_plan(const presto_attn_desc* d) {
     // + about 3 for a workgroup's prologue) plus the merge, whose partials
     // (2 D + 8 bytes per query row and split, written and read back, about
     // 4 MB per key-block time) grow with the split count
-    const int64_t base = (int64_t)d->batch * d->hkv * p.row_tiles;
-    const int keys = d->max_ctx + d->n_max;
+    // With ragged contexts and the caller's total, the workgroups are dealt
+    // over the (sequence, split) pairs that exist (about total/len + batch/2
+    // of them) rather than batch x splits of the longest sequence.
+    const int64_t per_pair = (int64_t)d->hkv * p.row_tiles;  // workgroups per (sequence, split)
+    const int keys = d->max_ctx + d->n_max;                  // the longest sequence
+    p.compact = d->batch > 1 && d->total_ctx > 0 && d->total_ctx < (int64_t)d->batch * d->max_ctx;
+    const double total_keys = (double)d->total_ctx + (double)d->batch * d->n_max;
     const int max_splits = (keys + 127) / 128;
     double best_cost = 1e30;
     p.splits = 1;
@@ -656,9 +706,11 @@ static AttnPlan attn_plan(const presto_attn_desc* d) {
         int len = (keys + s - 1) / s;
         len = (len + kKeyTile - 1) / kKeyTile * kKeyTile;
         const int se = (keys + len - 1) / len;
-        const double rounds = (double)((base * se + 255) / 256);
+        const double pairs = p.compact ? fmin((double)d->batch * se, total_keys / len + 0.5 * d->batch)
+                                       : (double)d->batch * se;
+        const double rounds = ceil(pairs * per_pair / 256.0);
         const double merge_bytes =
-            se > 1 ? 2.0 * d->batch * d->hkv * p.rows * se * (2.0 * d->head_dim + 8.0) : 0.0;
+            se > 1 ? 2.0 * d->hkv * p.rows * pairs * (2.0 * d->head_dim + 8.0) : 0.0;
         const double cost = rounds * ((len + 31) / 32 + 3) + merge_bytes / 4.0e6;
         if (cost < best_cost - 1e-9) {
             best_cost = cost;
@@ -666,7 +718,7 @@ static AttnPlan attn_plan(const presto_attn_desc* d) {
             p.split_len = len;
         }
     }
-    p.tasks = base * p.splits;
+    p.tasks = (int64_t)d->batch * p.splits * per_pair;  // in compact mode an upper bound
     p.blocks = (p.tasks + 7) / 8 * 8;
     return p;
 }
@@ -724,6 +776,7 @@ presto_status launch_tree_attention(const presto_attn_desc* d, const void* q, co
     a.splits = p.splits;
     a.split_len = p.split_len;
     a.n_tasks = (int32_t)p.tasks;
+    a.compact = p.compact ? 1 : 0;
     a.n_blocks = (int32_t)p.blocks;
     a.scale_log2 = d->scale * kLog2e;
     const dim3 block(p.waves * kWave), grid((unsigned)p.blocks);

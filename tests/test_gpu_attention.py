@@ -25,11 +25,12 @@ def _tree_for(cfg):
     return w, tree_to_dev(oracle_tree(cfg))
 
 
-def _run(w, att, tree_dev):
+def _run(w, att, tree_dev, total_ctx=0):
     return P.presto_tree_attention(
         to_dev(att["q"], w.dtype), to_dev(att["k_cache"], w.dtype), to_dev(att["v_cache"], w.dtype),
         to_dev(att["ctx_offsets"]), to_dev(att["k_tree"], w.dtype), to_dev(att["v_tree"], w.dtype),
-        tree_dev["anc"], tree_dev["n_nodes"], int(np.diff(att["ctx_offsets"]).max()), w.scale)
+        tree_dev["anc"], tree_dev["n_nodes"], int(np.diff(att["ctx_offsets"]).max()), w.scale,
+        total_ctx=total_ctx)
 
 
 def _row_errors(got, ref):
@@ -132,3 +133,30 @@ def test_attention_is_deterministic():
     a = to_host(_run(w, att, tree))
     b = to_host(_run(w, att, tree))
     np.testing.assert_array_equal(a, b)
+
+
+@pytest.mark.parametrize("hint", ["actual", "tiny", "half", "uniform"])
+def test_attention_ragged_total_ctx_hint(hint):
+    """Ragged contexts (workload 3): the total-context hint only changes how
+    the context is split and dealt to workgroups, never the result; a hint
+    below the real total (down to 1) or at batch x max_ctx (no compaction)
+    must match the oracle just the same."""
+    w, tree = _tree_for(3)
+    _, att = attn_data(3)
+    ctx = np.diff(att["ctx_offsets"]).astype(np.int64)
+    total = {"actual": int(ctx.sum()), "tiny": 1, "half": int(ctx.sum()) // 2,
+             "uniform": int(w.batch * ctx.max())}[hint]
+    print(f"attn ragged hint={hint} total_ctx={total}", flush=True)
+    out = _run(w, att, tree, total_ctx=total)
+    torch.cuda.synchronize()
+    th = tree_to_host(tree)
+    ref = oracle.tree_attention(w.dtype, att["q"], att["k_cache"], att["v_cache"],
+                                att["ctx_offsets"], att["k_tree"], att["v_tree"], th["anc"],
+                                th["n_nodes"], w.scale)
+    got = sy.as_f32(to_host(out), w.dtype).astype(np.float64)
+    reff = sy.as_f32(ref, w.dtype).astype(np.float64)
+    for s in range(w.batch):
+        nn = int(th["n_nodes"][s])
+        err = _row_errors(got[s, :nn], reff[s, :nn])
+        assert err.max() <= 2e-2, (s, err.max())
+        assert not got[s, nn:].any()
