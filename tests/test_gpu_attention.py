@@ -160,3 +160,53 @@ def test_attention_ragged_total_ctx_hint(hint):
         err = _row_errors(got[s, :nn], reff[s, :nn])
         assert err.max() <= 2e-2, (s, err.max())
         assert not got[s, nn:].any()
+
+
+@pytest.mark.parametrize("layout", ["packed", "slots"])
+def test_attention_many_ragged_sequences_compact(layout):
+    """More sequences than a wave has lanes (70), ragged contexts including
+    empty ones, with the total-context hint: the workgroups' pair search runs
+    over several 64-sequence groups.  The slots layout leaves gaps of large
+    values between the sequences' cache rows, which must never be read."""
+    rng = np.random.default_rng(77 if layout == "packed" else 78)
+    b, N, hq, hkv, d, dtype = 70, 9, 8, 2, 64, "bf16"
+    ctx = rng.integers(0, 600, b).astype(np.int32)
+    ctx[[3, 40]] = 0
+    ctx[65] = 3000
+    parent = np.full((b, N), -1, np.int32)
+    n_nodes = rng.integers(1, N + 1, b).astype(np.int32)
+    for s in range(b):
+        for n in range(1, int(n_nodes[s])):
+            parent[s, n] = rng.integers(0, n)
+    att, anc = _edge_inputs(rng, b, N, hq, hkv, d, ctx, dtype, parent, n_nodes)
+    scale = 1 / np.sqrt(d)
+    total = int(ctx.sum())
+    kc, vc, offs = att["k_cache"], att["v_cache"], att["ctx_offsets"]
+    ctx_arg, lay = offs, P.PRESTO_CTX_PACKED
+    if layout == "slots":
+        gap = 5
+        start = (offs[:-1] + gap * np.arange(1, b + 1)).astype(np.int32)
+        rows = int(start[-1] + ctx[-1]) + gap
+        big = sy.cast(np.full((rows, hkv, d), 300.0, np.float32), dtype)
+        ks, vs = big.copy(), big.copy()
+        for s in range(b):
+            ks[start[s]:start[s] + ctx[s]] = kc[offs[s]:offs[s + 1]]
+            vs[start[s]:start[s] + ctx[s]] = vc[offs[s]:offs[s + 1]]
+        kc_dev, vc_dev = to_dev(ks, dtype), to_dev(vs, dtype)
+        ctx_arg, lay = np.stack([start, ctx], axis=1).astype(np.int32), P.PRESTO_CTX_SLOTS
+    else:
+        kc_dev, vc_dev = to_dev(kc, dtype), to_dev(vc, dtype)
+    print(f"attn compact layout={layout} batch={b} total_ctx={total}", flush=True)
+    out = P.presto_tree_attention(
+        to_dev(att["q"], dtype), kc_dev, vc_dev, to_dev(ctx_arg), to_dev(att["k_tree"], dtype),
+        to_dev(att["v_tree"], dtype), to_dev(anc), to_dev(n_nodes), int(ctx.max()), scale,
+        ctx_layout=lay, total_ctx=total)
+    torch.cuda.synchronize()
+    ref = oracle.tree_attention(dtype, att["q"], kc, vc, offs, att["k_tree"], att["v_tree"], anc,
+                                n_nodes, scale)
+    got = sy.as_f32(to_host(out), dtype).astype(np.float64)
+    reff = sy.as_f32(ref, dtype).astype(np.float64)
+    for s in range(b):
+        nn = int(n_nodes[s])
+        assert _row_errors(got[s, :nn], reff[s, :nn]).max() <= 2e-2, s
+        assert not got[s, nn:].any()
