@@ -18,12 +18,13 @@
 // 64-key LDS buffers rotate: tile t is consumed, tile t+1 is resident (the
 // last block of a tile already scores the first block of the next), tile t+2
 // waits in registers; one barrier per tile.  Inside a wave the scores of
-// block i+1 are computed while the softmax and P V of block i run, so the
-// matrix cores and the vector ALUs overlap.  The running reference maximum
+// block i+1 are issued ahead of the softmax and P V of block i, so the matrix
+// cores can run while the vector ALUs work.  The running reference maximum
 // only moves when a block exceeds it by a margin, which keeps the 64-register
 // accumulator rescale off the common path.  The context is split across
-// workgroups when the batch alone cannot fill the chip; partial (reference,
-// sum, accumulator) triples are then merged by a second kernel.
+// workgroups when the batch alone cannot fill the chip; each split leaves,
+// per query row, its (reference, sum) pair and its output divided by its own
+// sum (bf16), which a second kernel merges.
 #include <math.h>
 
 #include "common.hpp"
@@ -73,7 +74,7 @@ struct AttnArgs {
     uint16_t* part_o;
     float2* part_ml;
     int32_t batch, n_max, hq, hkv, G, W;
-    int32_t row_tiles, rows_pad, splits, split_len;
+    int32_t row_tiles, splits, split_len;
     int32_t n_tasks, n_blocks;
     int32_t compact;  // tasks dealt over the (sequence, split) pairs that hold keys
     float scale_log2;  // scale * log2(e)
@@ -670,7 +671,7 @@ namespace presto_host {
 using namespace presto;
 
 struct AttnPlan {
-    int G, rows, row_tiles, rows_per_tile, rows_pad, waves, rb, splits, split_len;
+    int G, rows, row_tiles, rows_per_tile, waves, rb, splits, split_len;
     bool compact;
     int64_t tasks, blocks;
 };
@@ -685,7 +686,6 @@ static AttnPlan attn_plan(const presto_attn_desc* d) {
     p.waves = kAttnWaves / p.rb;
     p.rows_per_tile = p.waves * kRowsPerWave * p.rb;
     p.row_tiles = (p.rows + p.rows_per_tile - 1) / p.rows_per_tile;
-    p.rows_pad = p.rows_per_tile * p.row_tiles;
     // context splits: one workgroup per CU, so the time in key-block units
     // (about 0.85 us each) is (rounds of workgroups) x (key blocks per split
     // + about 3 for a workgroup's prologue) plus the merge, whose partials
@@ -772,7 +772,6 @@ presto_status launch_tree_attention(const presto_attn_desc* d, const void* q, co
     a.G = p.G;
     a.W = (d->n_max + 63) / 64;
     a.row_tiles = p.row_tiles;
-    a.rows_pad = p.rows_pad;
     a.splits = p.splits;
     a.split_len = p.split_len;
     a.n_tasks = (int32_t)p.tasks;
