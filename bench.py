@@ -250,6 +250,9 @@ def main() -> int:
         entry = {"us": round(us, 2)}
         if nme == "topk":
             entry["GB/s"] = round(work["topk_bytes"] / (us * 1e3), 1)
+        elif nme == "build_tree":
+            # a sequential search per sequence: latency per committed node
+            entry["ns_per_node"] = round(us * 1e3 / max(1, int(np.asarray(th["n_nodes"]).max()) - 1), 1)
         elif nme == "tree_attention":
             entry["GB/s"] = round(w.layers * work["attn_bytes_per_layer"] / (us * 1e3), 1)
             entry["TFLOP/s"] = round(w.layers * work["attn_flops_per_layer"] / (us * 1e6), 2)
