@@ -187,7 +187,8 @@ __global__ __launch_bounds__(NW * kWave) void tree_attn_bf16_kernel(AttnArgs a) 
             if (hit) {
                 const int l = __ffsll((unsigned long long)hit) - 1;
                 b = b0 + l;
-                split = item - base - (__builtin_amdgcn_readlane(incl, l) - __builtin_amdgcn_readlane(ns, l));
+                // last split first (see below)
+                split = __builtin_amdgcn_readlane(incl, l) - 1 - (item - base);
                 break;
             }
             base += __builtin_amdgcn_readlane(incl, kWave - 1);
@@ -196,9 +197,14 @@ __global__ __launch_bounds__(NW * kWave) void tree_attn_bf16_kernel(AttnArgs a) 
     } else {
         task = xcd_task(blockIdx.x, a.n_blocks);
         if (task >= a.n_tasks) return;
-        split = (task / a.row_tiles) % a.splits;
-        g = (task / a.row_tiles / a.splits) % a.hkv;
-        b = task / a.row_tiles / a.splits / a.hkv;
+        // task = ((b * splits + split') * hkv + g) * row_tiles + rt with the
+        // splits in reverse (split' = 0 is the last split): the XCDs start
+        // their workgroups a few microseconds apart in XCD order, and the
+        // last split, which holds the tree keys and their masks and so runs
+        // longest, then lands on the XCDs that start first.
+        g = (task / a.row_tiles) % a.hkv;
+        split = a.splits - 1 - (task / a.row_tiles / a.hkv) % a.splits;
+        b = task / a.row_tiles / a.hkv / a.splits;
     }
     const int rt = task % a.row_tiles;
 
@@ -353,21 +359,32 @@ __global__ __launch_bounds__(NW * kWave) void tree_attn_bf16_kernel(AttnArgs a) 
                                                          false, false);
         return fmaxf(mx, __uint_as_float(h == 0 ? sw[1] : sw[0]));
     };
+    // Visibility of the block's 32 keys for this lane's row as one 32-bit
+    // mask (bit t: key j0 + t): context keys, then the row's ancestor bits
+    // from tree index j0 - ctx on, cut at the split's end; each element then
+    // costs one bit test and one select.
     auto apply_mask = [&](floatx16& S, int j0, int nd) {
-        uint64_t aw0 = 0ull, aw1 = 0ull;
-        const int wbase = max(0, j0 - ctx) >> 6;
+        const int s0 = j0 - ctx;  // tree index of the block's first key (< 0: it starts in the context)
+        uint32_t anc = 0u;
         if (j0 + 32 > ctx) {
             const uint64_t* arow = &s_anc[(nd - n_first) * a.W];
-            aw0 = arow[wbase];
-            aw1 = wbase + 1 < a.W ? arow[wbase + 1] : 0ull;
+            if (s0 >= 0) {
+                const int w = s0 >> 6, sh = s0 & 63;
+                const uint64_t lo = arow[w];
+                const uint64_t hi = w + 1 < a.W ? arow[w + 1] : 0ull;
+                anc = (uint32_t)(sh == 0 ? lo : (lo >> sh) | (hi << (64 - sh)));
+            } else {
+                anc = (uint32_t)(arow[0] << (-s0));  // -s0 in 1 .. 31
+            }
         }
+        const int nctx = ctx - j0, nend = k_end - j0;
+        const uint32_t ctx_mask = nctx >= 32 ? ~0u : (nctx <= 0 ? 0u : (1u << nctx) - 1u);
+        const uint32_t end_mask = nend >= 32 ? ~0u : (nend <= 0 ? 0u : (1u << nend) - 1u);
+        const uint32_t vis = ((ctx_mask | anc) & end_mask) >> (4 * h);
 #pragma unroll
         for (int e = 0; e < 16; ++e) {
-            const int j = j0 + 8 * (e >> 2) + 4 * h + (e & 3);
-            const int m = max(j - ctx, 0);
-            const uint64_t wd = ((m >> 6) - wbase) == 0 ? aw0 : aw1;
-            const bool vis = (j < k_end) & ((j < ctx) | (bool)((wd >> (m & 63)) & 1ull));
-            S[e] = vis ? S[e] : -INFINITY;
+            const int t = 8 * (e >> 2) + (e & 3);  // element e is key j0 + 8(e/4) + 4h + e%4
+            S[e] = ((vis >> t) & 1u) ? S[e] : -INFINITY;
         }
     };
     // move m of row block rb when its block maximum mx (raw score) exceeds
