@@ -69,8 +69,9 @@ struct AttnArgs {
     const uint64_t* anc;
     const int32_t* n_nodes;
     uint16_t* out;
-    // split partials when splits > 1, per query row (b, g, rho < G n_max) and
-    // split: the normalised output as bf16 [.., splits, D] and (m, l) fp32
+    // split partials when splits > 1: the normalised output as bf16
+    // [b, g, split, rho < G n_max, D] (a workgroup's rows are contiguous, so
+    // its writes fill whole cache lines) and (m, l) fp32 [b, g, rho, split]
     uint16_t* part_o;
     float2* part_ml;
     int32_t batch, n_max, hq, hkv, G, W;
@@ -524,7 +525,12 @@ __global__ __launch_bounds__(NW * kWave) void tree_attn_bf16_kernel(AttnArgs a) 
                 }
         } else {
             // normalised here, so bf16 holds it to the output's own precision
-            const int64_t pr = (((int64_t)b * a.hkv + g) * all_rows + rho[rb]) * a.splits + split;
+            // output [b, g, split, row] (a workgroup's rows are contiguous: whole
+            // lines); (m, l) [b, g, row, split] (the merge reads a row's splits
+            // side by side)
+            const int64_t bg = (int64_t)b * a.hkv + g;
+            const int64_t pr = (bg * a.splits + split) * all_rows + rho[rb];
+            const int64_t pm = (bg * all_rows + rho[rb]) * a.splits + split;
             uint16_t* po = a.part_o + pr * D;
             const float inv = l > 0.f ? 1.f / l : 0.f;
 #pragma unroll
@@ -536,7 +542,7 @@ __global__ __launch_bounds__(NW * kWave) void tree_attn_bf16_kernel(AttnArgs a) 
                         make_uint2(pack_bf16x2(o[rb][db][4 * q4] * inv, o[rb][db][4 * q4 + 1] * inv),
                                    pack_bf16x2(o[rb][db][4 * q4 + 2] * inv, o[rb][db][4 * q4 + 3] * inv));
                 }
-            if (h == 0) a.part_ml[pr] = make_float2(m_run[rb], l);
+            if (h == 0) a.part_ml[pm] = make_float2(m_run[rb], l);
         }
     }
 }
@@ -566,10 +572,12 @@ __global__ __launch_bounds__(256) void tree_attn_merge_kernel(AttnArgs a) {
     if (rho < a.G * nn) {
         const int keys = ctx_span(a.ctx_off, b, a.ctx_slots).ctx + nn;
         const int nsplit = min(a.splits, (keys + a.split_len - 1) / a.split_len);
-        const int64_t pr = (((int64_t)b * a.hkv + g) * a.G * a.n_max + rho) * a.splits;
+        // split s of this row: ((b, g) * splits + s) * rows + rho
+        const int64_t rows_g = (int64_t)a.G * a.n_max;
+        const int64_t pr = ((int64_t)b * a.hkv + g) * a.splits * rows_g + rho;
         const uint16_t* po = a.part_o + pr * D + lane * PER;
         float2 ml = make_float2(-INFINITY, 0.f);
-        if (lane < nsplit) ml = a.part_ml[pr + lane];
+        if (lane < nsplit) ml = a.part_ml[(((int64_t)b * a.hkv + g) * rows_g + rho) * a.splits + lane];
         const float M = wave_max_f32_dpp(ml.x);
         const float wl = ml.x == -INFINITY ? 0.f : exp2f(ml.x - M) * ml.y;  // weight of split `lane`
         const float L = wave_sum_f32_dpp(wl);
@@ -579,9 +587,9 @@ __global__ __launch_bounds__(256) void tree_attn_merge_kernel(AttnArgs a) {
             for (int u = 0; u < kMergeUnroll; ++u) {
                 const int s = min(s0 + u, nsplit - 1);
                 if constexpr (PER == 1) {
-                    v[u][0] = bf16_to_f(po[(int64_t)s * D]);
+                    v[u][0] = bf16_to_f(po[s * rows_g * D]);
                 } else {
-                    const uint32_t w2 = *reinterpret_cast<const uint32_t*>(po + (int64_t)s * D);
+                    const uint32_t w2 = *reinterpret_cast<const uint32_t*>(po + s * rows_g * D);
                     v[u][0] = bf16_to_f((uint16_t)(w2 & 0xffffu));
                     v[u][1] = bf16_to_f((uint16_t)(w2 >> 16));
                 }
