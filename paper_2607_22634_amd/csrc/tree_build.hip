@@ -262,19 +262,22 @@ __global__ __launch_bounds__(kWave) void tree_build_kernel(TreeArgs a) {
     // Children of node n (depth d, own rank rn, parent's rank rp, score Sn):
     // lane r < k scores candidate r, the children are ranked by (S desc,
     // rank asc) with in-row rotations and stored in that order; returns the
-    // first child as (ord S, rank), ord 0 if none.
+    // first child as (ord S, rank), ord 0 if none.  A node at the depth limit
+    // (d == D) has no children: nothing is stored and ord 0 is returned.
     auto expand = [&](int n, int d, int rn, int rp, float Sn, int bidx, uint32_t& c_ord, int& c_rank) {
+        const bool live = d < D;
+        const int dr = min(d, D - 1);      // drafter row read (clamped at the depth limit)
         const int ctx2 = d >= 2 ? rp : 0;  // grandparent slot of the trigram
         const int ctx1 = d >= 1 ? rn : 0;  // parent slot of the trigram
-        const float lam_d = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(lam_lane), d));
+        const float lam_d = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(lam_lane), dr));
         // every lane reads (lanes >= k at a clamped index) so that no branch
         // separates the reads from their use; only lanes < k are kept
         const int rl = min(lane, k - 1);
         float s;
         {
-            const float lq = s_lp[d * k + rl];
+            const float lq = s_lp[dr * k + rl];
             if constexpr (RHO != 0) {
-                const int ri = ((d * k + ctx2) * k + ctx1) * k + rl;
+                const int ri = ((dr * k + ctx2) * k + ctx1) * k + rl;
                 float lr;
                 if constexpr (RHO == 1)
                     lr = s_rho[ri];
@@ -287,7 +290,7 @@ __global__ __launch_bounds__(kWave) void tree_build_kernel(TreeArgs a) {
             }
             s = (s == s && lane < k) ? s : -INFINITY;
         }
-        bool in = lane < k;
+        bool in = lane < k && live;
         if constexpr (BEAM) {
             // the children in T (the beam pass applied the branch filter)
             in = in && s_ktab[((d + 1) * Wb + bidx) * k + rl] >= -1;
@@ -310,7 +313,7 @@ __global__ __launch_bounds__(kWave) void tree_build_kernel(TreeArgs a) {
             pos = row_count_greater<15>(key);
         // the lanes that are not children all land on the first free position
         // and write the end marker there
-        if (lane < k) {
+        if (lane < k && live) {
             s_kord[n * k + pos] = in ? o : 0u;
             s_krank[n * k + pos] = (uint8_t)lane;
         }
@@ -418,12 +421,13 @@ __global__ __launch_bounds__(kWave) void tree_build_kernel(TreeArgs a) {
         // (read unconditionally, at a clamped index, so that its latency
         // overlaps the expansion's reads)
         const int si = p * k + min(pos + 1, k - 1);
-        const uint32_t sib_ord = pos + 1 < k ? s_kord[si] : 0u;
+        const uint32_t sib_raw = s_kord[si];
         const int sib_rank = s_krank[si];
         // first child of n
         uint32_t kid_ord = 0u;
         int kid_rank = 0;
-        if (d < D && bidx >= 0) expand(n, d, r, rp, S, bidx, kid_ord, kid_rank);
+        if (!BEAM || (d < D && bidx >= 0)) expand(n, d, r, rp, S, bidx, kid_ord, kid_rank);
+        const uint32_t sib_ord = pos + 1 < k ? sib_raw : 0u;
 
         // pushes: the first reuses the popped slot, the second takes a fresh slot
         uint32_t xS = 0u, xM = 0u, yS = 0u, yM = 0u;
