@@ -363,8 +363,9 @@ def measure_at_scale(P, sy, dev):
     drafter rows, 4128 node rows), tree attention at workload 3 (16 ragged
     contexts, HBM-bound) and workload 4 (4 x 32768 keys, MFMA-bound).  Inputs
     are N(0, 1) device draws of those shapes (scaled like the workloads'
-    logits); trees come from the GPU stages on them.  Timing only: parity at
-    these shapes is covered by the tests."""
+    logits); trees come from the GPU stages on them, and the tree build is
+    timed at workloads 3, 4 and 5 (latency-bound: one wave per sequence).
+    Timing only: parity at these shapes is covered by the tests."""
     import torch
 
     def time_us(fn, n=10):
@@ -390,6 +391,13 @@ def measure_at_scale(P, sy, dev):
         return {"us": round(us, 2), "bound": "hbm", "GB/s": round(gbs, 1), "TFLOP/s": round(tfs, 1),
                 "frac": round(gbs / HBM_PEAK_GBS, 4)}
 
+    def tree_latency(us, tree):
+        # one wave per sequence, all sequences at once: the launch takes as
+        # long as the longest sequence's search
+        nodes = int(tree["n_nodes"].max().item())
+        return {"us": round(us, 2), "bound": "latency", "nodes_per_seq": nodes,
+                "ns_per_node": round(us * 1e3 / nodes, 1)}
+
     gen = torch.Generator(device=dev)
     gen.manual_seed(1234)
     out = {}
@@ -408,8 +416,11 @@ def measure_at_scale(P, sy, dev):
     root = torch.zeros(w5.batch, dtype=torch.int32, device=dev)
     lp = torch.log_softmax(torch.randn(rows, 64, device=dev, generator=gen) * 4, dim=1)
     lp, ids = torch.topk(lp, w5.k, dim=1)
-    tree = P.presto_build_tree(ids.to(torch.int32).contiguous(), lp.contiguous(), None, lam, root,
-                               w5.depth, w5.k, w5.budget)
+    ids32, lpc = ids.to(torch.int32).contiguous(), lp.contiguous()
+    tree = P.presto_build_tree(ids32, lpc, None, lam, root, w5.depth, w5.k, w5.budget)
+    us = time_us(lambda: P.presto_build_tree(ids32, lpc, None, lam, root, w5.depth, w5.k, w5.budget,
+                                             out=tree))
+    out[f"tree_build_{w5.name}"] = tree_latency(us, tree)
     target = (torch.randn(w5.batch * w5.n_max, w5.vocab, device=dev, generator=gen) * 4).to(torch.bfloat16)
     aws = torch.zeros(P.lib().presto_accept_workspace(w5.batch, w5.n_max, w5.vocab), dtype=torch.uint8,
                       device=dev)
@@ -429,8 +440,11 @@ def measure_at_scale(P, sy, dev):
         lp, ids = torch.topk(lp, w.k, dim=1)
         lamw = torch.full((w.depth,), 0.2, dtype=torch.float32, device=dev)
         rootw = torch.zeros(w.batch, dtype=torch.int32, device=dev)
-        tr = P.presto_build_tree(ids.to(torch.int32).contiguous(), lp.contiguous(), None, lamw, rootw,
-                                 w.depth, w.k, w.budget)
+        ids32, lpc = ids.to(torch.int32).contiguous(), lp.contiguous()
+        tr = P.presto_build_tree(ids32, lpc, None, lamw, rootw, w.depth, w.k, w.budget)
+        us = time_us(lambda: P.presto_build_tree(ids32, lpc, None, lamw, rootw, w.depth, w.k, w.budget,
+                                                 out=tr))
+        out[f"tree_build_{w.name}"] = tree_latency(us, tr)
         bf = dict(device=dev, dtype=torch.bfloat16)
         q = torch.randn(w.batch, w.n_max, w.hq, w.head_dim, device=dev, generator=gen).to(torch.bfloat16)
         kc = torch.randn(total, w.hkv, w.head_dim, device=dev, generator=gen).to(torch.bfloat16)

@@ -72,6 +72,29 @@ __device__ __forceinline__ int row_count_greater(uint64_t key) {
     }
 }
 
+// One compare-exchange layer of a bitonic sort, descending: lane i pairs
+// with the lane that DPP control CTRL reads (i ^ m within the group), and
+// the lower lane of the pair (bit LOWBIT of i clear) keeps the larger key.
+template <int CTRL, int LOWBIT>
+__device__ __forceinline__ uint64_t bitonic_layer(uint64_t key, int lane) {
+    const uint64_t t = dpp_u64<CTRL>(0ull, key);
+    const bool lower = ((lane >> LOWBIT) & 1) == 0;
+    return (lower == (t > key)) ? t : key;
+}
+
+// Keys of lanes 0..7 of every row sorted descending in place (lane 0 of the
+// group holds the largest): blocks of 2, 4, 8, each merged by a flip
+// (i ^ (s - 1)) and half-cleaners (i ^ s/4, ..., i ^ 1).
+__device__ __forceinline__ uint64_t sort8_desc(uint64_t key, int lane) {
+    key = bitonic_layer<0xb1, 0>(key, lane);   // i ^ 1
+    key = bitonic_layer<0x1b, 1>(key, lane);   // i ^ 3 (quad_perm [3,2,1,0])
+    key = bitonic_layer<0xb1, 0>(key, lane);   // i ^ 1
+    key = bitonic_layer<0x141, 2>(key, lane);  // i ^ 7 (row_half_mirror)
+    key = bitonic_layer<0x4e, 1>(key, lane);   // i ^ 2
+    key = bitonic_layer<0xb1, 0>(key, lane);   // i ^ 1
+    return key;
+}
+
 // Same within this lane's quad (quad_perm rotations by 1, 2, 3).
 __device__ __forceinline__ int quad_count_greater(uint64_t key) {
     return (dpp_u64<0x39>(0ull, key) > key ? 1 : 0) + (dpp_u64<0x4e>(0ull, key) > key ? 1 : 0) +
@@ -306,20 +329,33 @@ __global__ __launch_bounds__(kWave) void tree_build_kernel(TreeArgs a) {
         const float sc = Sn + s;
         const uint32_t o = ord32(sc);  // nonzero for every non-NaN score
         const uint64_t key = in ? (((uint64_t)o << 8) | (uint64_t)(255 - lane)) : 0ull;
-        int pos;
-        if constexpr (KQ)
-            pos = quad_count_greater(key);
-        else
-            pos = row_count_greater<15>(key);
-        // the lanes that are not children all land on the first free position
-        // and write the end marker there
-        if (lane < k && live) {
-            s_kord[n * k + pos] = in ? o : 0u;
-            s_krank[n * k + pos] = (uint8_t)lane;
+        if (!KQ && k <= 8) {
+            // sorted in place: lane p holds the p-th child (key 0 past the
+            // last child, which writes the end marker)
+            const uint64_t sk = sort8_desc(key, lane);
+            if (lane < k && live) {
+                s_kord[n * k + lane] = (uint32_t)(sk >> 8);
+                s_krank[n * k + lane] = (uint8_t)(255 - (uint32_t)(sk & 255));
+            }
+            const uint64_t top = readlane_u64(sk, 0);
+            c_ord = (uint32_t)(top >> 8);
+            c_rank = c_ord ? 255 - (int)(top & 255) : 0;
+        } else {
+            int pos;
+            if constexpr (KQ)
+                pos = quad_count_greater(key);
+            else
+                pos = row_count_greater<15>(key);
+            // the lanes that are not children all land on the first free
+            // position and write the end marker there
+            if (lane < k && live) {
+                s_kord[n * k + pos] = in ? o : 0u;
+                s_krank[n * k + pos] = (uint8_t)lane;
+            }
+            const uint64_t first = __ballot(in && pos == 0);
+            c_rank = first ? __ffsll((unsigned long long)first) - 1 : 0;
+            c_ord = first ? (uint32_t)__builtin_amdgcn_readlane((int)o, c_rank) : 0u;
         }
-        const uint64_t first = __ballot(in && pos == 0);
-        c_rank = first ? __ffsll((unsigned long long)first) - 1 : 0;
-        c_ord = first ? (uint32_t)__builtin_amdgcn_readlane((int)o, c_rank) : 0u;
     };
 
     // Rank-path key (four 32-bit words, most significant first) of the child
@@ -459,8 +495,8 @@ __global__ __launch_bounds__(kWave) void tree_build_kernel(TreeArgs a) {
     __builtin_amdgcn_wave_barrier();
 
     // Output rows and ancestor masks, one node per lane: the mask of node n has
-    // the bits of n and of every node on its parent chain (SL words suffice:
-    // SL = ceil(N / 64) = W).
+    // the bits of n and of every node on its parent chain (SL >= W =
+    // ceil(N / 64) words suffice).
     const int64_t ob = (int64_t)b * N;
     const int root_tok = __builtin_amdgcn_readfirstlane(a.root_token[b]);
     for (int i = lane; i < N; i += kWave) {
@@ -592,7 +628,9 @@ presto_status launch_build_tree(const presto_tree_desc* desc, const int32_t* ids
     else { PRESTO_TREE2(S, 2); }
     if (SL <= 1) { PRESTO_TREE(1) }
     else if (SL <= 2) { PRESTO_TREE(2) }
+    else if (SL <= 3) { PRESTO_TREE(3) }
     else if (SL <= 4) { PRESTO_TREE(4) }
+    else if (SL <= 5) { PRESTO_TREE(5) }
     else { PRESTO_TREE(8) }
 #undef PRESTO_TREE
 #undef PRESTO_TREE2
