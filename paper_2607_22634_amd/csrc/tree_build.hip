@@ -120,6 +120,12 @@ __device__ __forceinline__ void stage_words(uint32_t* dst, const uint32_t* src, 
     }
 }
 
+// Number of frontier slots per lane a pop works on (a compile-time tag).
+template <int A>
+struct SlotCount {
+    static constexpr int value = A;
+};
+
 // One entry of a beam (beam search): score, candidate rank, rank of its
 // parent, and its place in rank-path order among the entries of its depth.
 struct BeamEntry {
@@ -390,17 +396,23 @@ __global__ __launch_bounds__(kWave) void tree_build_kernel(TreeArgs a) {
     }
     int fcount = 1, committed = 1;
 
-    while (committed - 1 < a.budget) {
+    // One pop: commit the best frontier entry and push its successors;
+    // false once the frontier is exhausted.  Slots fill lane-major (slot j
+    // holds entries 64 j .. 64 j + 63), so only the first A slots of every
+    // lane can be occupied, A = fcount / 64 + 1 counting the next fresh one:
+    // the per-slot work follows the frontier allocated so far.
+    auto pop = [&](auto act) -> bool {
+        constexpr int A = decltype(act)::value;
         uint32_t lm = 0u;
 #pragma unroll
-        for (int j = 0; j < SL; ++j) lm = max(lm, fS[j]);
+        for (int j = 0; j < A; ++j) lm = max(lm, fS[j]);
         const uint32_t M = wave_max_u32_dpp(lm);
-        if (M == 0u) break;  // frontier exhausted: the whole candidate tree is committed
+        if (M == 0u) return false;  // frontier exhausted: the whole candidate tree is committed
 
         // winner: the unique entry holding M, else the one with the smallest path key
         int cnt = 0, jsel = 0;
 #pragma unroll
-        for (int j = SL - 1; j >= 0; --j) {
+        for (int j = A - 1; j >= 0; --j) {
             const bool hit = fS[j] == M;
             cnt += hit ? 1 : 0;
             jsel = hit ? j : jsel;
@@ -412,7 +424,7 @@ __global__ __launch_bounds__(kWave) void tree_build_kernel(TreeArgs a) {
         } else {
             uint32_t bk[4] = {~0u, ~0u, ~0u, ~0u};
             int bj = 0;
-            for (int j = 0; j < SL; ++j) {
+            for (int j = 0; j < A; ++j) {
                 if (fS[j] == M) {
                     uint32_t kw[4];
                     child_key(fM[j] & 1023, (fM[j] >> 10) & 15, (fM[j] >> 14) & 63, kw);
@@ -437,7 +449,7 @@ __global__ __launch_bounds__(kWave) void tree_build_kernel(TreeArgs a) {
         }
         uint32_t lmeta = 0u;
 #pragma unroll
-        for (int j = 0; j < SL; ++j) lmeta = j == jsel ? fM[j] : lmeta;
+        for (int j = 0; j < A; ++j) lmeta = j == jsel ? fM[j] : lmeta;
         const uint32_t meta = (uint32_t)__builtin_amdgcn_readlane((int)lmeta, w);
         const int eslot = __builtin_amdgcn_readlane(jsel, w);
         const int p = meta & 1023, r = (meta >> 10) & 15, d = (meta >> 14) & 63, rp = (meta >> 20) & 15;
@@ -484,13 +496,25 @@ __global__ __launch_bounds__(kWave) void tree_build_kernel(TreeArgs a) {
         const bool second = yS != 0u;
         const int ylane = fcount & (kWave - 1), yslot = fcount >> 6;
 #pragma unroll
-        for (int j = 0; j < SL; ++j) {
+        for (int j = 0; j < A; ++j) {
             const bool px = lane == w && j == eslot;
             const bool py = second && lane == ylane && j == yslot;
             fS[j] = px ? xS : (py ? yS : fS[j]);
             fM[j] = px ? xM : (py ? yM : fM[j]);
         }
         if (second) ++fcount;
+        return true;
+    };
+    while (committed - 1 < a.budget) {
+        const int need = min((fcount >> 6) + 1, SL);
+        bool go;
+        if (need <= 1) go = pop(SlotCount<1>{});
+        else if (SL <= 2 || need <= 2) go = pop(SlotCount<(SL < 2 ? SL : 2)>{});
+        else if (SL <= 3 || need <= 3) go = pop(SlotCount<(SL < 3 ? SL : 3)>{});
+        else if (SL <= 4 || need <= 4) go = pop(SlotCount<(SL < 4 ? SL : 4)>{});
+        else if (SL <= 5 || need <= 5) go = pop(SlotCount<(SL < 5 ? SL : 5)>{});
+        else go = pop(SlotCount<SL>{});
+        if (!go) break;
     }
     __builtin_amdgcn_wave_barrier();
 
