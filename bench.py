@@ -522,6 +522,10 @@ def measure_next_rows(P, sy, w, R, reps, timed, topk_out, topk_ws, tree_out, rin
                                              w.k, w.budget, mode=P.PRESTO_TREE_BEAM,
                                              beam_width=10, out=beam_out), n, 0) * 1e3
     out["build_tree_beam10"] = {"us": round(us, 2)}
+    us = timed(lambda r: P.presto_build_tree(topk_out[0], topk_out[1], rho, lam, root, w.depth,
+                                             w.k, w.budget, mode=P.PRESTO_TREE_BEST_FIRST_ALG2,
+                                             out=beam_out), n, 0) * 1e3
+    out["build_tree_alg2"] = {"us": round(us, 2)}
 
     # bookkeeping after accept: commit the accepted path into a slotted cache
     L0 = R[0]["layers"][0]

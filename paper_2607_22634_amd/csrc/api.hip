@@ -30,7 +30,7 @@ presto_status launch_flatten_slots(int32_t batch, int32_t n_max, int32_t slots,
                                    const int32_t* n_nodes, const int32_t* root_pos,
                                    int32_t* pos_out, uint64_t* anc_out, int32_t* n_rows,
                                    hipStream_t stream);
-bool tree_build_fits(int D, int k, int branch, int N, int beam_width);
+bool tree_build_fits(int D, int k, int branch, int N, int beam_width, bool alg2);
 int tree_max_depth(int k);
 presto_status launch_build_tree(const presto_tree_desc* desc, const int32_t* ids,
                                 const float* logprob, const float* log_rho, const float* lambda,
@@ -233,9 +233,8 @@ presto_status presto_build_tree(const presto_tree_desc* desc, const int32_t* ids
     REQUIRE(d.depth <= tree_max_depth(d.k),
             "presto_build_tree: depth %d exceeds the rank-path key (at most %d for k=%d)", d.depth,
             tree_max_depth(d.k), d.k);
-    if (d.mode == PRESTO_TREE_BEST_FIRST_ALG2)
-        return set_error(PRESTO_ERR_UNSUPPORTED, "presto_build_tree: mode %d not built", d.mode);
-    REQUIRE(d.mode == PRESTO_TREE_BEST_FIRST || d.mode == PRESTO_TREE_BEAM,
+    REQUIRE(d.mode == PRESTO_TREE_BEST_FIRST || d.mode == PRESTO_TREE_BEST_FIRST_ALG2 ||
+                d.mode == PRESTO_TREE_BEAM,
             "presto_build_tree: unknown mode %d", d.mode);
     const int beam_width = d.mode == PRESTO_TREE_BEAM ? d.beam_width : 0;
     if (d.mode == PRESTO_TREE_BEAM) {
@@ -244,7 +243,8 @@ presto_status presto_build_tree(const presto_tree_desc* desc, const int32_t* ids
         REQUIRE(d.beam_width * d.k <= 256, "presto_build_tree: beam_width * k = %d exceeds 256",
                 d.beam_width * d.k);
     }
-    if (!tree_build_fits(d.depth, d.k, d.branch, d.budget + 1, beam_width))
+    if (!tree_build_fits(d.depth, d.k, d.branch, d.budget + 1, beam_width,
+                         d.mode == PRESTO_TREE_BEST_FIRST_ALG2))
         return set_error(PRESTO_ERR_UNSUPPORTED, "presto_build_tree: tables exceed 64 KiB of LDS");
     if (d.batch == 0) return PRESTO_OK;
     REQUIRE(ids && logprob && lambda && root_token && n_nodes && parent && token && depth_out &&

@@ -51,6 +51,8 @@ struct TreeArgs {
     int32_t beam_width;  // beam search only
     // LDS byte offsets
     int o_lp, o_ids, o_kord, o_krank, o_rec, o_ktab, o_beam, o_bidx, o_rho;
+    // literal Alg. 2 only: T (capacity budget + branch - 1) in LDS
+    int o_tmeta, o_tS, o_tkey, o_tplace;
 };
 
 // Frontier metadata in one word: parent node (10 bits), candidate rank (4),
@@ -557,6 +559,243 @@ __global__ __launch_bounds__(kWave) void tree_build_kernel(TreeArgs a) {
     if (lane == 0) a.n_nodes[b] = committed;
 }
 
+
+// Literal Alg. 2 (Sec. 4.2): T grows by whole expansions.  The root is
+// expanded first; every later pop takes the best node of T not yet expanded
+// (total order: S desc, rank path asc) and appends its top-`branch`
+// children to T.  The search stops once T holds `budget` non-root nodes (the
+// last expansion may overshoot by branch - 1) or nothing is left to expand,
+// and the tree is TopB(T): the `budget` best nodes of T, in the total order,
+// after the root.  One wavefront per sequence: T lives in LDS (per node the
+// parent, rank and depth in one word, S, and the rank-path key, built from
+// the parent's key when the node is appended); node e of T is "not yet
+// expanded" while slot e / 64 of lane e % 64 holds ord(S) (0 once expanded).
+// TopB(T) places every node by counting the nodes before it.
+template <int SLT, int RHO>
+__global__ __launch_bounds__(kWave) void tree_alg2_kernel(TreeArgs a) {
+    extern __shared__ __align__(16) char lds[];
+    const int lane = lane_id();
+    const int b = blockIdx.x;
+    const int D = a.D, k = a.k, N = a.N, W = a.W, wbits = a.wbits, per_word = a.per_word;
+    const int branch = a.branch, budget = a.budget;
+    float* s_lp = reinterpret_cast<float*>(lds + a.o_lp);
+    int32_t* s_ids = reinterpret_cast<int32_t*>(lds + a.o_ids);
+    float* s_rho = reinterpret_cast<float*>(lds + a.o_rho);
+    // T node c: (parent + 1, 0 for the root) | rank << 10 | depth << 14
+    uint32_t* s_tmeta = reinterpret_cast<uint32_t*>(lds + a.o_tmeta);
+    float* s_tS = reinterpret_cast<float*>(lds + a.o_tS);
+    uint4* s_tkey = reinterpret_cast<uint4*>(lds + a.o_tkey);  // x: most significant word
+    int32_t* s_tplace = reinterpret_cast<int32_t*>(lds + a.o_tplace);
+    const int rho_n = D * k * k * k;
+    const float* g_rho = RHO ? a.log_rho + (int64_t)b * rho_n : nullptr;
+
+    const int64_t tb = (int64_t)b * D * k;
+    stage_words(reinterpret_cast<uint32_t*>(s_lp), reinterpret_cast<const uint32_t*>(a.logprob + tb),
+                D * k, lane);
+    stage_words(reinterpret_cast<uint32_t*>(s_ids), reinterpret_cast<const uint32_t*>(a.ids + tb), D * k,
+                lane);
+    if constexpr (RHO == 1)
+        stage_words(reinterpret_cast<uint32_t*>(s_rho), reinterpret_cast<const uint32_t*>(g_rho), rho_n,
+                    lane);
+    const float lam_lane = lane < D ? a.lambda[(int64_t)b * a.lambda_stride + lane] : 0.f;
+    __builtin_amdgcn_wave_barrier();
+
+    // Appends the top-`branch` children (by s desc, rank asc) of the node v
+    // (T index, -1 for the root; depth d < D, own rank rn, parent's rank rp,
+    // score Sv, key kv) to T at index nT.  Lane r scores candidate r.
+    auto expand = [&](int v, int d, int rn, int rp, float Sv, uint4 kv, int nT) {
+        const int ctx2 = d >= 2 ? rp : 0;
+        const int ctx1 = d >= 1 ? rn : 0;
+        const int rl = min(lane, k - 1);
+        float s = s_lp[d * k + rl];
+        if constexpr (RHO != 0) {
+            const float lam_d = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(lam_lane), d));
+            const int ri = ((d * k + ctx2) * k + ctx1) * k + rl;
+            const float lr = RHO == 1 ? s_rho[ri] : g_rho[ri];
+            const float t = lam_d * lr;
+            s = s + t;
+        }
+        s = (s == s && lane < k) ? s : -INFINITY;
+        int sel = 0;
+        for (int j = 0; j < k; ++j) {
+            const float sj = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(s), j));
+            sel += (sj > s || (sj == s && j < lane)) ? 1 : 0;
+        }
+        if (lane < k && sel < branch) {
+            const int c = nT + sel;
+            s_tmeta[c] = (uint32_t)(v + 1) | ((uint32_t)lane << 10) | ((uint32_t)(d + 1) << 14);
+            s_tS[c] = Sv + s;
+            const int wi = d / per_word, sh = 32 - (d % per_word + 1) * wbits;
+            const uint32_t dig = (uint32_t)(lane + 1) << sh;
+            s_tkey[c] = make_uint4(kv.x | (wi == 0 ? dig : 0u), kv.y | (wi == 1 ? dig : 0u),
+                                   kv.z | (wi == 2 ? dig : 0u), kv.w | (wi == 3 ? dig : 0u));
+        }
+        __builtin_amdgcn_wave_barrier();
+    };
+    // marks T nodes n0 .. n0 + cnt - 1 as not yet expanded
+    uint32_t fO[SLT];
+#pragma unroll
+    for (int j = 0; j < SLT; ++j) fO[j] = 0u;
+    auto open = [&](int n0, int cnt) {
+#pragma unroll
+        for (int j = 0; j < SLT; ++j) {
+            const int e = j * kWave + lane;
+            if (e >= n0 && e < n0 + cnt) fO[j] = ord32(s_tS[e]);
+        }
+    };
+    auto key_less = [](uint4 x, uint4 y) {
+        return x.x != y.x ? x.x < y.x : (x.y != y.y ? x.y < y.y : (x.z != y.z ? x.z < y.z : x.w < y.w));
+    };
+
+    expand(-1, 0, 0, 0, 0.f, make_uint4(0u, 0u, 0u, 0u), 0);  // depth >= 1: the root has children
+    open(0, branch);
+    int nT = branch;
+    while (nT < budget) {
+        uint32_t lm = 0u;
+#pragma unroll
+        for (int j = 0; j < SLT; ++j) lm = max(lm, fO[j]);
+        const uint32_t M = wave_max_u32_dpp(lm);
+        if (M == 0u) break;  // every node of T expanded
+        int cnt = 0, jsel = 0;
+#pragma unroll
+        for (int j = SLT - 1; j >= 0; --j) {
+            const bool hit = fO[j] == M;
+            cnt += hit ? 1 : 0;
+            jsel = hit ? j : jsel;
+        }
+        const uint64_t any = __ballot(cnt > 0);
+        int w;
+        if (__popcll(any) == 1 && __ballot(cnt > 1) == 0ull) {
+            w = __ffsll((unsigned long long)any) - 1;
+        } else {
+            // several nodes share the best S: the smallest rank-path key wins
+            uint4 bk = make_uint4(~0u, ~0u, ~0u, ~0u);
+            int bj = 0;
+            for (int j = 0; j < SLT; ++j) {
+                if (fO[j] == M) {
+                    const uint4 kj = s_tkey[j * kWave + lane];
+                    if (key_less(kj, bk)) {
+                        bk = kj;
+                        bj = j;
+                    }
+                }
+            }
+            bool t = cnt > 0;
+            uint32_t m;
+            m = wave_min_u32_dpp(t ? bk.x : ~0u); t = t && bk.x == m;
+            m = wave_min_u32_dpp(t ? bk.y : ~0u); t = t && bk.y == m;
+            m = wave_min_u32_dpp(t ? bk.z : ~0u); t = t && bk.z == m;
+            m = wave_min_u32_dpp(t ? bk.w : ~0u); t = t && bk.w == m;
+            w = __ffsll((unsigned long long)__ballot(t)) - 1;
+            jsel = bj;
+        }
+        const int es = __builtin_amdgcn_readlane(jsel, w);
+        const int e = es * kWave + w;
+#pragma unroll
+        for (int j = 0; j < SLT; ++j) fO[j] = (lane == w && j == es) ? 0u : fO[j];
+        const uint32_t meta = s_tmeta[e];
+        const int d = (meta >> 14) & 63;
+        if (d < D) {
+            const int pv = (int)(meta & 1023) - 1;
+            const int rp = pv >= 0 ? (int)((s_tmeta[pv] >> 10) & 15) : 0;
+            expand(e, d, (meta >> 10) & 15, rp, s_tS[e], s_tkey[e], nT);
+            open(nT, branch);
+            nT += branch;
+        }
+    }
+
+    // TopB(T): the place of node i in the total order is the number of nodes
+    // of T before it (S larger, or S equal and rank-path key smaller)
+    const int keep = min(nT, budget);
+    uint32_t oT[SLT];
+#pragma unroll
+    for (int q = 0; q < SLT; ++q) {
+        const int i = q * kWave + lane;
+        oT[q] = i < nT ? ord32(s_tS[i]) : 0u;
+    }
+    int place[SLT];
+#pragma unroll
+    for (int q = 0; q < SLT; ++q) place[q] = 0;
+#pragma unroll
+    for (int sj = 0; sj < SLT; ++sj) {
+        for (int l = 0; l < kWave; ++l) {
+            const int j = sj * kWave + l;
+            if (j >= nT) break;
+            const uint32_t oj = (uint32_t)__builtin_amdgcn_readlane((int)oT[sj], l);
+            bool tie = false;
+#pragma unroll
+            for (int q = 0; q < SLT; ++q) {
+                place[q] += oj > oT[q] ? 1 : 0;
+                tie = tie || (oj == oT[q] && q * kWave + lane != j && q * kWave + lane < nT);
+            }
+            if (__ballot(tie)) {
+                const uint4 kj = s_tkey[j];
+#pragma unroll
+                for (int q = 0; q < SLT; ++q) {
+                    const int i = q * kWave + lane;
+                    if (oj == oT[q] && i != j && i < nT && key_less(kj, s_tkey[i])) ++place[q];
+                }
+            }
+        }
+    }
+#pragma unroll
+    for (int q = 0; q < SLT; ++q) {
+        const int i = q * kWave + lane;
+        if (i < nT) s_tplace[i] = place[q];
+    }
+    __builtin_amdgcn_wave_barrier();
+
+    // output: row 0 the root, rows 1 .. keep the kept nodes in order, then padding
+    const int64_t ob = (int64_t)b * N;
+    constexpr int SLW = SLT + 1;  // mask words: N = budget + 1 <= 64 * SLT + 1
+    for (int i = lane; i < nT; i += kWave) {
+        const int pl = s_tplace[i];
+        if (pl >= keep) continue;
+        const int o = pl + 1;
+        const uint32_t meta = s_tmeta[i];
+        const int pv = (int)(meta & 1023) - 1, r = (meta >> 10) & 15, d = (meta >> 14) & 63;
+        int po = 0;
+        if (pv >= 0) po = s_tplace[pv] < keep ? s_tplace[pv] + 1 : -2;
+        a.parent[ob + o] = po;
+        a.token[ob + o] = s_ids[(d - 1) * k + r];
+        a.depth[ob + o] = d;
+        a.rank[ob + o] = r;
+        a.score[ob + o] = s_tS[i];
+        // ancestor bits: this node, then the parent chain until the root
+        // (or a parent that TopB(T) dropped, which ends the chain)
+        uint64_t words[SLW];
+#pragma unroll
+        for (int q = 0; q < SLW; ++q) words[q] = 0ull;
+        int x = i, xo = o;
+        while (true) {
+#pragma unroll
+            for (int q = 0; q < SLW; ++q) words[q] |= q == (xo >> 6) ? 1ull << (xo & 63) : 0ull;
+            const int xv = (int)(s_tmeta[x] & 1023) - 1;
+            if (xv < 0) {
+                words[0] |= 1ull;  // the root
+                break;
+            }
+            if (s_tplace[xv] >= keep) break;
+            x = xv;
+            xo = s_tplace[xv] + 1;
+        }
+#pragma unroll
+        for (int q = 0; q < SLW; ++q)
+            if (q < W) a.anc[(ob + o) * W + q] = words[q];
+    }
+    const int root_tok = __builtin_amdgcn_readfirstlane(a.root_token[b]);
+    for (int i = lane; i < N; i += kWave) {
+        if (i != 0 && i <= keep) continue;
+        const bool root = i == 0;
+        a.parent[ob + i] = -1;
+        a.token[ob + i] = root ? root_tok : -1;
+        a.depth[ob + i] = root ? 0 : -1;
+        a.rank[ob + i] = -1;
+        a.score[ob + i] = root ? 0.f : -INFINITY;
+        for (int q = 0; q < W; ++q) a.anc[(ob + i) * W + q] = (root && q == 0) ? 1ull : 0ull;
+    }
+    if (lane == 0) a.n_nodes[b] = keep + 1;
+}
 }  // namespace presto
 
 namespace presto_host {
@@ -599,8 +838,31 @@ int tree_key_bits(int k) {
 // straddle a word).
 int tree_max_depth(int k) { return 4 * (32 / tree_key_bits(k)); }
 
-bool tree_build_fits(int D, int k, int branch, int N, int beam_width) {
-    (void)branch;
+// Literal Alg. 2: candidate table, then T (capacity budget + branch - 1:
+// the last expansion may overshoot the budget), then the lattice.
+struct Alg2Layout {
+    int cap, total_no_rho, total_with_rho;
+    int o_lp, o_ids, o_tmeta, o_tS, o_tkey, o_tplace, o_rho;
+};
+
+static Alg2Layout alg2_layout(int D, int k, int branch, int budget) {
+    Alg2Layout L;
+    L.cap = budget + branch - 1;
+    int off = 0;
+    L.o_lp = off; off = align16(off + D * k * 4);
+    L.o_ids = off; off = align16(off + D * k * 4);
+    L.o_tmeta = off; off = align16(off + L.cap * 4);
+    L.o_tS = off; off = align16(off + L.cap * 4);
+    L.o_tkey = off; off = align16(off + L.cap * 16);
+    L.o_tplace = off; off = align16(off + L.cap * 4);
+    L.total_no_rho = off;
+    L.o_rho = off;
+    L.total_with_rho = align16(off + D * k * k * k * 4);
+    return L;
+}
+
+bool tree_build_fits(int D, int k, int branch, int N, int beam_width, bool alg2) {
+    if (alg2) return alg2_layout(D, k, branch, N - 1).total_no_rho <= kTreeLdsBudget;
     return tree_layout(D, k, N, beam_width).total_no_rho <= kTreeLdsBudget;
 }
 
@@ -631,6 +893,26 @@ presto_status launch_build_tree(const presto_tree_desc* desc, const int32_t* ids
     a.rank = rank;
     a.score = score;
     a.anc = anc;
+    if (desc->mode == PRESTO_TREE_BEST_FIRST_ALG2) {
+        const Alg2Layout L = alg2_layout(a.D, a.k, a.branch, a.budget);
+        a.beam_width = 0;
+        a.o_lp = L.o_lp; a.o_ids = L.o_ids; a.o_rho = L.o_rho;
+        a.o_tmeta = L.o_tmeta; a.o_tS = L.o_tS; a.o_tkey = L.o_tkey; a.o_tplace = L.o_tplace;
+        a.rho_in_lds = log_rho != nullptr && L.total_with_rho <= kTreeLdsBudget;
+        const int lds = a.rho_in_lds ? L.total_with_rho : L.total_no_rho;
+        const int slt = (L.cap + kWave - 1) / kWave;
+        const int rho_mode = log_rho == nullptr ? 0 : (a.rho_in_lds ? 1 : 2);
+#define PRESTO_ALG2(S)                                                                              \
+    if (rho_mode == 0) tree_alg2_kernel<S, 0><<<desc->batch, kWave, lds, stream>>>(a);              \
+    else if (rho_mode == 1) tree_alg2_kernel<S, 1><<<desc->batch, kWave, lds, stream>>>(a);         \
+    else tree_alg2_kernel<S, 2><<<desc->batch, kWave, lds, stream>>>(a)
+        if (slt <= 1) { PRESTO_ALG2(1); }
+        else if (slt <= 2) { PRESTO_ALG2(2); }
+        else if (slt <= 4) { PRESTO_ALG2(4); }
+        else { PRESTO_ALG2(9); }
+#undef PRESTO_ALG2
+        return check_launch("tree_alg2_kernel");
+    }
     const bool beam = desc->mode == PRESTO_TREE_BEAM;
     a.beam_width = beam ? desc->beam_width : 0;
     const TreeLayout L = tree_layout(a.D, a.k, a.N, a.beam_width);

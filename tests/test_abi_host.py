@@ -95,10 +95,12 @@ def test_build_tree_rejects_bad_descriptor(field, value):
     assert st == P.PRESTO_ERR_INVALID_ARG
 
 
-def test_build_tree_unbuilt_modes_are_unsupported():
-    d = P.TreeDesc(1, 4, 4, 4, 8, P.PRESTO_TREE_BEST_FIRST_ALG2)
-    st, _ = _err(P.lib().presto_build_tree(ctypes.byref(d), *([None] * 13), 0, None))
-    assert st == P.PRESTO_ERR_UNSUPPORTED
+def test_build_tree_accepts_every_mode():
+    # batch 0: validated, nothing launched (no device needed)
+    for mode in (P.PRESTO_TREE_BEST_FIRST, P.PRESTO_TREE_BEST_FIRST_ALG2, P.PRESTO_TREE_BEAM):
+        d = P.TreeDesc(0, 4, 4, 4, 8, mode, 4)
+        st, msg = _err(P.lib().presto_build_tree(ctypes.byref(d), *([None] * 13), 0, None))
+        assert st == P.PRESTO_OK, msg
 
 
 @pytest.mark.parametrize("width,k", [(0, 4), (65, 1), (33, 8)])

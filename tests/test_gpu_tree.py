@@ -16,15 +16,17 @@ pytestmark = pytest.mark.gpu
 KEYS = ("n_nodes", "parent", "token", "depth", "rank", "score", "anc")
 
 
-def _gpu_and_oracle(ids, lp, rho, lam, root, D, k, B, branch=None, beam_width=0):
+def _gpu_and_oracle(ids, lp, rho, lam, root, D, k, B, branch=None, beam_width=0, alg2=False):
     mode = P.PRESTO_TREE_BEAM if beam_width else P.PRESTO_TREE_BEST_FIRST
+    omode = oracle.BEAM if beam_width else oracle.BEST_FIRST
+    if alg2:
+        mode, omode = P.PRESTO_TREE_BEST_FIRST_ALG2, oracle.BEST_FIRST_ALG2
     g = P.presto_build_tree(to_dev(ids), to_dev(lp), None if rho is None else to_dev(rho),
                             to_dev(lam), to_dev(root), D, k, B, branch=branch, mode=mode,
                             beam_width=beam_width)
     torch.cuda.synchronize()
     g = tree_to_host(g)
-    o = oracle.build_tree(ids, lp, rho, lam, root, D, k, B, branch=branch,
-                          mode=oracle.BEAM if beam_width else oracle.BEST_FIRST,
+    o = oracle.build_tree(ids, lp, rho, lam, root, D, k, B, branch=branch, mode=omode,
                           beam_width=beam_width)
     return g, o
 
@@ -110,6 +112,32 @@ def test_beam_tree_matches_oracle_random(D, k, branch, B, W, quant):
         g, o = _gpu_and_oracle(ids, lp, rho, lam, root, D, k, B, branch=branch, beam_width=W)
         _assert_same(g, o)
 
+
+
+@pytest.mark.parametrize("cfg", [1, 2, 3, 4, 5])
+def test_alg2_tree_matches_oracle_on_workload(cfg):
+    """Literal Alg. 2 (whole expansions, then TopB(T)) at the workloads' shapes."""
+    w, rin = round_data(cfg)
+    print(f"alg2 cfg={cfg}", flush=True)
+    ids, lp = oracle_candidates(cfg)
+    g, o = _gpu_and_oracle(ids, lp, rin["rho"], rin["lam"], rin["root_token"], w.depth, w.k,
+                           w.budget, alg2=True)
+    _assert_same(g, o)
+
+
+@pytest.mark.parametrize("D,k,branch,B", [(1, 1, 1, 1), (3, 2, 2, 4), (4, 3, 2, 40), (5, 3, 3, 200),
+                                          (6, 2, 1, 9), (16, 8, 8, 256), (32, 4, 3, 128),
+                                          (8, 16, 16, 255), (2, 16, 5, 63), (12, 5, 5, 130),
+                                          (10, 4, 4, 511), (2, 3, 3, 500), (7, 16, 16, 511)])
+@pytest.mark.parametrize("quant", [False, True])
+def test_alg2_tree_matches_oracle_random(D, k, branch, B, quant):
+    """Random tables, quantised ones full of ties; (2, 3, 3, 500): the whole
+    candidate tree (12 nodes) is smaller than the budget."""
+    ids, lp, R, root = _random_batch([D, k, B, int(quant), 2], 12, D, k, quant)
+    for lam_v, rho in ((0.2, R), (1.0, None)):
+        lam = np.full(D, lam_v, np.float32)
+        g, o = _gpu_and_oracle(ids, lp, rho, lam, root, D, k, B, branch=branch, alg2=True)
+        _assert_same(g, o)
 
 
 @pytest.mark.parametrize("cfg,beam_width", [(2, 0), (3, 0), (4, 0), (3, 4)])
