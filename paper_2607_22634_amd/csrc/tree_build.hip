@@ -636,7 +636,7 @@ __global__ __launch_bounds__(kWave) void tree_alg2_kernel(TreeArgs a) {
     uint32_t fO[SLT];
 #pragma unroll
     for (int j = 0; j < SLT; ++j) fO[j] = 0u;
-    auto open = [&](int n0, int cnt) {
+    auto mark_open = [&](int n0, int cnt) {
 #pragma unroll
         for (int j = 0; j < SLT; ++j) {
             const int e = j * kWave + lane;
@@ -648,7 +648,7 @@ __global__ __launch_bounds__(kWave) void tree_alg2_kernel(TreeArgs a) {
     };
 
     expand(-1, 0, 0, 0, 0.f, make_uint4(0u, 0u, 0u, 0u), 0);  // depth >= 1: the root has children
-    open(0, branch);
+    mark_open(0, branch);
     int nT = branch;
     while (nT < budget) {
         uint32_t lm = 0u;
@@ -699,7 +699,7 @@ __global__ __launch_bounds__(kWave) void tree_alg2_kernel(TreeArgs a) {
             const int pv = (int)(meta & 1023) - 1;
             const int rp = pv >= 0 ? (int)((s_tmeta[pv] >> 10) & 15) : 0;
             expand(e, d, (meta >> 10) & 15, rp, s_tS[e], s_tkey[e], nT);
-            open(nT, branch);
+            mark_open(nT, branch);
             nT += branch;
         }
     }
