@@ -103,6 +103,23 @@ __device__ __forceinline__ int quad_count_greater(uint64_t key) {
            (dpp_u64<0x93>(0ull, key) > key ? 1 : 0);
 }
 
+// Loads up to U words per lane of src[base ..] (batches of 64 words while
+// fewer than n; indices clamped, so every load is unconditional) into r.
+template <int U>
+__device__ __forceinline__ void load_words(uint32_t (&r)[U], const uint32_t* src, int n, int base, int lane) {
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+        if (base + u * kWave < n) r[u] = src[min(base + u * kWave + lane, n - 1)];
+}
+template <int U>
+__device__ __forceinline__ void store_words(uint32_t* dst, const uint32_t (&r)[U], int n, int base, int lane) {
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+        const int i = base + u * kWave + lane;
+        if (i < n) dst[i] = r[u];
+    }
+}
+
 // Copies n 32-bit words from global memory to LDS with one wave, 16 loads
 // in flight per lane before the first store.
 __device__ __forceinline__ void stage_words(uint32_t* dst, const uint32_t* src, int n, int lane) {
@@ -157,18 +174,31 @@ __global__ __launch_bounds__(kWave) void tree_build_kernel(TreeArgs a) {
     const int rho_n = D * k * k * k;
     const float* g_rho = RHO ? a.log_rho + (int64_t)b * rho_n : nullptr;
 
-    // stage the candidate table of this sequence (and the lattice when it
-    // fits), with many loads in flight per lane
-    const int64_t tb = (int64_t)b * D * k;
-    stage_words(reinterpret_cast<uint32_t*>(s_lp), reinterpret_cast<const uint32_t*>(a.logprob + tb),
-                D * k, lane);
-    stage_words(reinterpret_cast<uint32_t*>(s_ids), reinterpret_cast<const uint32_t*>(a.ids + tb), D * k,
-                lane);
-    if constexpr (RHO == 1)
-        stage_words(reinterpret_cast<uint32_t*>(s_rho), reinterpret_cast<const uint32_t*>(g_rho), rho_n,
-                    lane);
     const float lam_lane =
         lane < D ? a.lambda[(int64_t)b * a.lambda_stride + lane] : 0.f;  // lambda_d held by lane d
+    // stage the candidate table of this sequence (and the lattice when it
+    // fits): the table, lambda and the lattice's first 1024 words are all
+    // requested before the first store, so the common sizes cost one memory
+    // round trip
+    const int64_t tb = (int64_t)b * D * k;
+    {
+        const uint32_t* g_lp = reinterpret_cast<const uint32_t*>(a.logprob + tb);
+        const uint32_t* g_ids = reinterpret_cast<const uint32_t*>(a.ids + tb);
+        constexpr int UT = 8;  // D * k <= 512 words
+        uint32_t r_lp[UT], r_ids[UT], r_rho[16];
+        load_words(r_lp, g_lp, D * k, 0, lane);
+        load_words(r_ids, g_ids, D * k, 0, lane);
+        if constexpr (RHO == 1) load_words(r_rho, reinterpret_cast<const uint32_t*>(g_rho), rho_n, 0, lane);
+        store_words(reinterpret_cast<uint32_t*>(s_lp), r_lp, D * k, 0, lane);
+        store_words(reinterpret_cast<uint32_t*>(s_ids), r_ids, D * k, 0, lane);
+        if constexpr (RHO == 1) {
+            store_words(reinterpret_cast<uint32_t*>(s_rho), r_rho, rho_n, 0, lane);
+            if (rho_n > 16 * kWave)
+                stage_words(reinterpret_cast<uint32_t*>(s_rho) + 16 * kWave,
+                            reinterpret_cast<const uint32_t*>(g_rho) + 16 * kWave, rho_n - 16 * kWave,
+                            lane);
+        }
+    }
     __builtin_amdgcn_wave_barrier();
 
     // token score of candidate r at drafter row `row` under the trigram
