@@ -294,20 +294,34 @@ __global__ __launch_bounds__(kTopkWavesPerBlock * kWave) void topk_merge_kernel(
             kr[i] = idx < nk ? keys[idx] : 0ull;
         }
     }
+    // the chunks' (max, sum) pairs: the first kMsRegs per lane are read once
+    // into registers (every row up to 256 chunks), the rest read again below
+    constexpr int kMsRegs = 4;
+    float2 mr[kMsRegs];
+#pragma unroll
+    for (int i = 0; i < kMsRegs; ++i) {
+        const int c = i * kWave + lane;
+        mr[i] = c < chunks ? ms[c] : make_float2(-INFINITY, 0.f);
+    }
     float m = -INFINITY;
-    for (int c = lane; c < chunks; c += kWave) m = fmaxf(m, ms[c].x);
+#pragma unroll
+    for (int i = 0; i < kMsRegs; ++i) m = fmaxf(m, mr[i].x);
+    for (int c = kMsRegs * kWave + lane; c < chunks; c += kWave) m = fmaxf(m, ms[c].x);
     const float M = wave_max_f32_dpp(m);
     float s = 0.f, hx = 0.f;
-    if (M != -INFINITY)
-        for (int c = lane; c < chunks; c += kWave) {
-            const float2 p = ms[c];
-            if (p.x != -INFINITY) {
-                const float w = __expf(p.x - M);
-                s += p.y * w;
-                // chunk sums shift to the row max: (z - M) = (z - m_c) + (m_c - M)
-                if constexpr (ENT) hx += w * (part_h[row * chunks + c] + (p.x - M) * p.y);
-            }
+    // chunk sums shift to the row max: (z - M) = (z - m_c) + (m_c - M)
+    auto add_chunk = [&](float2 p, int c) {
+        if (p.x != -INFINITY) {
+            const float w = __expf(p.x - M);
+            s += p.y * w;
+            if constexpr (ENT) hx += w * (part_h[row * chunks + c] + (p.x - M) * p.y);
         }
+    };
+    if (M != -INFINITY) {
+#pragma unroll
+        for (int i = 0; i < kMsRegs; ++i) add_chunk(mr[i], i * kWave + lane);
+        for (int c = kMsRegs * kWave + lane; c < chunks; c += kWave) add_chunk(ms[c], c);
+    }
     const float S = wave_sum_f32_dpp(s);
     const float logS = __logf(S);
     const float L = (M == -INFINITY) ? -INFINITY : M + logS;
