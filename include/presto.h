@@ -50,7 +50,7 @@ extern "C" {
 typedef enum {
     PRESTO_OK = 0,
     PRESTO_ERR_INVALID_ARG = -1, /* rejected on the host; nothing launched          */
-    PRESTO_ERR_UNSUPPORTED = -2, /* valid request this build does not implement     */
+    PRESTO_ERR_UNSUPPORTED = -2, /* valid request the library does not implement   */
     PRESTO_ERR_WORKSPACE = -3,   /* workspace missing or smaller than *_workspace() */
     PRESTO_ERR_HIP = -4          /* HIP runtime error; see presto_last_error()      */
 } presto_status;
