@@ -364,7 +364,8 @@ def measure_at_scale(P, sy, dev):
     contexts, HBM-bound) and workload 4 (4 x 32768 keys, MFMA-bound).  Inputs
     are N(0, 1) device draws of those shapes (scaled like the workloads'
     logits); trees come from the GPU stages on them, and the tree build is
-    timed at workloads 3, 4 and 5 (latency-bound: one wave per sequence).
+    timed at workloads 3, 4 and 5 (latency-bound: one wave per sequence),
+    best-first and beam search (W = 10).
     Timing only: parity at these shapes is covered by the tests."""
     import torch
 
@@ -421,6 +422,10 @@ def measure_at_scale(P, sy, dev):
     us = time_us(lambda: P.presto_build_tree(ids32, lpc, None, lam, root, w5.depth, w5.k, w5.budget,
                                              out=tree))
     out[f"tree_build_{w5.name}"] = tree_latency(us, tree)
+    beam = {k: torch.empty_like(v) for k, v in tree.items()}
+    us = time_us(lambda: P.presto_build_tree(ids32, lpc, None, lam, root, w5.depth, w5.k, w5.budget,
+                                             mode=P.PRESTO_TREE_BEAM, beam_width=10, out=beam))
+    out[f"tree_build_beam10_{w5.name}"] = tree_latency(us, beam)
     target = (torch.randn(w5.batch * w5.n_max, w5.vocab, device=dev, generator=gen) * 4).to(torch.bfloat16)
     aws = torch.zeros(P.lib().presto_accept_workspace(w5.batch, w5.n_max, w5.vocab), dtype=torch.uint8,
                       device=dev)
@@ -445,6 +450,10 @@ def measure_at_scale(P, sy, dev):
         us = time_us(lambda: P.presto_build_tree(ids32, lpc, None, lamw, rootw, w.depth, w.k, w.budget,
                                                  out=tr))
         out[f"tree_build_{w.name}"] = tree_latency(us, tr)
+        beam = {k: torch.empty_like(v) for k, v in tr.items()}
+        us = time_us(lambda: P.presto_build_tree(ids32, lpc, None, lamw, rootw, w.depth, w.k, w.budget,
+                                                 mode=P.PRESTO_TREE_BEAM, beam_width=10, out=beam))
+        out[f"tree_build_beam10_{w.name}"] = tree_latency(us, beam)
         bf = dict(device=dev, dtype=torch.bfloat16)
         q = torch.randn(w.batch, w.n_max, w.hq, w.head_dim, device=dev, generator=gen).to(torch.bfloat16)
         kc = torch.randn(total, w.hkv, w.head_dim, device=dev, generator=gen).to(torch.bfloat16)
