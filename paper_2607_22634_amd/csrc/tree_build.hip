@@ -236,14 +236,18 @@ __global__ __launch_bounds__(kWave) void tree_build_kernel(TreeArgs a) {
         __builtin_amdgcn_wave_barrier();
         int nb = 1, cur = 0, nT = 0;
         constexpr int CS = kBeamCandSlots;
-        for (int d = 1; d <= D && nT < a.budget && nb > 0; ++d) {
+        // One depth: candidates c = q * 64 + lane of the nb beam entries
+        // (nb * k of them, in ceil(nb * k / 64) <= CS slots per lane: the
+        // per-slot work only covers the slots that hold candidates).
+        auto beam_depth = [&](auto act, int d) {
+            constexpr int A = decltype(act)::value;
             const int row = d - 1;  // drafter row of depth d
             const BeamEntry* bc = s_beam + cur * Wb;
             uint64_t key[CS];
             int cpb[CS], cr[CS];
             int count = 0;
 #pragma unroll
-            for (int q = 0; q < CS; ++q) {
+            for (int q = 0; q < A; ++q) {
                 const int ci = q * kWave + lane;
                 const bool valid = ci < nb * k;
                 const int pb = valid ? ci / k : 0, r = valid ? ci % k : 0;
@@ -275,11 +279,11 @@ __global__ __launch_bounds__(kWave) void tree_build_kernel(TreeArgs a) {
             for (int j = 0; j < nn; ++j) {
                 uint64_t lm = 0ull;
 #pragma unroll
-                for (int q = 0; q < CS; ++q) lm = key[q] > lm ? key[q] : lm;
+                for (int q = 0; q < A; ++q) lm = key[q] > lm ? key[q] : lm;
                 const uint64_t m = wave_max_u64_dpp(lm);
                 int wq = 0, wl = 0;
 #pragma unroll
-                for (int q = CS - 1; q >= 0; --q) {
+                for (int q = A - 1; q >= 0; --q) {
                     const uint64_t hit = __ballot(key[q] == m);
                     if (hit) {
                         wq = q;
@@ -288,7 +292,7 @@ __global__ __launch_bounds__(kWave) void tree_build_kernel(TreeArgs a) {
                 }
                 int lpb = 0, lr = 0;
 #pragma unroll
-                for (int q = 0; q < CS; ++q) {
+                for (int q = 0; q < A; ++q) {
                     lpb = q == wq ? cpb[q] : lpb;
                     lr = q == wq ? cr[q] : lr;
                 }
@@ -300,7 +304,7 @@ __global__ __launch_bounds__(kWave) void tree_build_kernel(TreeArgs a) {
                 }
                 if (lane == 0) s_ktab[(d * Wb + pb) * k + r] = (int8_t)j;
 #pragma unroll
-                for (int q = 0; q < CS; ++q) key[q] = (q == wq && lane == wl) ? 0ull : key[q];
+                for (int q = 0; q < A; ++q) key[q] = (q == wq && lane == wl) ? 0ull : key[q];
             }
             // place of each new entry in rank-path order: (parent's place, rank)
             const int okey = bc[mine_pb].path * 16 + mine.rank;
@@ -315,6 +319,12 @@ __global__ __launch_bounds__(kWave) void tree_build_kernel(TreeArgs a) {
             __builtin_amdgcn_wave_barrier();
             cur ^= 1;
             nb = nn;
+        };
+        for (int d = 1; d <= D && nT < a.budget && nb > 0; ++d) {
+            const int slots = (nb * k + kWave - 1) / kWave;
+            if (slots <= 1) beam_depth(SlotCount<1>{}, d);
+            else if (slots <= 2) beam_depth(SlotCount<2>{}, d);
+            else beam_depth(SlotCount<CS>{}, d);
         }
         if (lane == 0) s_bidx[0] = 0;  // the root is the beam of depth 0
         __builtin_amdgcn_wave_barrier();
