@@ -629,15 +629,25 @@ __global__ __launch_bounds__(kWave) void tree_alg2_kernel(TreeArgs a) {
     const int rho_n = D * k * k * k;
     const float* g_rho = RHO ? a.log_rho + (int64_t)b * rho_n : nullptr;
 
-    const int64_t tb = (int64_t)b * D * k;
-    stage_words(reinterpret_cast<uint32_t*>(s_lp), reinterpret_cast<const uint32_t*>(a.logprob + tb),
-                D * k, lane);
-    stage_words(reinterpret_cast<uint32_t*>(s_ids), reinterpret_cast<const uint32_t*>(a.ids + tb), D * k,
-                lane);
-    if constexpr (RHO == 1)
-        stage_words(reinterpret_cast<uint32_t*>(s_rho), reinterpret_cast<const uint32_t*>(g_rho), rho_n,
-                    lane);
+    // every load of the tables requested before the first store, as in the
+    // best-first kernel
     const float lam_lane = lane < D ? a.lambda[(int64_t)b * a.lambda_stride + lane] : 0.f;
+    const int64_t tb = (int64_t)b * D * k;
+    {
+        uint32_t r_lp[8], r_ids[8], r_rho[16];  // D * k <= 512 words
+        load_words(r_lp, reinterpret_cast<const uint32_t*>(a.logprob + tb), D * k, 0, lane);
+        load_words(r_ids, reinterpret_cast<const uint32_t*>(a.ids + tb), D * k, 0, lane);
+        if constexpr (RHO == 1) load_words(r_rho, reinterpret_cast<const uint32_t*>(g_rho), rho_n, 0, lane);
+        store_words(reinterpret_cast<uint32_t*>(s_lp), r_lp, D * k, 0, lane);
+        store_words(reinterpret_cast<uint32_t*>(s_ids), r_ids, D * k, 0, lane);
+        if constexpr (RHO == 1) {
+            store_words(reinterpret_cast<uint32_t*>(s_rho), r_rho, rho_n, 0, lane);
+            if (rho_n > 16 * kWave)
+                stage_words(reinterpret_cast<uint32_t*>(s_rho) + 16 * kWave,
+                            reinterpret_cast<const uint32_t*>(g_rho) + 16 * kWave, rho_n - 16 * kWave,
+                            lane);
+        }
+    }
     __builtin_amdgcn_wave_barrier();
 
     // Appends the top-`branch` children (by s desc, rank asc) of the node v
