@@ -276,7 +276,28 @@ __global__ __launch_bounds__(kWave) void tree_build_kernel(TreeArgs a) {
             const int nn = min(Wb, count);
             BeamEntry mine{0.f, 0, 0, 0};
             int mine_pb = 0;
-            for (int j = 0; j < nn; ++j) {
+            int okey = 0;
+            if constexpr (A == 1) {
+                // at most 64 candidates: each takes its place among them by
+                // comparing every key once (keys are distinct, 0 = not in T);
+                // the nn best hand themselves to lanes 0 .. nn-1 through the
+                // next beam's LDS buffer (path holds the rank-path key there)
+                int rk = 0;
+                const int ncand = nb * k;
+                for (int c = 0; c < ncand; ++c) rk += readlane_u64(key[0], c) > key[0] ? 1 : 0;
+                if (key[0] != 0ull && rk < nn) {
+                    const BeamEntry pe = bc[cpb[0]];
+                    s_ktab[(d * Wb + cpb[0]) * k + cr[0]] = (int8_t)rk;
+                    s_beam[(cur ^ 1) * Wb + rk] =
+                        BeamEntry{unord32((uint32_t)(key[0] >> 32)), cr[0], pe.rank, pe.path * 16 + cr[0]};
+                }
+                __builtin_amdgcn_wave_barrier();
+                if (lane < nn) {
+                    mine = s_beam[(cur ^ 1) * Wb + lane];
+                    okey = mine.path;
+                }
+            }
+            for (int j = 0; A > 1 && j < nn; ++j) {
                 uint64_t lm = 0ull;
 #pragma unroll
                 for (int q = 0; q < A; ++q) lm = key[q] > lm ? key[q] : lm;
@@ -307,7 +328,7 @@ __global__ __launch_bounds__(kWave) void tree_build_kernel(TreeArgs a) {
                 for (int q = 0; q < A; ++q) key[q] = (q == wq && lane == wl) ? 0ull : key[q];
             }
             // place of each new entry in rank-path order: (parent's place, rank)
-            const int okey = bc[mine_pb].path * 16 + mine.rank;
+            if constexpr (A > 1) okey = bc[mine_pb].path * 16 + mine.rank;
             int place = 0;
             for (int j = 0; j < nn; ++j) {
                 const int oj = __builtin_amdgcn_readlane(okey, j);
