@@ -50,7 +50,7 @@ struct TreeArgs {
     bool rho_in_lds;
     int32_t beam_width;  // beam search only
     // LDS byte offsets
-    int o_lp, o_ids, o_kord, o_krank, o_rec, o_ktab, o_beam, o_bidx, o_rho;
+    int o_lp, o_ids, o_kord, o_krank, o_rec, o_ktab, o_beam, o_kbeam, o_rho;
     // literal Alg. 2 only: T (capacity budget + branch - 1) in LDS
     int o_tmeta, o_tS, o_tkey, o_tplace;
 };
@@ -227,7 +227,9 @@ __global__ __launch_bounds__(kWave) void tree_build_kernel(TreeArgs a) {
     // its depth (its index there, >= 0); -2: not in T.
     int8_t* s_ktab = reinterpret_cast<int8_t*>(lds + a.o_ktab);
     BeamEntry* s_beam = reinterpret_cast<BeamEntry*>(lds + a.o_beam);  // [2][Wb]
-    int8_t* s_bidx = reinterpret_cast<int8_t*>(lds + a.o_bidx);        // [N] beam index per node
+    // [N][k]: the table entry above of every child of a committed node, by
+    // candidate rank (written when the node is expanded)
+    int8_t* s_kbeam = reinterpret_cast<int8_t*>(lds + a.o_kbeam);
     const int Wb = a.beam_width;
     if constexpr (BEAM) {
         const int tab = (D + 1) * Wb * k;
@@ -347,7 +349,6 @@ __global__ __launch_bounds__(kWave) void tree_build_kernel(TreeArgs a) {
             else if (slots <= 2) beam_depth(SlotCount<2>{}, d);
             else beam_depth(SlotCount<CS>{}, d);
         }
-        if (lane == 0) s_bidx[0] = 0;  // the root is the beam of depth 0
         __builtin_amdgcn_wave_barrier();
     }
 
@@ -384,8 +385,11 @@ __global__ __launch_bounds__(kWave) void tree_build_kernel(TreeArgs a) {
         }
         bool in = lane < k && live;
         if constexpr (BEAM) {
-            // the children in T (the beam pass applied the branch filter)
-            in = in && s_ktab[((d + 1) * Wb + bidx) * k + rl] >= -1;
+            // the children in T (the beam pass applied the branch filter);
+            // their table entries are kept for their own pops
+            const int tv = s_ktab[((d + 1) * Wb + bidx) * k + rl];
+            in = in && tv >= -1;
+            if (lane < k && live) s_kbeam[n * k + lane] = (int8_t)tv;
         } else if (a.branch < k) {
             // keep the top-`branch` by token score (larger s, then lower rank)
             int sel = 0;
@@ -524,8 +528,7 @@ __global__ __launch_bounds__(kWave) void tree_build_kernel(TreeArgs a) {
         if (lane == 0) s_rec[n] = make_uint2(meta, __float_as_uint(S));
         int bidx = 0;  // beam search: n's entry in the beam of its depth, or < 0
         if constexpr (BEAM) {
-            bidx = s_ktab[(d * Wb + s_bidx[p]) * k + r];
-            if (lane == 0) s_bidx[n] = (int8_t)bidx;
+            bidx = s_kbeam[p * k + r];  // recorded when p was expanded
         }
 
         // next sibling of n: the next entry of its parent's ordered children
@@ -877,7 +880,7 @@ static int align16(int x) { return (x + 15) & ~15; }
 
 struct TreeLayout {
     int total_no_rho, total_with_rho;
-    int o_lp, o_ids, o_kord, o_krank, o_rec, o_ktab, o_beam, o_bidx, o_rho;
+    int o_lp, o_ids, o_kord, o_krank, o_rec, o_ktab, o_beam, o_kbeam, o_rho;
 };
 
 static TreeLayout tree_layout(int D, int k, int N, int Wb) {
@@ -889,7 +892,7 @@ static TreeLayout tree_layout(int D, int k, int N, int Wb) {
     L.o_krank = off; off = align16(off + N * k);
     L.o_ktab = off; off = align16(off + (D + 1) * Wb * k);
     L.o_beam = off; off = align16(off + 2 * Wb * (int)sizeof(BeamEntry));
-    L.o_bidx = off; off = align16(off + N);
+    L.o_kbeam = off; off = align16(off + (Wb > 0 ? N * k : 0));  // beam search only
     L.o_rec = off; off = align16(off + N * 8);
     L.total_no_rho = off;
     L.o_rho = off;
@@ -988,7 +991,7 @@ presto_status launch_build_tree(const presto_tree_desc* desc, const int32_t* ids
     a.beam_width = beam ? desc->beam_width : 0;
     const TreeLayout L = tree_layout(a.D, a.k, a.N, a.beam_width);
     a.o_lp = L.o_lp; a.o_ids = L.o_ids; a.o_kord = L.o_kord; a.o_krank = L.o_krank; a.o_rec = L.o_rec;
-    a.o_ktab = L.o_ktab; a.o_beam = L.o_beam; a.o_bidx = L.o_bidx;
+    a.o_ktab = L.o_ktab; a.o_beam = L.o_beam; a.o_kbeam = L.o_kbeam;
     a.o_rho = L.o_rho;
     a.rho_in_lds = log_rho != nullptr && L.total_with_rho <= kTreeLdsBudget;
     const int lds = a.rho_in_lds ? L.total_with_rho : L.total_no_rho;
