@@ -78,7 +78,7 @@ enum {
 /* Stage 1: log-softmax normaliser and top-k candidates per drafter position.
  *
  * Defined by the diffusion marginal q_d = softmax(z_d) of each block
- * position d (Sec. 3, Eq. 6) and the per-position top-k candidate
+ * position d (Sec. 2.3, Eq. 6) and the per-position top-k candidate
  * extraction of Sec. 5.1 / Appendix C stage II.
  *
  * logits     [rows, row_stride] of dtype dt; row r = (sequence, position),
@@ -94,6 +94,11 @@ enum {
  *            -inf gives H = 0.
  * flags      optional: PRESTO_FLAG_NAN_DRAFTER when a row holds NaN or
  *            +inf; that row's outputs are then unspecified.
+ * Diagnostic: once the call has completed, the first 4 bytes of the
+ * workspace hold (uint32) the number of wave-sized chunks of the rows whose
+ * candidates did not fit the fast path (more than 256 values in groups that
+ * reach the chunk's k-th lane maximum: heavy ties) and were selected by the
+ * slower exact pass.  The results are the same either way.
  * Limits: 1 <= k <= 16, k <= vocab, row_stride >= vocab, rows >= 0
  * (rows == 0 is a no-op).
  */
@@ -207,7 +212,7 @@ typedef struct {
     int32_t depth;  /* block length D = maximal tree depth, 1 .. 32 (24 if k=16) */
     int32_t k;      /* candidates per position, 1 .. 16                        */
     int32_t branch; /* children per expansion, 1 .. k                          */
-    int32_t budget; /* B, draft nodes excluding the root, 1 .. 511            */
+    int32_t budget; /* B, draft nodes excluding the root, 1 .. 1023           */
     int32_t mode;   /* presto_tree_mode                                        */
     int32_t beam_width; /* W, PRESTO_TREE_BEAM only (ignored otherwise)        */
     int32_t lambda_per_seq; /* 0: lambda is [depth]; 1: lambda is [batch, depth] */
@@ -345,12 +350,12 @@ presto_status presto_commit_kv(const presto_commit_desc *desc, const void *k_tre
                                void *k_cache, void *v_cache, int64_t cache_rows, int32_t *ctx,
                                const int32_t *ctx_cap, int32_t *flags, hipStream_t stream);
 
-/* Quadratic self-speculation (Appendix E).  The verification forward also
+/* Quadratic self-speculation (Appendix C).  The verification forward also
  * denoises `slots` mask positions after every tree node; slot j (1-based)
  * of node n stands for the position j places after n.  Their logits form
  * the matrix [batch, n_max, slots, V] (row (b, n, j - 1)).
  *
- * presto_select_slots (Appendix E (II)): only the block of the last accepted
+ * presto_select_slots (Appendix C stage II): only the block of the last accepted
  * node a = path[b, accept_len[b]] feeds the next round.  Writes row_index
  * [batch, slots - first_slot] int64: next drafter row d of sequence b reads
  * slot first_slot + d + 1 of a, i.e. matrix row
@@ -359,7 +364,7 @@ presto_status presto_commit_kv(const presto_commit_desc *desc, const void *k_tre
  * An invalid path raises PRESTO_FLAG_KV_COMMIT and reads the root's block.
  * Limits: 0 <= first_slot < slots <= 64.
  *
- * presto_flatten_slots (Appendix E (IV)): the next forward's input puts a
+ * presto_flatten_slots (Appendix C stage IV): the next forward's input puts a
  * block of `slots` mask slots after every tree node: composite row
  * r = n * (1 + slots) + j is node n (j = 0) or its slot j.  Writes
  *   pos_out [batch, R] int32, R = n_max * (1 + slots): root_pos[b] +

@@ -235,7 +235,7 @@ def accept(dtype, target_logits, parent, token, n_nodes, depth: int) -> dict:
 
 
 # ----------------------------------------------------------------------------
-# Bookkeeping between rounds (Appendix C stage I; Appendix E)
+# Bookkeeping between rounds (Appendix C stages I, II and IV)
 
 def commit_kv(k_tree, v_tree, path, accept_len, k_cache, v_cache, ctx, ctx_cap):
     """The root and the accepted draft tokens join the committed prefix
@@ -268,7 +268,7 @@ def commit_kv(k_tree, v_tree, path, accept_len, k_cache, v_cache, ctx, ctx_cap):
 
 def select_slots(path, accept_len, n_max: int, slots: int, first_slot: int = 1) -> np.ndarray:
     """Rows of the next round's drafter positions in the slot-logit matrix
-    [b * n_max * slots, V] (Appendix E (II)): only the mask slots after the
+    [b * n_max * slots, V] (Appendix C stage II): only the mask slots after the
     last accepted node are used, from slot first_slot + 1 (1-based) on."""
     B = len(accept_len)
     out = np.empty((B, slots - first_slot), np.int64)
@@ -280,7 +280,7 @@ def select_slots(path, accept_len, n_max: int, slots: int, first_slot: int = 1) 
 
 
 def flatten_slots(parent, depth, n_nodes, root_pos, slots: int) -> dict:
-    """Composite input of the next forward (Appendix E (IV)): every tree node
+    """Composite input of the next forward (Appendix C stage IV): every tree node
     is followed by a block of `slots` mask slots; row n * (1 + slots) + j is
     node n (j = 0) or its slot j.  A node row attends to the node rows on its
     root path (itself included), a slot row to those same node rows and to

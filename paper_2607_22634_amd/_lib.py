@@ -202,6 +202,18 @@ def presto_topk(logits: torch.Tensor, k: int, *, ids=None, logprob=None, lse=Non
     return (ids, logprob, lse, h) if want_h else (ids, logprob, lse)
 
 
+def topk_workspace(rows: int, vocab: int, k: int, device) -> torch.Tensor:
+    """A workspace for presto_topk / presto_topk_rows of this size."""
+    return torch.empty(max(1, lib().presto_topk_workspace(rows, vocab, k)), dtype=torch.uint8,
+                       device=device)
+
+
+def topk_fallback_chunks(workspace: torch.Tensor) -> int:
+    """The diagnostic count a completed top-k call leaves in the first four
+    bytes of its workspace: chunks that took the exact tie pass."""
+    return int(workspace[:4].cpu().view(torch.int32).item())
+
+
 def presto_entropy_lambda(entropy: torch.Tensor, beta: float, c: float, *, out=None, stream=None):
     """Entropy-adaptive weight beta * H / (H + C) of every entry of entropy."""
     out = torch.empty_like(entropy) if out is None else out

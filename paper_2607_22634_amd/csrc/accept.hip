@@ -101,8 +101,9 @@ __global__ __launch_bounds__(kArgmaxWavesPerBlock * kWave) void argmax_partial_k
 // path is the chain of nodes whose whole root path is good.  Pointer jumping
 // (ceil(log2(depth + 1)) rounds) gives every node that property and its
 // depth at once; the accepted nodes then write themselves into the path.
-// Every global load (node count, parents, tokens, chunk keys) is issued
-// before the first one is used: the kernel waits for memory once.
+// The node count, parents and tokens are loaded together; the chunk keys of
+// the live nodes are then all requested before the first is used, so the
+// kernel waits for memory twice.
 __global__ __launch_bounds__(kWalkThreads) void accept_walk_kernel(
     int32_t n_max, int32_t depth, int32_t chunks, const uint64_t* __restrict__ part,
     const int32_t* __restrict__ parent, const int32_t* __restrict__ token,
@@ -122,12 +123,12 @@ __global__ __launch_bounds__(kWalkThreads) void accept_walk_kernel(
     const int my_tok = tid < n_max ? token[rb + tid] : 0;
     const int nn_raw = n_nodes[b];
     if (tid == 0) s_len = 0;
-    // each wave reduces the chunk keys of kNodesPerWave nodes at a time, up to
-    // kKeyCols chunk keys per lane and node with every load in flight before
-    // the first reduction (one memory round trip for a 151936-entry bf16 row);
-    // rows of padding nodes are reduced too (never written in this call;
-    // ignored below)
-    for (int n0 = wave * kNodesPerWave; n0 < n_max; n0 += nwaves * kNodesPerWave) {
+    // each wave reduces the chunk keys of kNodesPerWave live nodes at a time,
+    // up to kKeyCols chunk keys per lane and node with every load in flight
+    // before the first reduction (one memory round trip for a 151936-entry
+    // bf16 row); padding nodes have no keys (the argmax kernel skips them)
+    const int nn = min(max(nn_raw, 1), n_max);
+    for (int n0 = wave * kNodesPerWave; n0 < nn; n0 += nwaves * kNodesPerWave) {
         uint64_t best[kNodesPerWave];
 #pragma unroll
         for (int u = 0; u < kNodesPerWave; ++u) best[u] = 0ull;
@@ -138,7 +139,7 @@ __global__ __launch_bounds__(kWalkThreads) void accept_walk_kernel(
                 const int c = c0 + t * kWave + lane;
 #pragma unroll
                 for (int u = 0; u < kNodesPerWave; ++u)
-                    x[t][u] = (c < chunks && n0 + u < n_max) ? part[(rb + n0 + u) * chunks + c] : 0ull;
+                    x[t][u] = (c < chunks && n0 + u < nn) ? part[(rb + n0 + u) * chunks + c] : 0ull;
             }
 #pragma unroll
             for (int t = 0; t < kKeyCols; ++t)
@@ -148,10 +149,9 @@ __global__ __launch_bounds__(kWalkThreads) void accept_walk_kernel(
 #pragma unroll
         for (int u = 0; u < kNodesPerWave; ++u) {
             const uint64_t m = wave_max_u64_dpp(best[u]);
-            if (lane == 0 && n0 + u < n_max) s_a[n0 + u] = (int32_t)key_id(m);
+            if (lane == 0 && n0 + u < nn) s_a[n0 + u] = (int32_t)key_id(m);
         }
     }
-    const int nn = min(max(nn_raw, 1), n_max);
     __syncthreads();
     if (tid < n_max) {
         if (target_argmax) target_argmax[rb + tid] = tid < nn ? s_a[tid] : -1;

@@ -228,7 +228,7 @@ presto_status presto_build_tree(const presto_tree_desc* desc, const int32_t* ids
     REQUIRE(d.k >= 1 && d.k <= 16, "presto_build_tree: k=%d outside 1..16", d.k);
     REQUIRE(d.branch >= 1 && d.branch <= d.k, "presto_build_tree: branch=%d outside 1..k",
             d.branch);
-    REQUIRE(d.budget >= 1 && d.budget <= 511, "presto_build_tree: budget=%d outside 1..511",
+    REQUIRE(d.budget >= 1 && d.budget <= 1023, "presto_build_tree: budget=%d outside 1..1023",
             d.budget);
     REQUIRE(d.depth <= tree_max_depth(d.k),
             "presto_build_tree: depth %d exceeds the rank-path key (at most %d for k=%d)", d.depth,
@@ -245,7 +245,7 @@ presto_status presto_build_tree(const presto_tree_desc* desc, const int32_t* ids
     }
     if (!tree_build_fits(d.depth, d.k, d.branch, d.budget + 1, beam_width,
                          d.mode == PRESTO_TREE_BEST_FIRST_ALG2))
-        return set_error(PRESTO_ERR_UNSUPPORTED, "presto_build_tree: tables exceed 64 KiB of LDS");
+        return set_error(PRESTO_ERR_UNSUPPORTED, "presto_build_tree: tables exceed 160 KiB of LDS");
     if (d.batch == 0) return PRESTO_OK;
     REQUIRE(ids && logprob && lambda && root_token && n_nodes && parent && token && depth_out &&
                 rank && score && anc,
@@ -316,7 +316,7 @@ presto_status presto_accept(presto_dtype dt, const void* target_logits, int32_t 
     REQUIRE(row_stride >= vocab, "presto_accept: row_stride < vocab");
     REQUIRE(batch >= 0, "presto_accept: batch < 0");
     REQUIRE(n_max >= 1 && n_max <= 1024, "presto_accept: n_max outside 1..1024");
-    REQUIRE(depth >= 1, "presto_accept: depth < 1");
+    REQUIRE(depth >= 1 && depth <= 1024, "presto_accept: depth outside 1..1024");
     if (batch == 0) return PRESTO_OK;
     REQUIRE(target_logits && parent && token && n_nodes && accept_len && path && bonus,
             "presto_accept: null pointer");

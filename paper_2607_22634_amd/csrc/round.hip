@@ -1,4 +1,4 @@
-// Bookkeeping between rounds (Appendix C stage I, Appendix E):
+// Bookkeeping between rounds (Appendix C stages I, II and IV):
 //
 // * commit_kv_kernel: the root (the last committed token) and the accepted
 //   draft tokens become part of the committed prefix, so their tree K/V rows
@@ -32,9 +32,11 @@ __global__ __launch_bounds__(kCommitThreads) void commit_kv_kernel(
     const int m = al + 1;
     bool bad = al < 0 || al > depth || start < 0 || len < 0 || cap < 0 ||
                (int64_t)start + cap > cache_rows || (int64_t)len + m > cap;
-    if (!bad && tid < m) {
-        const int32_t node = pb[tid];
-        bad = node < 0 || node >= n_max || (tid == 0 && node != 0);
+    // every path entry is checked, whatever the depth (a path may be longer
+    // than the workgroup)
+    for (int i = tid; !bad && i < m; i += kCommitThreads) {
+        const int32_t node = pb[i];
+        bad = node < 0 || node >= n_max || (i == 0 && node != 0);
     }
     if (__syncthreads_or(bad)) {
         if (tid == 0) raise_flag(flags, PRESTO_FLAG_KV_COMMIT);

@@ -7,20 +7,22 @@
 //   * the chunk's k best (value desc, id asc) entries  (as 64-bit keys)
 // The k-th largest lane maximum (k rounds of wave max, or a ballot bisection
 // on its orderable bits for k > 8) is a lower bound on the chunk's k-th value, so only the
-// 16-byte groups whose maximum reaches it can hold a top-k entry (normally a
-// handful); their entries at or above it are compacted through a small
-// per-wave LDS list and the k best taken by k rounds of wave max.  A chunk
-// with more candidate groups than the list holds (massive ties) falls back
-// to k rounds of exact wave-wide selection over the chunk re-read from
-// memory.  A second kernel, queued right behind,
-// merges each row's chunk partials with one wave per row.
+// 16-byte groups whose maximum reaches it can hold a top-k entry (at least
+// k of them, normally about k); they are appended to a per-wave LDS list of
+// up to 256 values, their entries at or above the bound are keyed (one or
+// up to four per lane) and the k best taken by k rounds of wave max.  A
+// chunk with more candidate groups than the list holds (massive ties) falls
+// back to k rounds of exact wave-wide selection over the chunk re-read from
+// memory, and marks its partial so that the merge can count such chunks.
+// A second kernel, queued right behind, merges each row's chunk partials
+// with one wave per row.
 #include <math.h>
 
 #include "common.hpp"
 
 namespace presto {
 
-constexpr int kCandCap = 64;
+constexpr int kCandCap = 256;  // values of candidate groups a wave's list holds
 constexpr int kTopkWavesPerBlock = 4;
 constexpr float kLog2eF = 1.4426950408889634f;
 
@@ -110,7 +112,7 @@ __global__ __launch_bounds__(kTopkWavesPerBlock * kWave) void topk_partial_kerne
     const void* __restrict__ logits, int64_t rows, int32_t vocab, int64_t row_stride, int32_t k,
     int32_t chunks, bool aligned, const int64_t* __restrict__ row_index, int64_t logits_rows,
     float2* __restrict__ part_ms, uint64_t* __restrict__ part_keys, float* __restrict__ part_h,
-    int32_t* __restrict__ flags) {
+    uint32_t* __restrict__ n_fallback, int32_t* __restrict__ flags) {
     constexpr int P = VecTraits<BF16>::kPerVec;  // elements per 16-byte load (a "group")
     constexpr int E = NLOAD * P;
     constexpr int64_t CH = (int64_t)kWave * E;
@@ -123,6 +125,7 @@ __global__ __launch_bounds__(kTopkWavesPerBlock * kWave) void topk_partial_kerne
 
     const int wave = threadIdx.x / kWave, lane = lane_id();
     const int64_t gw = (int64_t)blockIdx.x * kTopkWavesPerBlock + wave;
+    if (gw == 0 && lane == 0) *n_fallback = 0u;  // counted by the merge kernel
     if (gw >= rows * chunks) return;
     const int64_t row = gw / chunks;
     const int32_t chunk = (int32_t)(gw % chunks);
@@ -223,16 +226,20 @@ __global__ __launch_bounds__(kTopkWavesPerBlock * kWave) void topk_partial_kerne
     const uint32_t ngroups = __builtin_amdgcn_readfirstlane(cand_n[wave]);
     uint64_t* out = part_keys + gw * k;
 
-    if (ngroups <= (uint32_t)kGroupCap) {
+    const int total = (int)ngroups * P;
+    // key of list entry e (0 if it is past the list, past the row or below
+    // the bound)
+    auto entry_key = [&](int e) -> uint64_t {
+        if (e >= total) return 0ull;
+        const float xv = cand_v[wave][e];
+        const int64_t idx = (int64_t)cand_i[wave][e / P] + e % P;
+        return ((full || idx < vocab) && xv >= thr) ? vocab_key(xv, (uint32_t)idx) : 0ull;
+    };
+    bool fell_back = false;
+    if (total <= kWave) {
         // one candidate per lane (keys are unique); k rounds of wave max,
         // retiring the lane that held it (0 past the last valid entry)
-        const int total = (int)ngroups * P;
-        uint64_t x = 0ull;
-        if (lane < total) {
-            const float xv = cand_v[wave][lane];
-            const int64_t idx = (int64_t)cand_i[wave][lane / P] + lane % P;
-            if ((full || idx < vocab) && xv >= thr) x = vocab_key(xv, (uint32_t)idx);
-        }
+        uint64_t x = entry_key(lane);
         uint64_t mine = 0ull;
         for (int j = 0; j < k; ++j) {
             const uint64_t m = wave_max_u64_dpp(x);
@@ -240,7 +247,25 @@ __global__ __launch_bounds__(kTopkWavesPerBlock * kWave) void topk_partial_kerne
             x = x == m ? 0ull : x;
         }
         if (lane < k) out[lane] = mine;
+    } else if (ngroups <= (uint32_t)kGroupCap) {
+        // up to four candidates per lane (the usual case for k > 8)
+        constexpr int C = kCandCap / kWave;
+        uint64_t x[C];
+#pragma unroll
+        for (int c = 0; c < C; ++c) x[c] = entry_key(c * kWave + lane);
+        uint64_t mine = 0ull;
+        for (int j = 0; j < k; ++j) {
+            uint64_t lmax = x[0];
+#pragma unroll
+            for (int c = 1; c < C; ++c) lmax = x[c] > lmax ? x[c] : lmax;
+            const uint64_t m = wave_max_u64_dpp(lmax);
+            mine = lane == j ? m : mine;
+#pragma unroll
+            for (int c = 0; c < C; ++c) x[c] = x[c] == m ? 0ull : x[c];
+        }
+        if (lane < k) out[lane] = mine;
     } else {
+        fell_back = true;
         // massive ties: exact selection, k rounds of "largest key below the
         // last one", re-reading the chunk from memory (rare; keeps the
         // register copy of the chunk out of this path)
@@ -262,7 +287,9 @@ __global__ __launch_bounds__(kTopkWavesPerBlock * kWave) void topk_partial_kerne
         }
     }
     if (lane == 0) {
-        part_ms[gw] = make_float2(M, S);
+        // the sum is never negative: its sign bit marks a chunk that took the
+        // exact fallback
+        part_ms[gw] = make_float2(M, fell_back ? -S : S);
         if constexpr (ENT) part_h[gw] = Hx;
         if (!(S == S)) raise_flag(flags, PRESTO_FLAG_NAN_DRAFTER);
     }
@@ -278,7 +305,7 @@ __global__ __launch_bounds__(kTopkWavesPerBlock * kWave) void topk_merge_kernel(
     int64_t rows, int32_t chunks, int32_t k, const float2* __restrict__ part_ms,
     const uint64_t* __restrict__ part_keys, const float* __restrict__ part_h,
     int32_t* __restrict__ ids, float* __restrict__ logprob, float* __restrict__ lse,
-    float* __restrict__ entropy) {
+    float* __restrict__ entropy, uint32_t* __restrict__ n_fallback) {
     const int wave = threadIdx.x / kWave, lane = lane_id();
     const int64_t row = (int64_t)blockIdx.x * kTopkWavesPerBlock + wave;
     if (row >= rows) return;
@@ -304,17 +331,28 @@ __global__ __launch_bounds__(kTopkWavesPerBlock * kWave) void topk_merge_kernel(
         mr[i] = c < chunks ? ms[c] : make_float2(-INFINITY, 0.f);
     }
     float m = -INFINITY;
+    int nfb = 0;  // chunks of this lane that took the exact fallback
 #pragma unroll
-    for (int i = 0; i < kMsRegs; ++i) m = fmaxf(m, mr[i].x);
-    for (int c = kMsRegs * kWave + lane; c < chunks; c += kWave) m = fmaxf(m, ms[c].x);
+    for (int i = 0; i < kMsRegs; ++i) {
+        m = fmaxf(m, mr[i].x);
+        nfb += __builtin_signbit(mr[i].y) ? 1 : 0;
+        mr[i].y = fabsf(mr[i].y);
+    }
+    for (int c = kMsRegs * kWave + lane; c < chunks; c += kWave) {
+        m = fmaxf(m, ms[c].x);
+        nfb += __builtin_signbit(ms[c].y) ? 1 : 0;
+    }
     const float M = wave_max_f32_dpp(m);
+    nfb = wave_sum_i32(nfb);
+    if (lane == 0 && nfb > 0) atomicAdd(n_fallback, (uint32_t)nfb);
     float s = 0.f, hx = 0.f;
     // chunk sums shift to the row max: (z - M) = (z - m_c) + (m_c - M)
     auto add_chunk = [&](float2 p, int c) {
         if (p.x != -INFINITY) {
             const float w = __expf(p.x - M);
-            s += p.y * w;
-            if constexpr (ENT) hx += w * (part_h[row * chunks + c] + (p.x - M) * p.y);
+            const float py = fabsf(p.y);
+            s += py * w;
+            if constexpr (ENT) hx += w * (part_h[row * chunks + c] + (p.x - M) * py);
         }
     };
     if (M != -INFINITY) {
@@ -370,6 +408,10 @@ namespace presto_host {
 
 using namespace presto;
 
+// The workspace starts with the fallback counter (read by callers that want
+// the diagnostic), then the partials.
+static constexpr size_t kTopkCounterBytes = 16;
+
 static int topk_nload(bool bf16, int64_t rows, int32_t vocab) {
     const int64_t ch8 = (int64_t)kWave * 8 * (bf16 ? 8 : 4);
     const int64_t waves8 = rows * ((vocab + ch8 - 1) / ch8);
@@ -381,7 +423,7 @@ size_t topk_workspace_bytes(int64_t rows, int32_t vocab, int32_t k) {
     // sized for the finest chunking any dtype may pick
     const int64_t chunks = (vocab + (int64_t)kWave * 16 - 1) / ((int64_t)kWave * 16);
     const size_t per = (size_t)chunks * (sizeof(float2) + sizeof(uint64_t) * (size_t)k + sizeof(float));
-    return (size_t)rows * per + 512;
+    return (size_t)rows * per + 512 + kTopkCounterBytes;
 }
 
 presto_status launch_topk(bool bf16, const void* logits, const int64_t* row_index,
@@ -393,7 +435,8 @@ presto_status launch_topk(bool bf16, const void* logits, const int64_t* row_inde
     const int64_t chunks = (vocab + ch - 1) / ch;
     const size_t esz = bf16 ? 2 : 4;
     const bool aligned = ((uintptr_t)logits % 16 == 0) && ((row_stride * (int64_t)esz) % 16 == 0);
-    float2* ms = static_cast<float2*>(ws);
+    uint32_t* n_fallback = static_cast<uint32_t*>(ws);
+    float2* ms = reinterpret_cast<float2*>(static_cast<char*>(ws) + kTopkCounterBytes);
     uint64_t* keys = reinterpret_cast<uint64_t*>(
         (reinterpret_cast<uintptr_t>(ms + rows * chunks) + 15) & ~uintptr_t(15));
     float* hs = reinterpret_cast<float*>(
@@ -406,7 +449,7 @@ presto_status launch_topk(bool bf16, const void* logits, const int64_t* row_inde
     topk_partial_kernel<BF, NL, EN><<<grid, block, 0, stream>>>(logits, rows, vocab, row_stride, \
                                                                k, (int32_t)chunks, aligned,      \
                                                                row_index, logits_rows, ms, keys, \
-                                                               hs, flags)
+                                                               hs, n_fallback, flags)
 #define PRESTO_TOPK2(BF, NL) \
     if (ent) PRESTO_TOPK(BF, NL, true); else PRESTO_TOPK(BF, NL, false)
     if (bf16) {
@@ -422,7 +465,7 @@ presto_status launch_topk(bool bf16, const void* logits, const int64_t* row_inde
     const int64_t per_lane = (chunks * k + kWave - 1) / kWave;
 #define PRESTO_MERGE(KP, EN)                                                                    \
     topk_merge_kernel<KP, EN><<<mgrid, block, 0, stream>>>(rows, (int32_t)chunks, k, ms, keys, hs, \
-                                                           ids, logprob, lse, entropy)
+                                                           ids, logprob, lse, entropy, n_fallback)
 #define PRESTO_MERGE2(KP) \
     if (ent) PRESTO_MERGE(KP, true); else PRESTO_MERGE(KP, false)
     if (per_lane <= 2) { PRESTO_MERGE2(2); }

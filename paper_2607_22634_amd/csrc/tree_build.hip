@@ -579,6 +579,7 @@ __global__ __launch_bounds__(kWave) void tree_build_kernel(TreeArgs a) {
         else if (SL <= 3 || need <= 3) go = pop(SlotCount<(SL < 3 ? SL : 3)>{});
         else if (SL <= 4 || need <= 4) go = pop(SlotCount<(SL < 4 ? SL : 4)>{});
         else if (SL <= 5 || need <= 5) go = pop(SlotCount<(SL < 5 ? SL : 5)>{});
+        else if (SL <= 8 || need <= 8) go = pop(SlotCount<(SL < 8 ? SL : 8)>{});
         else go = pop(SlotCount<SL>{});
         if (!go) break;
     }
@@ -645,7 +646,8 @@ __global__ __launch_bounds__(kWave) void tree_alg2_kernel(TreeArgs a) {
     float* s_lp = reinterpret_cast<float*>(lds + a.o_lp);
     int32_t* s_ids = reinterpret_cast<int32_t*>(lds + a.o_ids);
     float* s_rho = reinterpret_cast<float*>(lds + a.o_rho);
-    // T node c: (parent + 1, 0 for the root) | rank << 10 | depth << 14
+    // T node c: (parent + 1, 0 for the root) | rank << 11 | depth << 15
+    // (T holds up to budget + branch - 1 <= 1038 nodes: 11 bits of parent)
     uint32_t* s_tmeta = reinterpret_cast<uint32_t*>(lds + a.o_tmeta);
     float* s_tS = reinterpret_cast<float*>(lds + a.o_tS);
     uint4* s_tkey = reinterpret_cast<uint4*>(lds + a.o_tkey);  // x: most significant word
@@ -697,7 +699,7 @@ __global__ __launch_bounds__(kWave) void tree_alg2_kernel(TreeArgs a) {
         }
         if (lane < k && sel < branch) {
             const int c = nT + sel;
-            s_tmeta[c] = (uint32_t)(v + 1) | ((uint32_t)lane << 10) | ((uint32_t)(d + 1) << 14);
+            s_tmeta[c] = (uint32_t)(v + 1) | ((uint32_t)lane << 11) | ((uint32_t)(d + 1) << 15);
             s_tS[c] = Sv + s;
             const int wi = d / per_word, sh = 32 - (d % per_word + 1) * wbits;
             const uint32_t dig = (uint32_t)(lane + 1) << sh;
@@ -768,11 +770,11 @@ __global__ __launch_bounds__(kWave) void tree_alg2_kernel(TreeArgs a) {
 #pragma unroll
         for (int j = 0; j < SLT; ++j) fO[j] = (lane == w && j == es) ? 0u : fO[j];
         const uint32_t meta = s_tmeta[e];
-        const int d = (meta >> 14) & 63;
+        const int d = (meta >> 15) & 63;
         if (d < D) {
-            const int pv = (int)(meta & 1023) - 1;
-            const int rp = pv >= 0 ? (int)((s_tmeta[pv] >> 10) & 15) : 0;
-            expand(e, d, (meta >> 10) & 15, rp, s_tS[e], s_tkey[e], nT);
+            const int pv = (int)(meta & 2047) - 1;
+            const int rp = pv >= 0 ? (int)((s_tmeta[pv] >> 11) & 15) : 0;
+            expand(e, d, (meta >> 11) & 15, rp, s_tS[e], s_tkey[e], nT);
             mark_open(nT, branch);
             nT += branch;
         }
@@ -827,7 +829,7 @@ __global__ __launch_bounds__(kWave) void tree_alg2_kernel(TreeArgs a) {
         if (pl >= keep) continue;
         const int o = pl + 1;
         const uint32_t meta = s_tmeta[i];
-        const int pv = (int)(meta & 1023) - 1, r = (meta >> 10) & 15, d = (meta >> 14) & 63;
+        const int pv = (int)(meta & 2047) - 1, r = (meta >> 11) & 15, d = (meta >> 15) & 63;
         int po = 0;
         if (pv >= 0) po = s_tplace[pv] < keep ? s_tplace[pv] + 1 : -2;
         a.parent[ob + o] = po;
@@ -844,7 +846,7 @@ __global__ __launch_bounds__(kWave) void tree_alg2_kernel(TreeArgs a) {
         while (true) {
 #pragma unroll
             for (int q = 0; q < SLW; ++q) words[q] |= q == (xo >> 6) ? 1ull << (xo & 63) : 0ull;
-            const int xv = (int)(s_tmeta[x] & 1023) - 1;
+            const int xv = (int)(s_tmeta[x] & 2047) - 1;
             if (xv < 0) {
                 words[0] |= 1ull;  // the root
                 break;
@@ -900,7 +902,23 @@ static TreeLayout tree_layout(int D, int k, int N, int Wb) {
     return L;
 }
 
-static constexpr int kTreeLdsBudget = 64 * 1024;
+// gfx950 gives one workgroup up to 160 KiB of LDS; the search runs one wave
+// per CU anyway, so the lattice stays in LDS whenever the total fits.
+static constexpr int kTreeLdsBudget = 160 * 1024;
+static constexpr int kDefaultLds = 64 * 1024;
+
+// Dynamic LDS above the default needs the kernel's own limit raised (once
+// per instantiation and process).
+template <typename K>
+static presto_status allow_lds(K* kernel, int bytes) {
+    if (bytes <= kDefaultLds) return PRESTO_OK;
+    const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kernel),
+                                             hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
+    if (e != hipSuccess)
+        return set_error(PRESTO_ERR_HIP, "tree build: %d bytes of LDS refused: %s", bytes,
+                         hipGetErrorString(e));
+    return PRESTO_OK;
+}
 
 int tree_key_bits(int k) {
     int wbits = 1;
@@ -976,15 +994,22 @@ presto_status launch_build_tree(const presto_tree_desc* desc, const int32_t* ids
         const int lds = a.rho_in_lds ? L.total_with_rho : L.total_no_rho;
         const int slt = (L.cap + kWave - 1) / kWave;
         const int rho_mode = log_rho == nullptr ? 0 : (a.rho_in_lds ? 1 : 2);
-#define PRESTO_ALG2(S)                                                                              \
-    if (rho_mode == 0) tree_alg2_kernel<S, 0><<<desc->batch, kWave, lds, stream>>>(a);              \
-    else if (rho_mode == 1) tree_alg2_kernel<S, 1><<<desc->batch, kWave, lds, stream>>>(a);         \
-    else tree_alg2_kernel<S, 2><<<desc->batch, kWave, lds, stream>>>(a)
+        presto_status st = PRESTO_OK;
+        auto go = [&](auto kernel) {
+            st = allow_lds(kernel, lds);
+            if (st == PRESTO_OK) kernel<<<desc->batch, kWave, lds, stream>>>(a);
+        };
+#define PRESTO_ALG2(S)                                    \
+    if (rho_mode == 0) go(tree_alg2_kernel<S, 0>);        \
+    else if (rho_mode == 1) go(tree_alg2_kernel<S, 1>);   \
+    else go(tree_alg2_kernel<S, 2>)
         if (slt <= 1) { PRESTO_ALG2(1); }
         else if (slt <= 2) { PRESTO_ALG2(2); }
         else if (slt <= 4) { PRESTO_ALG2(4); }
-        else { PRESTO_ALG2(9); }
+        else if (slt <= 9) { PRESTO_ALG2(9); }
+        else { PRESTO_ALG2(17); }
 #undef PRESTO_ALG2
+        if (st != PRESTO_OK) return st;
         return check_launch("tree_alg2_kernel");
     }
     const bool beam = desc->mode == PRESTO_TREE_BEAM;
@@ -997,9 +1022,14 @@ presto_status launch_build_tree(const presto_tree_desc* desc, const int32_t* ids
     const int lds = a.rho_in_lds ? L.total_with_rho : L.total_no_rho;
     const int SL = (a.N + kWave - 1) / kWave;
     const int rho_mode = log_rho == nullptr ? 0 : (a.rho_in_lds ? 1 : 2);
-#define PRESTO_TREE4(S, R, Q)                                                       \
-    if (beam) tree_build_kernel<S, R, Q, true><<<desc->batch, kWave, lds, stream>>>(a); \
-    else tree_build_kernel<S, R, Q, false><<<desc->batch, kWave, lds, stream>>>(a)
+    presto_status st = PRESTO_OK;
+    auto go = [&](auto kernel) {
+        st = allow_lds(kernel, lds);
+        if (st == PRESTO_OK) kernel<<<desc->batch, kWave, lds, stream>>>(a);
+    };
+#define PRESTO_TREE4(S, R, Q)                         \
+    if (beam) go(tree_build_kernel<S, R, Q, true>);   \
+    else go(tree_build_kernel<S, R, Q, false>)
 #define PRESTO_TREE2(S, R) \
     if (a.k <= 4) { PRESTO_TREE4(S, R, true); } else { PRESTO_TREE4(S, R, false); }
 #define PRESTO_TREE(S)                      \
@@ -1011,10 +1041,12 @@ presto_status launch_build_tree(const presto_tree_desc* desc, const int32_t* ids
     else if (SL <= 3) { PRESTO_TREE(3) }
     else if (SL <= 4) { PRESTO_TREE(4) }
     else if (SL <= 5) { PRESTO_TREE(5) }
-    else { PRESTO_TREE(8) }
+    else if (SL <= 8) { PRESTO_TREE(8) }
+    else { PRESTO_TREE(16) }
 #undef PRESTO_TREE
 #undef PRESTO_TREE2
 #undef PRESTO_TREE4
+    if (st != PRESTO_OK) return st;
     return check_launch("tree_build_kernel");
 }
 

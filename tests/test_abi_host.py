@@ -86,13 +86,25 @@ def test_topk_rejects_small_workspace():
 
 
 @pytest.mark.parametrize("field,value", [("depth", 0), ("depth", 33), ("k", 0), ("k", 17),
-                                         ("branch", 5), ("budget", 0), ("budget", 512),
+                                         ("branch", 5), ("budget", 0), ("budget", 1024),
                                          ("mode", 9)])
 def test_build_tree_rejects_bad_descriptor(field, value):
     d = P.TreeDesc(1, 4, 4, 4, 8, 0)
     setattr(d, field, value)
     st, _ = _err(P.lib().presto_build_tree(ctypes.byref(d), *([None] * 13), 0, None))
     assert st == P.PRESTO_ERR_INVALID_ARG
+
+
+@pytest.mark.parametrize("mode", [0, 1, 2])
+def test_build_tree_accepts_budget_1023(mode):
+    # the largest budget (N = 1024 rows) with the paper's k = 10, depth 16 and
+    # beam width 10; batch 0: validated, nothing launched
+    d = P.TreeDesc(0, 16, 10, 10, 1023, mode, 10)
+    st, msg = _err(P.lib().presto_build_tree(ctypes.byref(d), *([None] * 13), 0, None))
+    assert st == P.PRESTO_OK, msg
+    d = P.TreeDesc(0, 24, 16, 16, 1023, mode, 16)
+    st, msg = _err(P.lib().presto_build_tree(ctypes.byref(d), *([None] * 13), 0, None))
+    assert st == P.PRESTO_OK, msg
 
 
 def test_build_tree_accepts_every_mode():
@@ -133,6 +145,24 @@ def test_accept_rejects_bad_arguments():
     assert lib.presto_accept(0, None, 1024, 1024, 1, 9, 0, *args, 0, None) == P.PRESTO_ERR_INVALID_ARG
     assert lib.presto_accept(0, None, 1024, 1024, 1, 9, 4, *args, 0, None) == P.PRESTO_ERR_INVALID_ARG
     assert lib.presto_accept(0, None, 1024, 1024, 0, 9, 4, *args, 0, None) == P.PRESTO_OK
+    # depth bounds the pointer-jumping rounds and the path rows: at most 1024
+    st, msg = _err(lib.presto_accept(0, None, 1024, 1024, 0, 9, 1025, *args, 0, None))
+    assert st == P.PRESTO_ERR_INVALID_ARG and "depth" in msg
+    assert lib.presto_accept(0, None, 1024, 1024, 0, 9, 1024, *args, 0, None) == P.PRESTO_OK
+
+
+def test_commit_kv_rejects_bad_descriptor():
+    lib = P.lib()
+    for field, value in [("depth", 0), ("depth", 1025), ("n_max", 1025), ("head_dim", 96),
+                         ("hkv", 0), ("dt", 4)]:
+        d = P.CommitDesc(1, 65, 8, 128, 16, P.PRESTO_DT_BF16)
+        setattr(d, field, value)
+        st, _ = _err(lib.presto_commit_kv(ctypes.byref(d), *([None] * 6), 0, None, None, None,
+                                          None))
+        assert st == P.PRESTO_ERR_INVALID_ARG, (field, value)
+    d = P.CommitDesc(0, 1024, 8, 128, 1024, P.PRESTO_DT_BF16)  # the largest path; batch 0
+    assert lib.presto_commit_kv(ctypes.byref(d), *([None] * 6), 0, None, None, None,
+                                None) == P.PRESTO_OK
 
 
 def test_ngram_entry_points_validate_on_the_host():

@@ -1,7 +1,7 @@
 """GPU parity of the bookkeeping between rounds: tree attention over a
 slotted cache (start, len per sequence), the KV commit after acceptance,
 slot selection with row-gathered top-k, and the flattened slot-block layout
-of quadratic self-speculation (Appendix C stage I, Appendix E).  Every
+of quadratic self-speculation (Appendix C stages I, II and IV).  Every
 input the oracle sees comes from the oracle or the synthetic generators."""
 import numpy as np
 import pytest

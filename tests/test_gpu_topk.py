@@ -168,3 +168,42 @@ def test_entropy_lambda_matches_oracle():
         # three fp32 roundings (H + C, the quotient, the product)
         np.testing.assert_allclose(lam, want, rtol=4e-7, atol=0)
         assert lam[0] == 0.0
+
+
+@pytest.mark.parametrize("cfg,k", [(2, 8), (2, 10), (2, 16), (4, 10), (5, 10), (3, 12)])
+def test_topk_large_k_on_workload(cfg, k):
+    """k above 8 (the paper's k = 10, Sec. 5.1) at the workloads' shapes: ids
+    bit-exact, and the fast path holds every chunk (no exact-pass fallback
+    on continuous logits: at most one group per lane reaches the bound)."""
+    w, rin = round_data(cfg)
+    logits = rin["drafter_logits"]
+    print(f"topk large-k cfg={cfg} rows={logits.shape[0]} k={k}", flush=True)
+    dev_logits = to_dev(logits, w.dtype)
+    ws = P.topk_workspace(logits.shape[0], w.vocab, k, dev_logits.device)
+    ids, lp, lse = P.presto_topk(dev_logits, k, workspace=ws)
+    torch.cuda.synchronize()
+    _compare(logits, w.dtype, k, ids, lp, lse)
+    assert P.topk_fallback_chunks(ws) == 0
+
+
+def test_topk_fallback_count_on_ties():
+    """Rows made of one repeated value send every chunk through the exact
+    pass; the workspace counter says how many chunks that was, and a later
+    call without ties resets it."""
+    rng = np.random.default_rng(8)
+    rows, V, k = 6, 151936, 10
+    x = (rng.standard_normal((rows, V)) * 4).astype(np.float32)
+    x[1, :] = 2.0
+    x[4, :] = np.round(x[4] / 64) * 64  # a handful of distinct values
+    store = sy.cast(x, "bf16")
+    dl = to_dev(store, "bf16")
+    ws = P.topk_workspace(rows, V, k, dl.device)
+    ids, lp, lse = P.presto_topk(dl, k, workspace=ws)
+    torch.cuda.synchronize()
+    _compare(store, "bf16", k, ids, lp, lse)
+    n_fb = P.topk_fallback_chunks(ws)
+    assert n_fb > 0
+    ids, lp, lse = P.presto_topk(dl[:1].contiguous(), k, workspace=ws)
+    torch.cuda.synchronize()
+    _compare(np.ascontiguousarray(store[:1]), "bf16", k, ids, lp, lse)
+    assert P.topk_fallback_chunks(ws) == 0

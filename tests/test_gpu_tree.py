@@ -163,3 +163,39 @@ def test_tree_per_sequence_lambda_random():
     lam[::5] = 0.0
     g, o = _gpu_and_oracle(ids, lp, R, lam, root, D, k, B, branch=4)
     _assert_same(g, o)
+
+
+@pytest.mark.parametrize("B", [128, 256, 512, 1023])
+@pytest.mark.parametrize("mode", ["best_first", "beam10", "alg2"])
+def test_tree_paper_operating_point(B, mode):
+    """Sec. 5.1's operating point: k = 10 candidates per position from the
+    16-position block of the single-sequence workload, beam width 10, budgets
+    128, 256, 512 (and 1023: N = 1024 rows, the largest tree Table 1's budget
+    range reaches).  The 64,000-byte trigram lattice of k = 10 is read from
+    LDS at every budget."""
+    w, rin = round_data(2)
+    k, D = 10, w.depth
+    ids, lp, _, _ = oracle.topk(rin["drafter_logits"], k, w.dtype)
+    ids, lp = ids.reshape(1, D, k), lp.reshape(1, D, k)
+    rho = sy.rho_lattice(w.with_(k=k))
+    print(f"paper point mode={mode} B={B}", flush=True)
+    g, o = _gpu_and_oracle(ids, lp, rho, rin["lam"], rin["root_token"], D, k, B,
+                           beam_width=10 if mode == "beam10" else 0, alg2=mode == "alg2")
+    _assert_same(g, o)
+    assert int(g["n_nodes"][0]) == B + 1
+
+
+@pytest.mark.parametrize("D,k,branch,B", [(16, 10, 10, 1023), (24, 16, 16, 1023), (9, 3, 3, 700),
+                                          (16, 10, 6, 777)])
+@pytest.mark.parametrize("mode", ["best_first", "beam10", "alg2"])
+def test_tree_large_budgets_random(D, k, branch, B, mode):
+    """Budgets above 511 on random and tie-heavy tables, every mode, with
+    k = 16 (the lattice is read from global memory: 393 KB per sequence) and
+    branch < k among them."""
+    for quant in (False, True):
+        ids, lp, R, root = _random_batch([D, k, B, int(quant), 9], 6, D, k, quant)
+        for lam_v, rho in ((0.2, R), (1.0, None)):
+            lam = np.full(D, lam_v, np.float32)
+            g, o = _gpu_and_oracle(ids, lp, rho, lam, root, D, k, B, branch=branch,
+                                   beam_width=10 if mode == "beam10" else 0, alg2=mode == "alg2")
+            _assert_same(g, o)

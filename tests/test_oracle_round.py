@@ -5,7 +5,7 @@
   old cache plus its root path (recomputed from parent pointers); the new
   rows are that root path in depth order; nothing else moves; an overflow
   leaves the sequence as it was.
-* slot selection and flattening: the Appendix E walk-through worked by hand
+* slot selection and flattening: the Appendix C walk-through worked by hand
   (tests/golden/self_spec_round.json); the node rows of the flattened mask
   equal the tree's own ancestor mask; node rows of the composite attention
   equal plain tree attention (they never see a slot).
