@@ -23,7 +23,9 @@
  *   caller-provided device workspace of at least *_workspace() bytes
  *   (a null workspace is allowed when that size is 0).  Its contents on
  *   entry are ignored; two calls in flight at the same time (on different
- *   streams) need distinct workspaces.
+ *   streams) need distinct workspaces.  The one exception,
+ *   presto_topk_noalloc, uses a fixed static device array of the library
+ *   instead of a workspace.
  * - Every call is asynchronous on `stream` (0 = the null stream).  All
  *   argument checks happen on the host before anything is launched; on an
  *   error return nothing was enqueued.
@@ -107,6 +109,25 @@ presto_status presto_topk(presto_dtype dt, const void *logits, int64_t rows, int
                           int64_t row_stride, int32_t k, int32_t *ids, float *logprob, float *lse,
                           float *entropy, int32_t *flags, void *ws, size_t ws_bytes,
                           hipStream_t stream);
+
+/* presto_topk for callers that cannot allocate: code under HIP graph
+ * capture, serving loops and harnesses that forbid device allocation.  Same
+ * arguments, results and limits as presto_topk, without the workspace: the
+ * partials live in a static device array of
+ * PRESTO_TOPK_NOALLOC_SCRATCH_BYTES per GPU (held from the first call on
+ * that GPU until the process ends).  A request whose
+ * presto_topk_workspace(rows, vocab, k) exceeds it returns
+ * PRESTO_ERR_WORKSPACE with nothing launched (at vocab 151936 that is more
+ * than about 2500 rows at k = 4, 800 at k = 16).  Every call on one GPU
+ * shares the array: calls that overlap on one GPU (on different streams)
+ * race; calls ordered on one stream do not.  The workspace diagnostic of
+ * presto_topk is not available here.
+ */
+#define PRESTO_TOPK_NOALLOC_SCRATCH_BYTES ((size_t)16 << 20)
+presto_status presto_topk_noalloc(presto_dtype dt, const void *logits, int64_t rows,
+                                  int32_t vocab, int64_t row_stride, int32_t k, int32_t *ids,
+                                  float *logprob, float *lse, float *entropy, int32_t *flags,
+                                  hipStream_t stream);
 
 /* The same on gathered rows: output row r reads logits row row_index[r]
  * (int64 device, [rows]) of logits [logits_rows, row_stride].  An index

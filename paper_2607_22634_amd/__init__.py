@@ -14,5 +14,6 @@ from ._lib import (  # noqa: F401
     PRESTO_OK, PRESTO_TREE_BEAM, PRESTO_TREE_BEST_FIRST, PRESTO_TREE_BEST_FIRST_ALG2, AttnDesc,
     PrestoError, TreeDesc, lib, presto_accept, presto_build_tree, presto_entropy_lambda, presto_ngram_clear,
     presto_ngram_gather, presto_ngram_insert, presto_ngram_table_bytes, presto_topk,
+    presto_topk_noalloc,
     presto_tree_attention, topk_fallback_chunks, topk_workspace, version,
 )

@@ -40,7 +40,8 @@ PRESTO_CTX_PACKED = 0
 PRESTO_CTX_SLOTS = 1
 
 EXPORTS = (
-    "presto_topk_workspace", "presto_topk", "presto_entropy_lambda", "presto_ngram_table_bytes",
+    "presto_topk_workspace", "presto_topk", "presto_topk_noalloc", "presto_entropy_lambda",
+    "presto_ngram_table_bytes",
     "presto_ngram_clear", "presto_ngram_insert", "presto_ngram_gather", "presto_build_tree_workspace",
     "presto_build_tree",
     "presto_tree_attention_workspace", "presto_tree_attention", "presto_accept_workspace",
@@ -88,6 +89,8 @@ def lib() -> ctypes.CDLL:
         L.presto_topk_workspace.restype = _SZ
         L.presto_topk.argtypes = [_I32, _VP, _I64, _I32, _I64, _I32] + [_VP] * 6 + [_SZ, _VP]
         L.presto_topk.restype = _I32
+        L.presto_topk_noalloc.argtypes = [_I32, _VP, _I64, _I32, _I64, _I32] + [_VP] * 6
+        L.presto_topk_noalloc.restype = _I32
         L.presto_entropy_lambda.argtypes = [_I64, _VP, ctypes.c_float, ctypes.c_float, _VP, _VP]
         L.presto_entropy_lambda.restype = _I32
         L.presto_ngram_table_bytes.argtypes = [_I64]
@@ -199,6 +202,28 @@ def presto_topk(logits: torch.Tensor, k: int, *, ids=None, logprob=None, lse=Non
                              _ptr(logprob), _ptr(lse), _ptr(h), _ptr(flags), _ptr(ws), nb,
                              _stream(stream)),
            "presto_topk")
+    return (ids, logprob, lse, h) if want_h else (ids, logprob, lse)
+
+
+def presto_topk_noalloc(logits: torch.Tensor, k: int, *, ids=None, logprob=None, lse=None,
+                        entropy=None, flags=None, stream=None):
+    """presto_topk without a workspace (the library's static scratch; for
+    callers that cannot allocate).  Returns (ids, logprob, lse[, entropy])."""
+    _rows(logits)
+    rows, V = logits.shape
+    dev = logits.device
+    ids = torch.empty(rows, k, dtype=torch.int32, device=dev) if ids is None else ids
+    logprob = torch.empty(rows, k, dtype=torch.float32, device=dev) if logprob is None else logprob
+    lse = torch.empty(rows, dtype=torch.float32, device=dev) if lse is None else lse
+    want_h = entropy is not None and entropy is not False
+    if entropy is True:
+        entropy = torch.empty(rows, dtype=torch.float32, device=dev)
+    h = entropy if want_h else None
+    _dev(ids, logprob, lse, h, flags)
+    _check(lib().presto_topk_noalloc(_dt(logits), _ptr(logits), rows, V, logits.stride(0), k,
+                                     _ptr(ids), _ptr(logprob), _ptr(lse), _ptr(h), _ptr(flags),
+                                     _stream(stream)),
+           "presto_topk_noalloc")
     return (ids, logprob, lse, h) if want_h else (ids, logprob, lse)
 
 

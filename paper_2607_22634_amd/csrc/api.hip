@@ -11,6 +11,9 @@
 namespace presto_host {
 
 size_t topk_workspace_bytes(int64_t rows, int32_t vocab, int32_t k);
+presto_status launch_topk_noalloc(bool bf16, const void* logits, int64_t rows, int32_t vocab,
+                                  int64_t row_stride, int32_t k, int32_t* ids, float* logprob,
+                                  float* lse, float* entropy, int32_t* flags, hipStream_t stream);
 presto_status launch_entropy_lambda(int64_t rows, const float* entropy, float beta, float c,
                                     float* lambda, hipStream_t stream);
 presto_status launch_topk(bool bf16, const void* logits, const int64_t* row_index,
@@ -118,6 +121,25 @@ presto_status presto_topk(presto_dtype dt, const void* logits, int64_t rows, int
     if (st != PRESTO_OK) return st;
     return launch_topk(dt == PRESTO_DT_BF16, logits, nullptr, rows, rows, vocab, row_stride, k, ids,
                        logprob, lse, entropy, flags, ws, stream);
+}
+
+presto_status presto_topk_noalloc(presto_dtype dt, const void* logits, int64_t rows,
+                                  int32_t vocab, int64_t row_stride, int32_t k, int32_t* ids,
+                                  float* logprob, float* lse, float* entropy, int32_t* flags,
+                                  hipStream_t stream) {
+    g_err[0] = 0;
+    REQUIRE(valid_dtype(dt), "presto_topk_noalloc: unknown dtype %d", (int)dt);
+    REQUIRE(rows >= 0, "presto_topk_noalloc: rows < 0");
+    REQUIRE(vocab >= 1, "presto_topk_noalloc: vocab < 1");
+    REQUIRE(k >= 1 && k <= vocab, "presto_topk_noalloc: k=%d outside 1..vocab", k);
+    REQUIRE(row_stride >= vocab, "presto_topk_noalloc: row_stride < vocab");
+    if (k > 16) return set_error(PRESTO_ERR_UNSUPPORTED, "presto_topk_noalloc: k=%d > 16", k);
+    if (rows == 0) return PRESTO_OK;
+    REQUIRE(logits && ids && logprob, "presto_topk_noalloc: null pointer");
+    REQUIRE(rows * (int64_t)((vocab + 1023) / 1024) < (int64_t)1 << 31,
+            "presto_topk_noalloc: too many rows");
+    return launch_topk_noalloc(dt == PRESTO_DT_BF16, logits, rows, vocab, row_stride, k, ids,
+                               logprob, lse, entropy, flags, stream);
 }
 
 presto_status presto_topk_rows(presto_dtype dt, const void* logits, int64_t logits_rows,

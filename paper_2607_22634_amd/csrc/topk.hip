@@ -18,10 +18,13 @@
 // with one wave per row.
 #include <math.h>
 
+#include <mutex>
+
 #include "common.hpp"
 
 namespace presto {
 
+constexpr int kMaxDevices = 64;
 constexpr int kCandCap = 256;  // values of candidate groups a wave's list holds
 constexpr int kTopkWavesPerBlock = 4;
 constexpr float kLog2eF = 1.4426950408889634f;
@@ -476,6 +479,53 @@ presto_status launch_topk(bool bf16, const void* logits, const int64_t* row_inde
 #undef PRESTO_MERGE2
 #undef PRESTO_MERGE
     return check_launch("topk_merge_kernel");
+}
+
+// ---------------------------------------------------------------------------
+// Top-k without a caller workspace, for callers that cannot allocate (code
+// under graph capture, serving loops that forbid allocation).  The partials
+// live in one static device array per GPU; every call on a GPU shares it, so
+// calls that overlap on one GPU race.  Nothing in it needs to start at zero
+// (the fallback counter is cleared by the partial kernel of each call).
+
+constexpr size_t kTopkScratchBytes = PRESTO_TOPK_NOALLOC_SCRATCH_BYTES;
+static __device__ __align__(256) unsigned char scratch[kTopkScratchBytes];
+
+static std::mutex g_scratch_mu;
+static void* g_scratch_ptr[kMaxDevices];  // this device's address of `scratch`
+
+presto_status launch_topk_noalloc(bool bf16, const void* logits, int64_t rows, int32_t vocab,
+                                  int64_t row_stride, int32_t k, int32_t* ids, float* logprob,
+                                  float* lse, float* entropy, int32_t* flags, hipStream_t stream) {
+    const size_t need = topk_workspace_bytes(rows, vocab, k);
+    if (need > kTopkScratchBytes)
+        return set_error(PRESTO_ERR_WORKSPACE,
+                         "presto_topk_noalloc: %zu bytes of scratch needed, the static scratch "
+                         "holds %zu (fewer rows per call)",
+                         need, kTopkScratchBytes);
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess)
+        return set_error(PRESTO_ERR_HIP, "presto_topk_noalloc: hipGetDevice: %s", hipGetErrorString(e));
+    if (dev < 0 || dev >= kMaxDevices)
+        return set_error(PRESTO_ERR_UNSUPPORTED, "presto_topk_noalloc: device %d", dev);
+    void* ptr;
+    {
+        std::lock_guard<std::mutex> lock(g_scratch_mu);
+        if (g_scratch_ptr[dev] == nullptr) {
+            // the array's name is a host-side stand-in: its device address
+            // (one per GPU) comes from the runtime, with this device current
+            void* p = nullptr;
+            e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+            if (e != hipSuccess || p == nullptr)
+                return set_error(PRESTO_ERR_HIP, "presto_topk_noalloc: hipGetSymbolAddress: %s",
+                                 hipGetErrorString(e));
+            g_scratch_ptr[dev] = p;
+        }
+        ptr = g_scratch_ptr[dev];
+    }
+    return launch_topk(bf16, logits, nullptr, rows, rows, vocab, row_stride, k, ids, logprob, lse,
+                       entropy, flags, ptr, stream);
 }
 
 presto_status launch_entropy_lambda(int64_t rows, const float* entropy, float beta, float c,
