@@ -54,10 +54,13 @@ typedef enum {
     PRESTO_ERR_INVALID_ARG = -1, /* rejected on the host; nothing launched          */
     PRESTO_ERR_UNSUPPORTED = -2, /* valid request the library does not implement   */
     PRESTO_ERR_WORKSPACE = -3,   /* workspace missing or smaller than *_workspace() */
-    PRESTO_ERR_HIP = -4          /* HIP runtime error; see presto_last_error()      */
+    PRESTO_ERR_HIP = -4,         /* HIP runtime error; see presto_last_error()      */
+    PRESTO_STATUS_MAX_ENUM_ = 0x7fffffff /* not a status: keeps the type 32 bits wide */
 } presto_status;
 
-typedef enum { PRESTO_DT_BF16 = 0, PRESTO_DT_F32 = 1 } presto_dtype;
+/* Any other non-negative value is rejected with PRESTO_ERR_INVALID_ARG (the
+ * last enumerator only keeps the type 32 bits wide). */
+typedef enum { PRESTO_DT_BF16 = 0, PRESTO_DT_F32 = 1, PRESTO_DT_MAX_ENUM_ = 0x7fffffff } presto_dtype;
 
 typedef enum {
     PRESTO_TREE_BEST_FIRST = 0,      /* commit on pop: exactly the B best prefixes by S        */

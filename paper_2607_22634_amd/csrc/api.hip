@@ -88,6 +88,12 @@ using namespace presto_host;
 
 static bool valid_dtype(presto_dtype dt) { return dt == PRESTO_DT_BF16 || dt == PRESTO_DT_F32; }
 
+// rows x (1024-entry chunks of the vocabulary) stays below 2^31 (the
+// kernels' wave index); checked by division, so that no product overflows
+static bool rows_fit(int64_t rows, int32_t vocab) {
+    return rows >= 0 && vocab >= 1 && rows < (((int64_t)1 << 31) - 1) / ((vocab + 1023) / 1024);
+}
+
 static presto_status check_ws(void* ws, size_t have, size_t need) {
     if (need > 0 && (ws == nullptr || have < need))
         return set_error(PRESTO_ERR_WORKSPACE, "workspace of %zu bytes needed, %zu given", need,
@@ -98,7 +104,7 @@ static presto_status check_ws(void* ws, size_t have, size_t need) {
 extern "C" {
 
 size_t presto_topk_workspace(int64_t rows, int32_t vocab, int32_t k) {
-    if (rows <= 0 || vocab <= 0 || k <= 0) return 0;
+    if (rows <= 0 || vocab <= 0 || k <= 0 || k > 16 || !rows_fit(rows, vocab)) return 0;
     return topk_workspace_bytes(rows, vocab, k);
 }
 
@@ -115,7 +121,7 @@ presto_status presto_topk(presto_dtype dt, const void* logits, int64_t rows, int
     if (k > 16) return set_error(PRESTO_ERR_UNSUPPORTED, "presto_topk: k=%d > 16", k);
     if (rows == 0) return PRESTO_OK;
     REQUIRE(logits && ids && logprob, "presto_topk: null pointer");
-    REQUIRE(rows * (int64_t)((vocab + 1023) / 1024) < (int64_t)1 << 31,
+    REQUIRE(rows_fit(rows, vocab),
             "presto_topk: too many rows");
     presto_status st = check_ws(ws, ws_bytes, presto_topk_workspace(rows, vocab, k));
     if (st != PRESTO_OK) return st;
@@ -136,7 +142,7 @@ presto_status presto_topk_noalloc(presto_dtype dt, const void* logits, int64_t r
     if (k > 16) return set_error(PRESTO_ERR_UNSUPPORTED, "presto_topk_noalloc: k=%d > 16", k);
     if (rows == 0) return PRESTO_OK;
     REQUIRE(logits && ids && logprob, "presto_topk_noalloc: null pointer");
-    REQUIRE(rows * (int64_t)((vocab + 1023) / 1024) < (int64_t)1 << 31,
+    REQUIRE(rows_fit(rows, vocab),
             "presto_topk_noalloc: too many rows");
     return launch_topk_noalloc(dt == PRESTO_DT_BF16, logits, rows, vocab, row_stride, k, ids,
                                logprob, lse, entropy, flags, stream);
@@ -157,7 +163,7 @@ presto_status presto_topk_rows(presto_dtype dt, const void* logits, int64_t logi
     if (rows == 0) return PRESTO_OK;
     REQUIRE(logits && row_index && ids && logprob, "presto_topk_rows: null pointer");
     REQUIRE(logits_rows >= 1, "presto_topk_rows: no logits rows");
-    REQUIRE(rows * (int64_t)((vocab + 1023) / 1024) < (int64_t)1 << 31,
+    REQUIRE(rows_fit(rows, vocab),
             "presto_topk_rows: too many rows");
     presto_status st = check_ws(ws, ws_bytes, presto_topk_workspace(rows, vocab, k));
     if (st != PRESTO_OK) return st;
@@ -416,6 +422,7 @@ const char* presto_status_string(presto_status s) {
         case PRESTO_ERR_UNSUPPORTED: return "unsupported";
         case PRESTO_ERR_WORKSPACE: return "workspace too small";
         case PRESTO_ERR_HIP: return "HIP error";
+        default: break;
     }
     return "unknown status";
 }
