@@ -27,6 +27,8 @@
 // sum (bf16), which a second kernel merges.
 #include <math.h>
 
+#include <type_traits>
+
 #include "common.hpp"
 
 namespace presto {
@@ -45,17 +47,13 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
 
 constexpr int kKeyTile = 64;      // keys per LDS tile: two 32-key blocks per barrier
 constexpr int kBlocksPerTile = kKeyTile / 32;
-constexpr int kBufs = 3;          // LDS tile buffers
-constexpr float kSlack = 8.f;     // log2 headroom before the accumulator is rescaled
+constexpr int kRing = 4;          // LDS tile buffers: tile t consumed, t+1 resident, t+2 and t+3 in flight
 constexpr int kMaxAncWords = 16;  // ancestor words per node: n_max <= 1024
 constexpr int kRowsPerWave = 32;  // one 32-row MFMA block per wave
-// Workgroups are 8 waves, two per SIMD: one wave's softmax hides behind the
-// other's MFMAs (with one wave per SIMD the matrix cores sit idle during it).
+// Workgroups are 8 waves, two per SIMD, so that one wave's vector work runs
+// while the other's MFMAs occupy the matrix core.
 constexpr int kAttnWaves = 8;
-// 32-row blocks per wave.  Two (four waves, each K/V fragment feeding two
-// MFMAs) needs about 340 registers per lane at head_dim 128 and spills with
-// the current register allocation, so one block per wave is used.
-constexpr int kAttnRowBlocks = 1;
+constexpr int kAttnRows = kAttnWaves * kRowsPerWave;  // query rows per workgroup
 constexpr float kLog2e = 1.4426950408889634f;
 
 struct AttnArgs {
@@ -103,55 +101,54 @@ __device__ __forceinline__ int xcd_task(int bid, int n_blocks) {
     return (bid & 7) * per + (bid >> 3);
 }
 
-// This thread's PT 16-byte pieces of one K tile and one V tile.
-template <int PT>
-struct TilePieces {
-    uint4 k[PT], v[PT];
-};
-
-// Loads this thread's pieces of the K and V tile that starts at key t0.
-// Keys below ctx come from the packed cache row c0 + j, the others from the
-// tree K/V of node j - ctx; rows past k_end repeat the last key (every load
-// stays in bounds; their scores are masked to -inf).
-template <int D, int PT, int NT>
-__device__ __forceinline__ TilePieces<PT> fetch_tile(const uint16_t* kc, const uint16_t* vc,
-                                                     const uint16_t* kt, const uint16_t* vt, int tid,
-                                                     int t0, int k_end, int ctx, int c0, int hkv,
-                                                     int g, int64_t tree_row0) {
-    const int64_t kv_stride = (int64_t)hkv * D;
-    TilePieces<PT> r;
-#pragma unroll
-    for (int i = 0; i < PT; ++i) {
-        const int p = tid + i * NT;
-        const int kk = p / (D / 8), c8 = p % (D / 8);
-        const int j = min(t0 + kk, k_end - 1);
-        const bool in_ctx = j < ctx;
-        const int64_t off = in_ctx ? (int64_t)(c0 + j) * kv_stride + (int64_t)g * D + c8 * 8
-                                   : ((tree_row0 + (j - ctx)) * hkv + g) * D + c8 * 8;
-        const uint16_t* kp = in_ctx ? kc : kt;
-        const uint16_t* vp = in_ctx ? vc : vt;
-        r.k[i] = *reinterpret_cast<const uint4*>(kp + off);
-        r.v[i] = *reinterpret_cast<const uint4*>(vp + off);
-    }
-    return r;
+// LDS layout of the bf16 kernel (bytes).  A K tile is 64 key rows of D
+// bf16 (D*2 bytes, no padding) with the 16-byte chunks of row r permuted by
+// chunk ^ (r mod 16); a V tile likewise with chunk ^ 4(r mod 4).  The two
+// permutations make the fragment reads free of bank conflicts (sixteen
+// consecutive K rows read one chunk each: sixteen different chunks; the
+// transposed V reads of four consecutive rows cover four disjoint 64-byte
+// chunk groups), and since the global-to-LDS loads write 64 consecutive
+// 16-byte chunks per instruction, the permutation is applied by choosing
+// which global chunk each lane fetches.  K tiles of the ring sit in the
+// first 64 KB and V tiles in the second, so that every fragment read is a
+// per-lane base register plus an immediate offset.
+// Global-to-LDS load of 16 bytes per lane (global_load_lds_dwordx4): lane
+// l's bytes land at LDS address lds + 16 l (lds wave-uniform, in m0).  The
+// instruction is issued from inline assembly so that the compiler does not
+// guard every later LDS read with a wait for all outstanding loads; the
+// kernel waits for each tile itself (vmcnt) before the barrier that
+// publishes it.
+__device__ __forceinline__ void lds_load16(const void* gptr, uint32_t lds) {
+    asm volatile("global_load_lds_dwordx4 %0, off" ::"v"(gptr), "{m0}"(lds) : "memory");
+}
+// the same with a wave-uniform base and a per-lane 32-bit byte offset
+__device__ __forceinline__ void lds_load16(const void* base, uint32_t off, uint32_t lds) {
+    asm volatile("global_load_lds_dwordx4 %0, %1" ::"v"(off), "s"(base), "{m0}"(lds) : "memory");
 }
 
-template <int D, int NW, int RB>
-__global__ __launch_bounds__(NW * kWave) void tree_attn_bf16_kernel(AttnArgs a) {
+template <int D>
+struct AttnLds {
+    static constexpr int kTile = kKeyTile * D * 2;           // bytes of one K (or V) tile
+    static constexpr int kV = kRing * kTile;                 // start of the V tiles
+};
+
+template <int D>
+__global__ __launch_bounds__(kAttnWaves * kWave) void tree_attn_bf16_kernel(AttnArgs a) {
     constexpr int KS = D / 16;                 // S^T contraction steps over the head dimension
     constexpr int DB = D / 32;                 // 32-wide blocks of the output head dimension
-    constexpr int KROW = D + 8;                // K row in LDS (bf16): conflict-free b128 reads
-    constexpr int VROW = D + 32;               // V row in LDS: conflict-free transposed b64 reads
-    constexpr int PIECES = kKeyTile * D / 8;   // 16-byte pieces of one K (or V) tile
-    constexpr int NT = NW * kWave;
-    constexpr int PT = PIECES / NT;            // pieces per thread
-    constexpr int WROWS = RB * kRowsPerWave;   // query rows per wave (RB blocks of 32)
-    constexpr int ROWS = NW * WROWS;           // query rows per workgroup
-    constexpr int KBUF = kKeyTile * KROW, VBUF = kKeyTile * VROW;
-    static_assert(PT * NT == PIECES, "tile pieces must divide evenly");
-    __shared__ __align__(16) uint16_t sK[kBufs * KBUF];
-    __shared__ __align__(16) uint16_t sV[kBufs * VBUF];
-    __shared__ uint64_t s_anc[(ROWS + 1) * kMaxAncWords];  // ancestor rows of this tile's nodes
+    constexpr int CH = D / 8;                  // 16-byte chunks per K/V row
+    constexpr int NT = kAttnWaves * kWave;
+    constexpr int ROWS = kAttnRows;
+    // global-to-LDS loads per thread per tile, K and V each: 64 rows x CH
+    // chunks, 64 chunks per instruction
+    constexpr int LPT = kKeyTile * CH / 64 / kAttnWaves;
+    constexpr int ROWS_PER_LOAD = 64 / CH;     // key rows covered by one load instruction
+    static_assert(LPT >= 1 && LPT * kAttnWaves * 64 == kKeyTile * CH, "tile loads must divide evenly");
+    static_assert(AttnLds<D>::kV + kRing * AttnLds<D>::kTile <= 65536 * 2, "ring must fit 128 KB");
+    __shared__ __align__(16) char s_kv[2 * kRing * AttnLds<D>::kTile];
+    // ancestor rows of this workgroup's nodes: at most ROWS nodes (G = 1)
+    // of at most kMaxAncWords words; with the ring this is 160 KB at D = 128
+    __shared__ uint64_t s_anc[ROWS * kMaxAncWords];
 
     int task, split, g, b;
     if (a.compact) {
@@ -225,79 +222,31 @@ __global__ __launch_bounds__(NW * kWave) void tree_attn_bf16_kernel(AttnArgs a) 
     const int tid = threadIdx.x;
     const int wave = tid / kWave, lane = lane_id();
     const int l32 = lane & 31, h = lane >> 5;
-    const int row0 = rt * ROWS + wave * WROWS;  // first query row of this wave
+    const int row0 = rt * ROWS + wave * kRowsPerWave;  // first query row of this wave
     const bool active = row0 < live_rows;
-    int rho[RB], qn[RB], qh[RB], node[RB];  // this lane's query row in each row block
-#pragma unroll
-    for (int rb = 0; rb < RB; ++rb) {
-        rho[rb] = row0 + rb * kRowsPerWave + l32;
-        qn[rb] = rho[rb] / a.G;
-        qh[rb] = rho[rb] - qn[rb] * a.G;
-        node[rb] = min(qn[rb], a.n_max - 1);
-    }
+    const int rho = row0 + l32;  // this lane's query row
+    const int qn = rho / a.G, qh = rho - qn * a.G;
+    const int node = min(qn, a.n_max - 1);
+    const float c = a.scale_log2;
 
-    // Q fragments, B operand of S^T = K Q^T: lane holds row l32, d = ks*16 + h*8 .. +8.
-    // Loaded before the first K/V tiles, so the waits for those tiles also
-    // cover Q and nothing in the key loop waits on global loads but the stage.
-    bf16x8 qf[RB][KS];
-#pragma unroll
-    for (int rb = 0; rb < RB; ++rb) {
-        const uint16_t* qp = a.q + (((int64_t)b * a.n_max + qn[rb]) * a.hq + g * a.G + qh[rb]) * D;
+    // Q fragments, B operand of S^T = K Q^T: lane holds row l32,
+    // d = ks*16 + h*8 .. +8, pre-scaled by scale*log2(e) (rounded once to
+    // bf16), so that the scores come out in log2 units.
+    bf16x8 qf[KS];
+    {
+        const uint16_t* qp = a.q + (((int64_t)b * a.n_max + qn) * a.hq + g * a.G + qh) * D;
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks) {
             uint4 u = make_uint4(0, 0, 0, 0);
-            if (rho[rb] < all_rows) u = *reinterpret_cast<const uint4*>(qp + ks * 16 + h * 8);
-            qf[rb][ks] = __builtin_bit_cast(bf16x8, u);
+            if (rho < all_rows) u = *reinterpret_cast<const uint4*>(qp + ks * 16 + h * 8);
+            const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+            uint32_t r[4];
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+                r[j] = pack_bf16x2(__uint_as_float(w[j] << 16) * c, __uint_as_float(w[j] & 0xffff0000u) * c);
+            qf[ks] = __builtin_bit_cast(bf16x8, make_uint4(r[0], r[1], r[2], r[3]));
         }
     }
-
-    // ---- K/V staging: global -> registers -> LDS, three buffers: while tile t
-    // is consumed, tile t+1 is already in LDS (the last block of a tile scores
-    // the first block of the next one) and tile t+2 is in flight.
-    // A tile wholly inside the context is read at a uniform base plus a
-    // per-thread 32-bit byte offset fixed for the whole loop (no per-tile
-    // address arithmetic); other tiles take the general path.
-    const int fast_end = min(ctx, k_end);
-    uint32_t piece_off[PT];
-#pragma unroll
-    for (int i = 0; i < PT; ++i) {
-        const int p = tid + i * NT;
-        piece_off[i] = (uint32_t)(((p / (D / 8)) * a.hkv * D + (p % (D / 8)) * 8) * 2);
-    }
-    auto fetch = [&](int t0) {
-        if (t0 + kKeyTile <= fast_end) {
-            const int64_t row = ((int64_t)(c0 + t0) * a.hkv + g) * D;
-            const char* kb = reinterpret_cast<const char*>(a.kc + row);
-            const char* vb = reinterpret_cast<const char*>(a.vc + row);
-            TilePieces<PT> r;
-#pragma unroll
-            for (int i = 0; i < PT; ++i) {
-                r.k[i] = *reinterpret_cast<const uint4*>(kb + piece_off[i]);
-                r.v[i] = *reinterpret_cast<const uint4*>(vb + piece_off[i]);
-            }
-            return r;
-        }
-        return fetch_tile<D, PT, NT>(a.kc, a.vc, a.kt, a.vt, tid, t0, k_end, ctx, c0, a.hkv, g,
-                                     (int64_t)b * a.n_max);
-    };
-    auto stage = [&](int buf, const TilePieces<PT>& tp) {
-#pragma unroll
-        for (int i = 0; i < PT; ++i) {
-            const int p = tid + i * NT;
-            const int kk = p / (D / 8), c8 = p % (D / 8);
-            *reinterpret_cast<uint4*>(&sK[buf * KBUF + kk * KROW + c8 * 8]) = tp.k[i];
-            *reinterpret_cast<uint4*>(&sV[buf * VBUF + kk * VROW + c8 * 8]) = tp.v[i];
-        }
-    };
-    // unconditional: tiles past the split only repeat the last key, and a
-    // buffer staged with them is never read
-    TilePieces<PT> pend = fetch(k_begin);
-    {
-        const TilePieces<PT> second = fetch(k_begin + kKeyTile);
-        stage(0, pend);
-        stage(1, second);
-    }
-    pend = fetch(k_begin + 2 * kKeyTile);
     // ancestor bitmask rows of the nodes this workgroup serves, when the
     // split reaches the tree keys (masks then read LDS, not global memory)
     const int n_first = (rt * ROWS) / a.G;
@@ -307,51 +256,93 @@ __global__ __launch_bounds__(NW * kWave) void tree_attn_bf16_kernel(AttnArgs a) 
         const uint64_t* src = a.anc + ((int64_t)b * a.n_max + n_first) * a.W;
         for (int w = tid; w < words; w += NT) s_anc[w] = src[w];
     }
-    __syncthreads();
 
-    floatx16 o[RB][DB];
+    // ---- K/V tiles: global -> LDS directly (global_load_lds_dwordx4), a
+    // ring of kRing tiles.  Load instruction j of this wave covers key rows
+    // ROWS_PER_LOAD * (wave * LPT + j) .. of the tile; lane l writes chunk
+    // l % CH of row l / CH and so fetches the global chunk that the row's
+    // permutation puts there.  The byte offsets of those chunks within a
+    // tile that lies wholly in the cache are fixed for the whole loop.
+    uint32_t goff_k[LPT], goff_v[LPT];
+    int lrow[LPT], lck[LPT], lcv[LPT];
 #pragma unroll
-    for (int rb = 0; rb < RB; ++rb)
-#pragma unroll
-        for (int db = 0; db < DB; ++db)
-#pragma unroll
-            for (int i = 0; i < 16; ++i) o[rb][db][i] = 0.f;
-    // Running reference m (log2 domain, scaled) and denominator l per row.
-    // m only moves when a block's maximum exceeds it by more than kSlack, so
-    // most blocks skip the accumulator rescale; probabilities stay below
-    // 2^kSlack.
-    float m_run[RB], l_run[RB];
-#pragma unroll
-    for (int rb = 0; rb < RB; ++rb) {
-        m_run[rb] = -INFINITY;
-        l_run[rb] = 0.f;
+    for (int j = 0; j < LPT; ++j) {
+        const int r = ROWS_PER_LOAD * (wave * LPT + j) + lane / CH;
+        const int pc = lane % CH;
+        lrow[j] = r;
+        lck[j] = pc ^ (r & (CH - 1) & 15);
+        lcv[j] = pc ^ ((4 * (r & 3)) & (CH - 1));
+        goff_k[j] = (uint32_t)((r * a.hkv * D + lck[j] * 8) * 2);
+        goff_v[j] = (uint32_t)((r * a.hkv * D + lcv[j] * 8) * 2);
     }
-
-    const float c = a.scale_log2;
-    // per-lane LDS element offsets; every fragment read adds only a constant
-    const int k_lane = l32 * KROW + h * 8;
-    const int v_lane = (4 * h + ((lane & 15) >> 2)) * VROW + ((lane >> 4) & 1) * 16 + 4 * (lane & 3);
-
-    // S^T blocks of 32 keys (block i of the split) for every row block: each
-    // K fragment read from LDS feeds RB MFMAs
-    auto scores = [&](int i, floatx16 (&S)[RB]) {
+    const int fast_end = min(ctx, k_end);
+    const int64_t tree_row0 = (int64_t)b * a.n_max;
+    // all loads of the tile starting at key t0 into ring buffer `buf`
+    const uint32_t lds_kv = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char*)s_kv;
+    // the four base pointers as scalars: a per-lane choice between them is
+    // then a register select, not a load from the argument block
+    auto scalar_ptr = [](const uint16_t* ptr) {
+        const uint64_t v = (uint64_t)(uintptr_t)ptr;
+        const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)v);
+        const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(v >> 32));
+        return (const uint16_t*)(uintptr_t)(((uint64_t)hi << 32) | lo);
+    };
+    const uint16_t* const kc_s = scalar_ptr(a.kc);
+    const uint16_t* const vc_s = scalar_ptr(a.vc);
+    const uint16_t* const kt_s = scalar_ptr(a.kt);
+    const uint16_t* const vt_s = scalar_ptr(a.vt);
+    auto load_tile = [&](int t0, int buf) {
+        const uint32_t kdst = lds_kv + buf * AttnLds<D>::kTile + wave * LPT * 1024;
+        const uint32_t vdst = kdst + AttnLds<D>::kV;
+        if (t0 + kKeyTile <= fast_end) {
+            const int64_t row = ((int64_t)(c0 + t0) * a.hkv + g) * D;
+            const uint16_t* kb = a.kc + row;
+            const uint16_t* vb = a.vc + row;
 #pragma unroll
-        for (int rb = 0; rb < RB; ++rb)
+            for (int j = 0; j < LPT; ++j) {
+                lds_load16(kb, goff_k[j], kdst + j * 1024);
+                lds_load16(vb, goff_v[j], vdst + j * 1024);
+            }
+        } else {
+            // keys below ctx from the cache, the others from the tree K/V;
+            // rows past k_end repeat the last key (their scores are masked)
 #pragma unroll
-            for (int e = 0; e < 16; ++e) S[rb][e] = 0.f;
-        const int buf = (i / kBlocksPerTile) % kBufs, blk = i % kBlocksPerTile;
-        int koff = buf * KBUF + blk * 32 * KROW + k_lane;
-        asm volatile("" : "+v"(koff));  // keep the per-read constants as immediate offsets
-        const uint16_t* kb = sK + koff;
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks) {
-            const bf16x8 ka = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(kb + ks * 16));
-#pragma unroll
-            for (int rb = 0; rb < RB; ++rb)
-                S[rb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qf[rb][ks], S[rb], 0, 0, 0);
+            for (int j = 0; j < LPT; ++j) {
+                const int kk = min(t0 + lrow[j], k_end - 1);
+                const bool in_ctx = kk < ctx;
+                const int64_t base = in_ctx ? ((int64_t)(c0 + kk) * a.hkv + g) * D
+                                            : ((tree_row0 + (kk - ctx)) * a.hkv + g) * D;
+                const uint16_t* kp = (in_ctx ? kc_s : kt_s) + base + lck[j] * 8;
+                const uint16_t* vp = (in_ctx ? vc_s : vt_s) + base + lcv[j] * 8;
+                lds_load16(kp, kdst + j * 1024);
+                lds_load16(vp, vdst + j * 1024);
+            }
         }
     };
-    // element e of a lane is key j0 + 8(e/4) + 4h + e%4
+    // vmcnt(n) with the other counters left alone (gfx9 encoding)
+#define PRESTO_WAIT_VM(n) __builtin_amdgcn_s_waitcnt(((n) & 15) | (((n) >> 4) << 14) | 0x0f70)
+
+    floatx16 o[DB];
+#pragma unroll
+    for (int db = 0; db < DB; ++db)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) o[db][i] = 0.f;
+
+    // per-lane LDS byte addresses of the fragment reads (ring buffer 0,
+    // block 0); buffer, block and step offsets are immediates
+    constexpr uint32_t lds0 = 0;  // offsets from s_kv
+    uint32_t kaddr[KS];
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks)
+        kaddr[ks] = lds0 + l32 * (D * 2) + ((((2 * ks + h) ^ (l32 & 15)) & (CH - 1)) * 16);
+    const int vr = 4 * h + ((lane & 15) >> 2);                  // row within an 8-row group
+    const int vc = ((lane >> 4) & 1) * 2 + ((lane & 3) >> 1);   // chunk within a 4-chunk group
+    uint32_t vaddr[DB];
+#pragma unroll
+    for (int db = 0; db < DB; ++db)
+        vaddr[db] = lds0 + AttnLds<D>::kV + vr * (D * 2) + (((4 * (db ^ (vr & 3))) + vc) & (CH - 1)) * 16 +
+                    (lane & 1) * 8;
+
     auto row_max = [&](const floatx16& S) {
         float mx = S[0];
 #pragma unroll
@@ -364,11 +355,11 @@ __global__ __launch_bounds__(NW * kWave) void tree_attn_bf16_kernel(AttnArgs a) 
     // mask (bit t: key j0 + t): context keys, then the row's ancestor bits
     // from tree index j0 - ctx on, cut at the split's end; each element then
     // costs one bit test and one select.
-    auto apply_mask = [&](floatx16& S, int j0, int nd) {
+    auto apply_mask = [&](floatx16& S, int j0) {
         const int s0 = j0 - ctx;  // tree index of the block's first key (< 0: it starts in the context)
         uint32_t anc = 0u;
         if (j0 + 32 > ctx) {
-            const uint64_t* arow = &s_anc[(nd - n_first) * a.W];
+            const uint64_t* arow = &s_anc[(node - n_first) * a.W];
             if (s0 >= 0) {
                 const int w = s0 >> 6, sh = s0 & 63;
                 const uint64_t lo = arow[w];
@@ -388,162 +379,196 @@ __global__ __launch_bounds__(NW * kWave) void tree_attn_bf16_kernel(AttnArgs a) 
             S[e] = ((vis >> t) & 1u) ? S[e] : -INFINITY;
         }
     };
-    // move m of row block rb when its block maximum mx (raw score) exceeds
-    // it by more than kSlack
-    auto update = [&](int rb, float mx) {
-        const float mx2 = mx * c;
-        const bool need = mx2 > m_run[rb] + kSlack;
-        if (__ballot(need)) {
-            const float mn = need ? mx2 : m_run[rb];
-            const float alpha = need ? __builtin_amdgcn_exp2f(m_run[rb] - mn) : 1.f;
-            m_run[rb] = mn;
-            l_run[rb] *= alpha;
+
+    // ---- Key loop, pipelined over three key blocks so that the matrix
+    // cores always have two independent chains and the vector ALUs work in
+    // their shadow.  Step i issues, interleaved,
+    //   * the P V MFMAs of block i (probabilities from step i-1),
+    //   * the score MFMAs of block i+2 (its tile is resident),
+    //   * the exponentials of block i+1 (scores from step i-1).
+    // Every score chain starts from -m, so the MFMAs deliver x = s*c - m and
+    // a probability costs one v_exp.  m is a lazy reference: no per-block
+    // maximum is taken; a row whose block sum exceeds 2^8 (some x above
+    // about 3) or that has no mass yet takes an exact step (block maximum,
+    // rescale of o and l), which is rare.
+    constexpr int EPK = 16 / KS;  // exponentials per score MFMA
+    static_assert(EPK * KS == 16 && EPK % 2 == 0 && KS == 2 * DB, "head_dim 64 or 128");
+    const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
+    float m = 0.f, l_run = 0.f;  // lazy reference (log2 units) and row sum
+    floatx16 negm;
 #pragma unroll
-            for (int db = 0; db < DB; ++db) o[rb][db] *= alpha;
+    for (int e = 0; e < 16; ++e) negm[e] = 0.f;
+    typedef __attribute__((address_space(3))) short4_t* lds_s4;
+    // scores of block blk of ring buffer buf (compile-time) into Sx
+    auto qk = [&](auto bufc, int blk, floatx16& Sx) {
+        constexpr int buf = decltype(bufc)::value;
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+            const uint4 u = *reinterpret_cast<const uint4*>(s_kv + kaddr[ks] + buf * AttnLds<D>::kTile +
+                                                             blk * 32 * D * 2);
+            Sx = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, u), qf[ks],
+                                                         ks == 0 ? negm : Sx, 0, 0, 0);
         }
     };
+    auto exps = [&](const floatx16& Sx, uint32_t (&Px)[8]) {
+        float ls = 0.f;
+#pragma unroll
+        for (int e = 0; e < 16; e += 2) {
+            Px[e >> 1] = pack_bf16x2(__builtin_amdgcn_exp2f(Sx[e]), __builtin_amdgcn_exp2f(Sx[e + 1]));
+            ls = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, Px[e >> 1]), ones, ls, false);
+        }
+        return ls;
+    };
+    auto row_sum = [&](float v) {
+        const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+        return v + __uint_as_float(h == 0 ? sw[1] : sw[0]);
+    };
+    // exact step for the rows that need it: move m to the block's maximum,
+    // rescale the accumulated state and recompute the block's probabilities
+    // (Sy: a block already scored against the old m, shifted along)
+    auto exact = [&](floatx16& Sx, uint32_t (&Px)[8], float& ls, bool need, floatx16& Sy) {
+        const float mx = row_max(Sx);
+        const float delta = (need && mx != -INFINITY) ? mx : 0.f;
+        const float alpha = l_run > 0.f ? __builtin_amdgcn_exp2f(-delta) : 0.f;
+        m += delta;
+        l_run *= alpha;
+#pragma unroll
+        for (int db = 0; db < DB; ++db) o[db] *= alpha;
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+            Sx[e] -= delta;
+            Sy[e] -= delta;
+            negm[e] = -m;
+        }
+        ls = row_sum(exps(Sx, Px));
+    };
+    auto j0_of = [&](int i) { return k_begin + i * 32; };
+    auto masked = [&](int i) { return j0_of(i) + 32 > mask_from; };
 
-    // one 32-key block: scores of every row block (K fragments shared), then
-    // the softmax and P V of each row block; with two row blocks one block's
-    // softmax overlaps the other's MFMAs
-    auto block_step = [&](int t, int q, int i, floatx16 (&S)[RB]) {
-        const int j0 = k_begin + i * 32;
-        float mx[RB];
-#pragma unroll
-        for (int rb = 0; rb < RB; ++rb) mx[rb] = row_max(S[rb]);
-        if (j0 + 32 > mask_from) {
-#pragma unroll
-            for (int rb = 0; rb < RB; ++rb) {
-                apply_mask(S[rb], j0, node[rb]);
-                mx[rb] = row_max(S[rb]);
-            }
-        }
-#pragma unroll
-        for (int rb = 0; rb < RB; ++rb) update(rb, mx[rb]);
-        uint32_t P[RB][8];
-#pragma unroll
-        for (int rb = 0; rb < RB; ++rb) {
-            const float m_use = m_run[rb] == -INFINITY ? 0.f : m_run[rb];
-            float ls = 0.f;
-#pragma unroll
-            for (int e = 0; e < 16; e += 2) {
-                const float p0 = __builtin_amdgcn_exp2f(fmaf(S[rb][e], c, -m_use));
-                const float p1 = __builtin_amdgcn_exp2f(fmaf(S[rb][e + 1], c, -m_use));
-                ls += p0 + p1;
-                P[rb][e >> 1] = pack_bf16x2(p0, p1);
-            }
-            l_run[rb] += ls;
-        }
-        int voff = (t % kBufs) * VBUF + q * 32 * VROW + v_lane;
-        asm volatile("" : "+v"(voff));
-        const uint16_t* vb = sV + voff;
+    floatx16 Sa = negm, Sb = negm;  // scores of blocks i+1 and i+2
+    uint32_t Pp[8];                 // probabilities of block i
+    // one block step: block i = 2 t + q; V of tile t in ring buffer bv, the
+    // K of block i+2 (tile t+1) in ring buffer bk
+    auto step = [&](auto bvc, auto bkc, int i, int q) {
+        constexpr int bv = decltype(bvc)::value, bk = decltype(bkc)::value;
+        const bool more = i + 1 < nblocks;
+        if (more && masked(i + 1)) apply_mask(Sa, j0_of(i + 1));
+        const int kblk = (i + 2) % kBlocksPerTile;
+        uint32_t Pn[8];
+        float ls = 0.f;
 #pragma unroll
         for (int st = 0; st < 2; ++st) {
+            const bf16x8 pb =
+                __builtin_bit_cast(bf16x8, make_uint4(Pp[4 * st], Pp[4 * st + 1], Pp[4 * st + 2], Pp[4 * st + 3]));
 #pragma unroll
             for (int db = 0; db < DB; ++db) {
-                const uint16_t* v0 = vb + st * 16 * VROW + db * 32;
-                const short4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-                    (__attribute__((address_space(3))) short4_t*)(v0));
-                const short4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-                    (__attribute__((address_space(3))) short4_t*)(v0 + 8 * VROW));
+                const uint32_t v0 = vaddr[db] + bv * AttnLds<D>::kTile + q * 32 * D * 2 + st * 16 * D * 2;
+                const short4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s4)(s_kv + v0));
+                const short4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s4)(s_kv + v0 + 8 * D * 2));
                 const uint2 ul = __builtin_bit_cast(uint2, lo), uh = __builtin_bit_cast(uint2, hi);
                 const bf16x8 va = __builtin_bit_cast(bf16x8, make_uint4(ul.x, ul.y, uh.x, uh.y));
+                o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pb, o[db], 0, 0, 0);
+                const int ks = st * DB + db;
+                const uint4 u = *reinterpret_cast<const uint4*>(s_kv + kaddr[ks] + bk * AttnLds<D>::kTile +
+                                                                 kblk * 32 * D * 2);
+                Sb = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, u), qf[ks],
+                                                             ks == 0 ? negm : Sb, 0, 0, 0);
 #pragma unroll
-                for (int rb = 0; rb < RB; ++rb) {
-                    const bf16x8 pb = __builtin_bit_cast(
-                        bf16x8, make_uint4(P[rb][4 * st], P[rb][4 * st + 1], P[rb][4 * st + 2], P[rb][4 * st + 3]));
-                    o[rb][db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pb, o[rb][db], 0, 0, 0);
+                for (int uu = 0; uu < EPK; uu += 2) {
+                    const int e = ks * EPK + uu;
+                    Pn[e >> 1] = pack_bf16x2(__builtin_amdgcn_exp2f(Sa[e]), __builtin_amdgcn_exp2f(Sa[e + 1]));
+                    ls = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, Pn[e >> 1]), ones, ls, false);
                 }
             }
         }
+        if (more) {
+            ls = row_sum(ls);
+            const bool need = !(ls <= 256.f) || l_run + ls == 0.f;
+            if (__ballot(need)) exact(Sa, Pn, ls, need, Sb);
+            l_run += ls;
+        }
+#pragma unroll
+        for (int j = 0; j < 8; ++j) Pp[j] = Pn[j];
+        Sa = Sb;
+    };
+    // one tile: its two block steps, then the load of tile t+3 into the
+    // buffer of tile t-1 (every wave finished it before the last barrier),
+    // and the wait for tile t+2 before the barrier
+    auto tile = [&](auto uc, int t) {
+        constexpr int u = decltype(uc)::value;
+        using BV = std::integral_constant<int, u>;
+        using BK = std::integral_constant<int, (u + 1) % kRing>;
+        load_tile(k_begin + (t + 3) * kKeyTile, (u + 3) % kRing);
+        if (active) {
+            if (2 * t < nblocks) step(BV{}, BK{}, 2 * t, 0);
+            if (2 * t + 1 < nblocks) step(BV{}, BK{}, 2 * t + 1, 1);
+        }
+        PRESTO_WAIT_VM(2 * LPT);
+        __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): this wave's LDS reads are done
+        __builtin_amdgcn_s_barrier();
     };
 
-    if constexpr (RB == 1) {
-        // one row block: the scores of block i+1 (its tile is already in LDS)
-        // are issued ahead of the softmax and P V of block i
-        floatx16 S_cur[1];
-        if (active) scores(0, S_cur);
-        for (int t = 0; t < ntiles; ++t) {
-            if (active) {
-#pragma unroll
-                for (int q = 0; q < kBlocksPerTile; ++q) {
-                    const int i = t * kBlocksPerTile + q;
-                    if (i < nblocks) {
-                        floatx16 S_nxt[1];
-                        scores(i + 1, S_nxt);
-                        block_step(t, q, i, S_cur);
-                        S_cur[0] = S_nxt[0];
-                    }
-                }
-            }
-            // tile t+2 goes into the buffer of tile t-1, which every wave
-            // finished before the previous barrier
-            stage((t + 2) % kBufs, pend);
-            pend = fetch(k_begin + (t + 3) * kKeyTile);
-            __syncthreads();
-        }
-    } else {
-        for (int t = 0; t < ntiles; ++t) {
-            if (active) {
-#pragma unroll
-                for (int q = 0; q < kBlocksPerTile; ++q) {
-                    const int i = t * kBlocksPerTile + q;
-                    if (i < nblocks) {
-                        floatx16 S[RB];
-                        scores(i, S);
-                        block_step(t, q, i, S);
-                    }
-                }
-            }
-            stage((t + 2) % kBufs, pend);
-            pend = fetch(k_begin + (t + 3) * kKeyTile);
-            __syncthreads();
-        }
+    // prologue: tiles 0..2 requested, tiles 0 and 1 awaited (and with them
+    // Q and the ancestor rows, which were requested first)
+    load_tile(k_begin, 0);
+    load_tile(k_begin + kKeyTile, 1);
+    load_tile(k_begin + 2 * kKeyTile, 2);
+    PRESTO_WAIT_VM(2 * LPT);
+    __syncthreads();
+    using B0 = std::integral_constant<int, 0>;
+    if (active) {
+        floatx16 S0 = negm;
+        qk(B0{}, 0, S0);
+        if (masked(0)) apply_mask(S0, j0_of(0));
+        float ls;
+        exact(S0, Pp, ls, true, Sb);  // m from block 0; Sb not yet live
+        l_run = ls;
+        qk(B0{}, 1, Sa);
     }
+    for (int t = 0; t < ntiles; t += kRing) {
+        tile(std::integral_constant<int, 0>{}, t);
+        if (t + 1 < ntiles) tile(std::integral_constant<int, 1>{}, t + 1);
+        if (t + 2 < ntiles) tile(std::integral_constant<int, 2>{}, t + 2);
+        if (t + 3 < ntiles) tile(std::integral_constant<int, 3>{}, t + 3);
+    }
+    PRESTO_WAIT_VM(0);  // no load into LDS outlives the workgroup
+#undef PRESTO_WAIT_VM
 
-    // ---- epilogue: lane holds row l32 of each row block, d = db*32 + 8(i/4) + 4h + i%4
+    // ---- epilogue: lane holds row l32, d = db*32 + 8(i/4) + 4h + i%4
+    if (rho >= all_rows) return;
+    const float l = l_run;  // whole-row sum
+    if (a.splits == 1) {
+        uint16_t* op = a.out + (((int64_t)b * a.n_max + qn) * a.hq + g * a.G + qh) * D;
+        const float inv = (rho < live_rows && l > 0.f) ? 1.f / l : 0.f;
 #pragma unroll
-    for (int rb = 0; rb < RB; ++rb) {
-        float l = l_run[rb];
-        {
-            const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(l), __float_as_uint(l), false,
-                                                             false);
-            l += __uint_as_float(h == 0 ? sw[1] : sw[0]);
-        }
-        if (rho[rb] >= all_rows) continue;
-        if (a.splits == 1) {
-            uint16_t* op = a.out + (((int64_t)b * a.n_max + qn[rb]) * a.hq + g * a.G + qh[rb]) * D;
-            const float inv = (rho[rb] < live_rows && l > 0.f) ? 1.f / l : 0.f;
+        for (int db = 0; db < DB; ++db)
 #pragma unroll
-            for (int db = 0; db < DB; ++db)
+            for (int q4 = 0; q4 < 4; ++q4) {
+                const int dd = db * 32 + 8 * q4 + 4 * h;
+                *reinterpret_cast<uint2*>(op + dd) =
+                    make_uint2(pack_bf16x2(o[db][4 * q4] * inv, o[db][4 * q4 + 1] * inv),
+                               pack_bf16x2(o[db][4 * q4 + 2] * inv, o[db][4 * q4 + 3] * inv));
+            }
+    } else {
+        // normalised here, so bf16 holds it to the output's own precision
+        // output [b, g, split, row] (a workgroup's rows are contiguous: whole
+        // lines); (m, l) [b, g, row, split] (the merge reads a row's splits
+        // side by side)
+        const int64_t bg = (int64_t)b * a.hkv + g;
+        const int64_t pr = (bg * a.splits + split) * all_rows + rho;
+        const int64_t pm = (bg * all_rows + rho) * a.splits + split;
+        uint16_t* po = a.part_o + pr * D;
+        const float inv = l > 0.f ? 1.f / l : 0.f;
 #pragma unroll
-                for (int q4 = 0; q4 < 4; ++q4) {
-                    const int dd = db * 32 + 8 * q4 + 4 * h;
-                    *reinterpret_cast<uint2*>(op + dd) =
-                        make_uint2(pack_bf16x2(o[rb][db][4 * q4] * inv, o[rb][db][4 * q4 + 1] * inv),
-                                   pack_bf16x2(o[rb][db][4 * q4 + 2] * inv, o[rb][db][4 * q4 + 3] * inv));
-                }
-        } else {
-            // normalised here, so bf16 holds it to the output's own precision
-            // output [b, g, split, row] (a workgroup's rows are contiguous: whole
-            // lines); (m, l) [b, g, row, split] (the merge reads a row's splits
-            // side by side)
-            const int64_t bg = (int64_t)b * a.hkv + g;
-            const int64_t pr = (bg * a.splits + split) * all_rows + rho[rb];
-            const int64_t pm = (bg * all_rows + rho[rb]) * a.splits + split;
-            uint16_t* po = a.part_o + pr * D;
-            const float inv = l > 0.f ? 1.f / l : 0.f;
+        for (int db = 0; db < DB; ++db)
 #pragma unroll
-            for (int db = 0; db < DB; ++db)
-#pragma unroll
-                for (int q4 = 0; q4 < 4; ++q4) {
-                    const int dd = db * 32 + 8 * q4 + 4 * h;
-                    *reinterpret_cast<uint2*>(po + dd) =
-                        make_uint2(pack_bf16x2(o[rb][db][4 * q4] * inv, o[rb][db][4 * q4 + 1] * inv),
-                                   pack_bf16x2(o[rb][db][4 * q4 + 2] * inv, o[rb][db][4 * q4 + 3] * inv));
-                }
-            if (h == 0) a.part_ml[pm] = make_float2(m_run[rb], l);
-        }
+            for (int q4 = 0; q4 < 4; ++q4) {
+                const int dd = db * 32 + 8 * q4 + 4 * h;
+                *reinterpret_cast<uint2*>(po + dd) =
+                    make_uint2(pack_bf16x2(o[db][4 * q4] * inv, o[db][4 * q4 + 1] * inv),
+                               pack_bf16x2(o[db][4 * q4 + 2] * inv, o[db][4 * q4 + 3] * inv));
+            }
+        if (h == 0) a.part_ml[pm] = make_float2(l > 0.f ? m : -INFINITY, l);
     }
 }
 
@@ -707,9 +732,8 @@ static AttnPlan attn_plan(const presto_attn_desc* d) {
     p.rows = p.G * d->n_max;
     // 256 query rows per workgroup: eight waves of one 32-row block, or four
     // waves of two (each K/V fragment read from LDS then feeds two MFMAs)
-    p.rb = kAttnRowBlocks;
-    p.waves = kAttnWaves / p.rb;
-    p.rows_per_tile = p.waves * kRowsPerWave * p.rb;
+    p.waves = kAttnWaves;
+    p.rows_per_tile = kAttnRows;
     p.row_tiles = (p.rows + p.rows_per_tile - 1) / p.rows_per_tile;
     // context splits: one workgroup per CU, so the time in key-block units
     // (about 0.85 us each) is (rounds of workgroups) x (key blocks per split
@@ -804,11 +828,10 @@ presto_status launch_tree_attention(const presto_attn_desc* d, const void* q, co
     a.n_blocks = (int32_t)p.blocks;
     a.scale_log2 = d->scale * kLog2e;
     const dim3 block(p.waves * kWave), grid((unsigned)p.blocks);
-    constexpr int RB = kAttnRowBlocks, NW = kAttnWaves / kAttnRowBlocks;
     if (d->head_dim == 64)
-        tree_attn_bf16_kernel<64, NW, RB><<<grid, block, 0, stream>>>(a);
+        tree_attn_bf16_kernel<64><<<grid, block, 0, stream>>>(a);
     else
-        tree_attn_bf16_kernel<128, NW, RB><<<grid, block, 0, stream>>>(a);
+        tree_attn_bf16_kernel<128><<<grid, block, 0, stream>>>(a);
     presto_status st = check_launch("tree_attn_bf16_kernel");
     if (st != PRESTO_OK || p.splits == 1) return st;
     const int64_t merge_rows = (int64_t)d->batch * d->hkv * p.G * d->n_max;
