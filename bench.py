@@ -65,6 +65,8 @@ def main() -> int:
                          "captured HIP graph per input replica, replayed (measured slower)")
     ap.add_argument("--at-scale-run", action="store_true",
                     help="only the at-scale kernels (printed as JSON), for rocprofv3 counter runs")
+    ap.add_argument("--round-run", type=int, default=0,
+                    help="only the whole rounds of workload 3, 4 or 5 (printed as JSON), for rocprofv3")
     ap.add_argument("--traffic-run", action="store_true",
                     help="only the workload's tree attention (5 calls) and a 256 MiB device copy "
                          "(3 calls), for rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE runs")
@@ -83,6 +85,10 @@ def main() -> int:
     torch.cuda.set_device(dev)
     if args.at_scale_run:
         print(json.dumps(measure_at_scale(P, sy, dev)), flush=True)
+        return 0
+    if args.round_run:
+        print(json.dumps({sy.workload(args.round_run).name:
+                          measure_round_at_scale(P, sy, args.round_run, dev)}), flush=True)
         return 0
     w = sy.workload(args.workload)
     t_gen = time.time()
@@ -239,12 +245,14 @@ def main() -> int:
     torch.cuda.synchronize()
     per_round_us = np.array([a0.elapsed_time(a1) * 1e3 for a0, a1 in ev])
     warm_ms = timed(lambda r: step(0), args.steps, 0)
-    # per-stage averages (each stage alone, same replica cycling), for the rooflines
-    stage_ms = np.array([timed(f, args.steps, 0) for f in stage_fns])
+    # per-stage device time per launch: each stage alone, launched back to
+    # back from a captured HIP graph (so the host's launch cost is not in the
+    # figure), cycling the replicas as the rounds do
+    stage_ms = np.array([graph_time_us(f, reps) * 1e-3 for f in stage_fns])
     assert int(flags.item()) == 0, "device flagged NaN inputs"
 
     names = ["topk", "build_tree", "tree_attention", "accept"]
-    stages = {}
+    stages = {"timing": "device time per launch, from graph replays of back-to-back launches"}
     for j, nme in enumerate(names):
         us = float(stage_ms[j] * 1e3)
         entry = {"us": round(us, 2)}
@@ -261,7 +269,7 @@ def main() -> int:
         stages[nme] = entry
 
     # roofline of the dominant kernel among the bandwidth/compute-bound stages
-    dom = max(["topk", "tree_attention", "accept"], key=lambda s: stages[s]["us"])
+    dom = max(["topk", "tree_attention", "accept"], key=lambda s_: stages[s_]["us"])
     us = stages[dom]["us"]
     if dom == "tree_attention":
         t_hbm = w.layers * work["attn_bytes_per_layer"] / (HBM_PEAK_GBS * 1e3)
@@ -279,6 +287,8 @@ def main() -> int:
     roof["traffic"] = measured_traffic(dom, w)
 
     extra = measure_next_rows(P, sy, w, R, reps, timed, topk_out, topk_ws, tree_out, rin, dev)
+    rounds = None if args.no_at_scale else {
+        sy.workload(c).name: measure_round_at_scale(P, sy, c, dev) for c in (3, 4, 5)}
     at_scale = None if args.no_at_scale else measure_at_scale(P, sy, dev)
 
     cpu = None
@@ -302,7 +312,7 @@ def main() -> int:
                      "rounds": int(per_round_us.size)},
         "warm_rounds_per_s": round(1e3 / warm_ms, 2),
         "stages": stages, "roofline": roof, "cpu_baseline": cpu, "next_rows": extra,
-        "at_scale": at_scale,
+        "rounds_at_scale": rounds, "at_scale": at_scale,
         "accept_len": acc_out["accept_len"].cpu().tolist(),
         "gen_seconds": round(gen_s, 1),
     }
@@ -357,29 +367,185 @@ def traffic_run(P, w, layers, tree, max_ctx, dev) -> int:
     return 0
 
 
-def measure_at_scale(P, sy, dev):
-    """The data-parallel kernels at the larger workloads' shapes, each against
-    its roofline: top-k and the accept argmax over workload 5's rows (1024
-    drafter rows, 4128 node rows), tree attention at workload 3 (16 ragged
-    contexts, HBM-bound) and workload 4 (4 x 32768 keys, MFMA-bound).  Inputs
-    are N(0, 1) device draws of those shapes (scaled like the workloads'
-    logits); trees come from the GPU stages on them, and the tree build is
-    timed at workloads 3, 4 and 5 (latency-bound: one wave per sequence),
-    best-first and beam search (W = 10).
-    Timing only: parity at these shapes is covered by the tests."""
+def graph_time_us(fn, calls: int, reps: int = 5) -> float:
+    """Device time per call of fn(i) (i = 0 .. calls-1, so the caller can
+    cycle input replicas): `calls` launches captured into one HIP graph,
+    the graph replayed `reps` times, the fastest replay divided by `calls`.
+    The library only launches kernels, so its calls capture as they are."""
     import torch
 
-    def time_us(fn, n=10):
-        fn()
-        torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    for i in range(calls):
+        fn(i)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    side = torch.cuda.Stream()
+    side.wait_stream(stream)
+    with torch.cuda.graph(g, stream=side):
+        for i in range(calls):
+            fn(i)
+    stream.wait_stream(side)
+    torch.cuda.synchronize()
+    g.replay()
+    torch.cuda.synchronize()
+    best = float("inf")
+    for _ in range(reps):
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        st = torch.cuda.current_stream()
-        e0.record(st)
-        for _ in range(n):
-            fn()
-        e1.record(st)
+        e0.record(stream)
+        g.replay()
+        e1.record(stream)
         torch.cuda.synchronize()
-        return e0.elapsed_time(e1) * 1e3 / n
+        best = min(best, e0.elapsed_time(e1) * 1e3 / calls)
+    del g
+    return best
+
+
+def measure_round_at_scale(P, sy, cfg: int, dev, rounds: int = 10):
+    """Whole rounds (top-k -> tree -> every layer's tree attention -> accept)
+    at workload `cfg`, launched on one stream as the bench workload's rounds.
+    Drafter logits, lattice, lambda, root tokens and context lengths follow
+    the workload's recipe (host draws); the attention inputs of every layer
+    are N(0, 1) device draws of the workload's shapes, and the target logits
+    follow the recipe on the device (field row of the node's depth plus
+    sigma_t N(0, 1) noise) for the tree the library builds: timing inputs
+    only, parity at these shapes is in the tests.  One round touches far
+    more than the 256 MB last-level cache, so every round is cold."""
+    import ctypes
+
+    import torch
+
+    w = sy.workload(cfg)
+    rin = sy.round_inputs(w)
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(1000 + cfg)
+    bf = torch.bfloat16
+
+    def up(a, bf16=False):
+        t = torch.from_numpy(np.ascontiguousarray(a))
+        if bf16:
+            t = t.view(torch.int16).view(bf)
+        return t.to(dev)
+
+    drafter = up(rin["drafter_logits"], w.dtype == "bf16")
+    rho, lam, root = up(rin["rho"]), up(rin["lam"]), up(rin["root_token"])
+    ctx = rin["ctx"].astype(np.int64)
+    total = int(ctx.sum())
+    offs = up(np.concatenate([[0], np.cumsum(ctx)]).astype(np.int32))
+    N = w.n_max
+
+    def randn(*shape):
+        return torch.randn(*shape, device=dev, generator=gen).to(bf)
+
+    layers = [{"q": randn(w.batch, N, w.hq, w.head_dim), "kc": randn(total, w.hkv, w.head_dim),
+               "vc": randn(total, w.hkv, w.head_dim), "kt": randn(w.batch, N, w.hkv, w.head_dim),
+               "vt": randn(w.batch, N, w.hkv, w.head_dim)} for _ in range(w.layers)]
+    rows = w.batch * w.depth
+    i32 = dict(dtype=torch.int32, device=dev)
+    ids = torch.empty(rows, w.k, **i32)
+    lp = torch.empty(rows, w.k, dtype=torch.float32, device=dev)
+    lse = torch.empty(rows, dtype=torch.float32, device=dev)
+    tws = torch.zeros(max(1, P.lib().presto_topk_workspace(rows, w.vocab, w.k)), dtype=torch.uint8,
+                      device=dev)
+    P.presto_topk(drafter, w.k, ids=ids, logprob=lp, lse=lse, workspace=tws)
+    tree = P.presto_build_tree(ids, lp, rho, lam, root, w.depth, w.k, w.budget)
+    torch.cuda.synchronize()
+    # target logits of the tree's nodes: F[b, depth(n)] + sigma_t N(0, 1)
+    field = up(rin["field"])
+    dep = tree["depth"].clamp(min=0).long()
+    target = torch.empty(w.batch, N, w.vocab, dtype=bf, device=dev)
+    for b in range(w.batch):
+        t = field[b].index_select(0, dep[b])
+        t += float(w.sigma_t) * torch.randn(t.shape, device=dev, generator=gen)
+        target[b] = t.to(bf)
+    del field
+    out = [torch.empty_like(L["q"]) for L in layers]
+    desc = P.AttnDesc(w.batch, N, w.hq, w.hkv, w.head_dim, int(ctx.max()), w.scale, P.PRESTO_DT_BF16,
+                      P.PRESTO_CTX_PACKED, total)
+    nws = P.lib().presto_tree_attention_workspace(ctypes.byref(desc))
+    aws = torch.zeros(max(1, nws), dtype=torch.uint8, device=dev)
+    acc = {"accept_len": torch.empty(w.batch, **i32), "path": torch.empty(w.batch, w.depth + 1, **i32),
+           "bonus": torch.empty(w.batch, **i32), "target_argmax": torch.empty(w.batch, N, **i32)}
+    accws = torch.zeros(P.lib().presto_accept_workspace(w.batch, N, w.vocab), dtype=torch.uint8, device=dev)
+    flags = torch.zeros(1, **i32)
+
+    def st_topk(i=0):
+        P.presto_topk(drafter, w.k, ids=ids, logprob=lp, lse=lse, flags=flags, workspace=tws)
+
+    def st_tree(i=0):
+        P.presto_build_tree(ids, lp, rho, lam, root, w.depth, w.k, w.budget, out=tree)
+
+    def st_attn(i=0):
+        for li, L in enumerate(layers):
+            P.presto_tree_attention(L["q"], L["kc"], L["vc"], offs, L["kt"], L["vt"], tree["anc"],
+                                    tree["n_nodes"], int(ctx.max()), w.scale, out=out[li], workspace=aws,
+                                    total_ctx=total)
+
+    def st_accept(i=0):
+        P.presto_accept(target, tree["parent"], tree["token"], tree["n_nodes"], w.depth, out=acc,
+                        flags=flags, workspace=accws)
+
+    fns = [st_topk, st_tree, st_attn, st_accept]
+
+    def step():
+        for f in fns:
+            f()
+
+    stream = torch.cuda.current_stream()
+    for _ in range(2):
+        step()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(rounds):
+        step()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    assert int(flags.item()) == 0, "device flagged NaN inputs"
+    ms = e0.elapsed_time(e1) / rounds
+    nn = tree["n_nodes"].cpu().numpy()
+    work = algorithmic_work(w, ctx, nn, tree["depth"].cpu().numpy())
+    stage_us = [graph_time_us(lambda i, f=f: f(), 4 if f is not st_attn else 1, 3) for f in fns]
+    attn_bytes = w.layers * work["attn_bytes_per_layer"]
+    attn_flops = w.layers * work["attn_flops_per_layer"]
+    res = {
+        "rounds_per_s": round(1e3 / ms, 2), "sequence_rounds_per_s": round(w.batch * 1e3 / ms, 2),
+        "ms_per_round": round(ms, 4), "rounds": rounds, "layers": w.layers,
+        "stages_us": {"topk": round(stage_us[0], 2), "build_tree": round(stage_us[1], 2),
+                      "tree_attention": round(stage_us[2], 2), "accept": round(stage_us[3], 2)},
+        "topk_GB/s": round(work["topk_bytes"] / (stage_us[0] * 1e3), 1),
+        "attention_GB/s": round(attn_bytes / (stage_us[2] * 1e3), 1),
+        "attention_TFLOP/s": round(attn_flops / (stage_us[2] * 1e6), 1),
+        "accept_GB/s": round(work["argmax_bytes"] / (stage_us[3] * 1e3), 1),
+        "accept_len_mean": round(float(acc["accept_len"].float().mean().item()), 3),
+        "inputs": "drafter logits, lattice, lambda, roots and contexts by the workload recipe; "
+                  "Q/K/V N(0,1) device draws; target logits by the recipe on the device",
+    }
+    del layers, out, target, drafter
+    torch.cuda.empty_cache()
+    return res
+
+
+def measure_at_scale(P, sy, dev):
+    """Single stages at the larger workloads' shapes, each against its
+    roofline (device time per launch from graph replays after a warm-up):
+    top-k over 1024 drafter rows at k = 4, 8 and 10 (with the count of
+    chunks that took the exact tie path), the accept argmax over 4128 node
+    rows, tree attention at workloads 3 and 4, and tree builds (best-first
+    and beam search, W = 10) at workloads 3, 4 and 5 and at the paper's
+    operating point (block 16, k = 10, budgets 128 / 256 / 512).  Logits are
+    N(0, 4^2) device draws of those shapes; candidate tables come from
+    presto_topk on them.  Timing only: parity at these shapes is covered by
+    the tests."""
+    import ctypes
+
+    import torch
+
+    def time_us(fn, calls=8):
+        t0 = time.time()
+        while time.time() - t0 < 0.05:  # clocks up before timing
+            fn(0)
+        torch.cuda.synchronize()
+        return graph_time_us(fn, calls, 5)
 
     def roof(bytes_, flops, us):
         gbs = bytes_ / (us * 1e3)
@@ -401,60 +567,84 @@ def measure_at_scale(P, sy, dev):
 
     gen = torch.Generator(device=dev)
     gen.manual_seed(1234)
+    i32 = dict(dtype=torch.int32, device=dev)
     out = {}
-    # top-k and argmax over workload 5's rows
+
+    def candidates(batch, D, V, k):
+        """A candidate table from presto_topk over N(0, 4^2) bf16 drafter rows."""
+        rows = batch * D
+        x = (torch.randn(rows, V, device=dev, generator=gen) * 4).to(torch.bfloat16)
+        ids, lp, _ = P.presto_topk(x, k)
+        del x
+        return ids.contiguous(), lp.contiguous()
+
+    # top-k over workload 5's 1024 drafter rows, at k = 4, 8 and 10
     w5 = sy.workload(5)
     rows = w5.batch * w5.depth
     logits = (torch.randn(rows, w5.vocab, device=dev, generator=gen) * 4).to(torch.bfloat16)
-    ws = torch.zeros(P.lib().presto_topk_workspace(rows, w5.vocab, w5.k), dtype=torch.uint8, device=dev)
-    o = (torch.empty(rows, w5.k, dtype=torch.int32, device=dev),
-         torch.empty(rows, w5.k, dtype=torch.float32, device=dev),
-         torch.empty(rows, dtype=torch.float32, device=dev))
-    us = time_us(lambda: P.presto_topk(logits, w5.k, ids=o[0], logprob=o[1], lse=o[2], workspace=ws))
-    out["topk_1024_rows"] = roof(rows * w5.vocab * 2 + rows * (8 * w5.k + 4), 0, us)
+    for k in (4, 8, 10):
+        ws = torch.zeros(P.lib().presto_topk_workspace(rows, w5.vocab, k), dtype=torch.uint8, device=dev)
+        o = (torch.empty(rows, k, **i32), torch.empty(rows, k, dtype=torch.float32, device=dev),
+             torch.empty(rows, dtype=torch.float32, device=dev))
+        us = time_us(lambda i: P.presto_topk(logits, k, ids=o[0], logprob=o[1], lse=o[2], workspace=ws))
+        P.presto_topk(logits, k, ids=o[0], logprob=o[1], lse=o[2], workspace=ws)
+        torch.cuda.synchronize()
+        r = roof(rows * w5.vocab * 2 + rows * (8 * k + 4), 0, us)
+        r["fallback_chunks"] = P.topk_fallback_chunks(ws)
+        out[f"topk_1024_rows_k{k}"] = r
     del logits
+    # accept argmax over workload 5's 4128 node rows
     lam = torch.full((w5.depth,), 0.2, dtype=torch.float32, device=dev)
-    root = torch.zeros(w5.batch, dtype=torch.int32, device=dev)
-    lp = torch.log_softmax(torch.randn(rows, 64, device=dev, generator=gen) * 4, dim=1)
-    lp, ids = torch.topk(lp, w5.k, dim=1)
-    ids32, lpc = ids.to(torch.int32).contiguous(), lp.contiguous()
-    tree = P.presto_build_tree(ids32, lpc, None, lam, root, w5.depth, w5.k, w5.budget)
-    us = time_us(lambda: P.presto_build_tree(ids32, lpc, None, lam, root, w5.depth, w5.k, w5.budget,
-                                             out=tree))
-    out[f"tree_build_{w5.name}"] = tree_latency(us, tree)
-    beam = {k: torch.empty_like(v) for k, v in tree.items()}
-    us = time_us(lambda: P.presto_build_tree(ids32, lpc, None, lam, root, w5.depth, w5.k, w5.budget,
-                                             mode=P.PRESTO_TREE_BEAM, beam_width=10, out=beam))
-    out[f"tree_build_beam10_{w5.name}"] = tree_latency(us, beam)
+    root = torch.zeros(w5.batch, **i32)
+    ids5, lp5 = candidates(w5.batch, w5.depth, w5.vocab, w5.k)
+    tree = P.presto_build_tree(ids5, lp5, None, lam, root, w5.depth, w5.k, w5.budget)
     target = (torch.randn(w5.batch * w5.n_max, w5.vocab, device=dev, generator=gen) * 4).to(torch.bfloat16)
     aws = torch.zeros(P.lib().presto_accept_workspace(w5.batch, w5.n_max, w5.vocab), dtype=torch.uint8,
                       device=dev)
-    us = time_us(lambda: P.presto_accept(target, tree["parent"], tree["token"], tree["n_nodes"], w5.depth,
-                                         workspace=aws))
+    accout = {"accept_len": torch.empty(w5.batch, **i32), "path": torch.empty(w5.batch, w5.depth + 1, **i32),
+              "bonus": torch.empty(w5.batch, **i32), "target_argmax": torch.empty(w5.batch, w5.n_max, **i32)}
+    us = time_us(lambda i: P.presto_accept(target, tree["parent"], tree["token"], tree["n_nodes"], w5.depth,
+                                           out=accout, workspace=aws))
     live = int(tree["n_nodes"].sum().item())
     out["accept_4128_rows"] = roof(live * w5.vocab * 2, 0, us)
     del target
+
+    # tree builds: workloads 3, 4, 5 and the paper's point (k = 10, block 16)
+    def trees(name, batch, D, k, B, lam_v=0.2, lattice=True):
+        ids, lp = candidates(batch, D, 151936, k)
+        lamw = torch.full((D,), lam_v, dtype=torch.float32, device=dev)
+        rootw = torch.zeros(batch, **i32)
+        rho = None
+        if lattice:
+            g2 = torch.Generator(device=dev)
+            g2.manual_seed(77)
+            u = torch.rand(batch, D, k, k, k, device=dev, generator=g2)
+            rho = torch.where(torch.rand(u.shape, device=dev, generator=g2) < 0.5,
+                              torch.full_like(u, float(np.log(np.float32(1e-4)))),
+                              torch.log(u * (1 - 1e-3) + 1e-3))
+        tr = P.presto_build_tree(ids, lp, rho, lamw, rootw, D, k, B)
+        us = time_us(lambda i: P.presto_build_tree(ids, lp, rho, lamw, rootw, D, k, B, out=tr))
+        out[f"tree_build_{name}"] = tree_latency(us, tr)
+        bm = {kk: torch.empty_like(v) for kk, v in tr.items()}
+        us = time_us(lambda i: P.presto_build_tree(ids, lp, rho, lamw, rootw, D, k, B,
+                                                   mode=P.PRESTO_TREE_BEAM, beam_width=10, out=bm))
+        out[f"tree_build_beam10_{name}"] = tree_latency(us, bm)
+
+    for cfg in (3, 4, 5):
+        w = sy.workload(cfg)
+        trees(w.name, w.batch, w.depth, w.k, w.budget, w.lam)
+    for B in (128, 256, 512):
+        trees(f"paper-k10-B{B}", 1, 16, 10, B)
+
     # tree attention at workloads 3 and 4
     for cfg in (3, 4):
         w = sy.workload(cfg)
         ctx = sy.ctx_lengths(w).astype(np.int64)
         offs = torch.from_numpy(np.concatenate([[0], np.cumsum(ctx)]).astype(np.int32)).to(dev)
         total = int(ctx.sum())
-        rows = w.batch * w.depth
-        lp = torch.log_softmax(torch.randn(rows, 64, device=dev, generator=gen) * 4, dim=1)
-        lp, ids = torch.topk(lp, w.k, dim=1)
+        ids, lp = candidates(w.batch, w.depth, w.vocab, w.k)
         lamw = torch.full((w.depth,), 0.2, dtype=torch.float32, device=dev)
-        rootw = torch.zeros(w.batch, dtype=torch.int32, device=dev)
-        ids32, lpc = ids.to(torch.int32).contiguous(), lp.contiguous()
-        tr = P.presto_build_tree(ids32, lpc, None, lamw, rootw, w.depth, w.k, w.budget)
-        us = time_us(lambda: P.presto_build_tree(ids32, lpc, None, lamw, rootw, w.depth, w.k, w.budget,
-                                                 out=tr))
-        out[f"tree_build_{w.name}"] = tree_latency(us, tr)
-        beam = {k: torch.empty_like(v) for k, v in tr.items()}
-        us = time_us(lambda: P.presto_build_tree(ids32, lpc, None, lamw, rootw, w.depth, w.k, w.budget,
-                                                 mode=P.PRESTO_TREE_BEAM, beam_width=10, out=beam))
-        out[f"tree_build_beam10_{w.name}"] = tree_latency(us, beam)
-        bf = dict(device=dev, dtype=torch.bfloat16)
+        tr = P.presto_build_tree(ids, lp, None, lamw, torch.zeros(w.batch, **i32), w.depth, w.k, w.budget)
         q = torch.randn(w.batch, w.n_max, w.hq, w.head_dim, device=dev, generator=gen).to(torch.bfloat16)
         kc = torch.randn(total, w.hkv, w.head_dim, device=dev, generator=gen).to(torch.bfloat16)
         vc = torch.randn(total, w.hkv, w.head_dim, device=dev, generator=gen).to(torch.bfloat16)
@@ -463,17 +653,17 @@ def measure_at_scale(P, sy, dev):
         ao = torch.empty_like(q)
         desc = P.AttnDesc(w.batch, w.n_max, w.hq, w.hkv, w.head_dim, int(ctx.max()), w.scale,
                           P.PRESTO_DT_BF16, P.PRESTO_CTX_PACKED, total)
-        import ctypes
         nws = P.lib().presto_tree_attention_workspace(ctypes.byref(desc))
-        aw = torch.zeros(max(1, nws), dtype=torch.uint8, device=dev) if nws else None
-        us = time_us(lambda: P.presto_tree_attention(q, kc, vc, offs, kt, vt, tr["anc"], tr["n_nodes"],
-                                                     int(ctx.max()), w.scale, out=ao, workspace=aw,
-                                                     total_ctx=total))
+        aw = torch.zeros(max(1, nws), dtype=torch.uint8, device=dev)
+        us = time_us(lambda i: P.presto_tree_attention(q, kc, vc, offs, kt, vt, tr["anc"], tr["n_nodes"],
+                                                       int(ctx.max()), w.scale, out=ao, workspace=aw,
+                                                       total_ctx=total), calls=4)
         nn = tr["n_nodes"].cpu().numpy()
         dep = tr["depth"].cpu().numpy()
         ww = algorithmic_work(w, ctx, nn, dep)
         out[f"tree_attention_{w.name}"] = roof(ww["attn_bytes_per_layer"], ww["attn_flops_per_layer"], us)
         del q, kc, vc, kt, vt, ao, aw
+    torch.cuda.empty_cache()
     return out
 
 
