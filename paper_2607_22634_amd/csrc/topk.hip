@@ -88,9 +88,11 @@ __device__ __forceinline__ void load_chunk(const void* __restrict__ row, int64_t
 
 // The k-th largest value of one u32 per lane (k <= 64).  Small k: k rounds
 // of "wave max, then retire one lane holding it"; larger k: bisection on the
-// bits, counting lanes at or above each probe with a ballot.
+// top BITS bits (the others of every x are equal: 16 for ord32 of bf16
+// values), counting lanes at or above each probe with a ballot.
+template <int BITS = 32>
 __device__ __forceinline__ uint32_t wave_kth_largest_u32(uint32_t x, int k) {
-    if (k <= 8) {
+    if (k <= (BITS == 32 ? 8 : 4)) {
         const int lane = lane_id();
         uint32_t t = 0u;
         for (int j = 0; j < k; ++j) {
@@ -102,7 +104,7 @@ __device__ __forceinline__ uint32_t wave_kth_largest_u32(uint32_t x, int k) {
     }
     uint32_t t = 0u;
 #pragma unroll
-    for (int bit = 31; bit >= 0; --bit) {
+    for (int bit = 31; bit >= 32 - BITS; --bit) {
         const uint32_t c = t | (1u << bit);
         if (__popcll(__ballot(x >= c)) >= k) t = c;
     }
@@ -199,7 +201,15 @@ __global__ __launch_bounds__(kTopkWavesPerBlock * kWave) void topk_partial_kerne
     if constexpr (ENT) Hx = wave_sum_f32_dpp(sx) * corr * (1.f / kLog2eF);
     // the k-th largest lane maximum bounds the chunk's k-th value from below:
     // only groups whose maximum reaches it can hold a top-k entry
-    const float thr = unord32(wave_kth_largest_u32(ord32(lm), k));
+    // (bf16: ord32 of every value ends in 0x0000 or 0xffff, so the bisection
+    // runs over the top 16 bits and the bound is completed below them)
+    float thr;
+    if constexpr (BF16) {
+        const uint32_t t = wave_kth_largest_u32<16>(ord32(lm) & 0xffff0000u, k);
+        thr = unord32(t | ((t & 0x80000000u) ? 0u : 0xffffu));
+    } else {
+        thr = unord32(wave_kth_largest_u32(ord32(lm), k));
+    }
 
     // A lane appends its candidate groups (values as they are) with one LDS
     // atomic for all of them; the keys are formed afterwards, one candidate
@@ -239,7 +249,40 @@ __global__ __launch_bounds__(kTopkWavesPerBlock * kWave) void topk_partial_kerne
         return ((full || idx < vocab) && xv >= thr) ? vocab_key(xv, (uint32_t)idx) : 0ull;
     };
     bool fell_back = false;
-    if (total <= kWave) {
+    // bf16: a chunk-local 32-bit key, the value's 16-bit order code over
+    // 0xffff minus the index within the chunk (chunks hold at most 65536
+    // entries), orders the entries exactly as the 64-bit vocabulary key
+    auto entry_key32 = [&](int e) -> uint32_t {
+        if (e >= total) return 0u;
+        const float xv = cand_v[wave][e];
+        const int64_t idx = (int64_t)cand_i[wave][e / P] + e % P;
+        return ((full || idx < vocab) && xv >= thr)
+                   ? (ord32(xv) & 0xffff0000u) | (0xffffu - (uint32_t)(idx - c0))
+                   : 0u;
+    };
+    auto key64 = [&](uint32_t k32) -> uint64_t {
+        const uint32_t o = k32 & 0xffff0000u;
+        const float xv = unord32(o | ((o & 0x80000000u) ? 0u : 0xffffu));
+        return vocab_key(xv, (uint32_t)(c0 + (0xffffu - (k32 & 0xffffu))));
+    };
+    if (BF16 && total <= kCandCap && ngroups <= (uint32_t)kGroupCap) {
+        constexpr int C = kCandCap / kWave;
+        uint32_t x[C];
+#pragma unroll
+        for (int c = 0; c < C; ++c) x[c] = (c == 0 || total > c * kWave) ? entry_key32(c * kWave + lane) : 0u;
+        uint32_t mine = 0u;
+        const int nc = (total + kWave - 1) / kWave;  // slots holding entries
+        for (int j = 0; j < k; ++j) {
+            uint32_t lmax = x[0];
+#pragma unroll
+            for (int c = 1; c < C; ++c) lmax = (c < nc && x[c] > lmax) ? x[c] : lmax;
+            const uint32_t m = wave_max_u32_dpp(lmax);
+            mine = lane == j ? m : mine;
+#pragma unroll
+            for (int c = 0; c < C; ++c) x[c] = x[c] == m ? 0u : x[c];
+        }
+        if (lane < k) out[lane] = mine ? key64(mine) : 0ull;
+    } else if (total <= kWave) {
         // one candidate per lane (keys are unique); k rounds of wave max,
         // retiring the lane that held it (0 past the last valid entry)
         uint64_t x = entry_key(lane);
@@ -416,10 +459,13 @@ using namespace presto;
 static constexpr size_t kTopkCounterBytes = 16;
 
 static int topk_nload(bool bf16, int64_t rows, int32_t vocab) {
-    const int64_t ch8 = (int64_t)kWave * 8 * (bf16 ? 8 : 4);
-    const int64_t waves8 = rows * ((vocab + ch8 - 1) / ch8);
-    // 8 loads per lane only when that still leaves >= 16 waves per CU
-    return waves8 >= 16 * 256 ? 8 : 4;
+    auto waves = [&](int nl) {
+        const int64_t ch = (int64_t)kWave * nl * (bf16 ? 8 : 4);
+        return rows * ((vocab + ch - 1) / ch);
+    };
+    // 8 loads per lane only when that still leaves >= 16 waves per CU (16
+    // loads, 165 registers, measured slower at 1024 rows: 58 -> 70 us)
+    return waves(8) >= 16 * 256 ? 8 : 4;
 }
 
 size_t topk_workspace_bytes(int64_t rows, int32_t vocab, int32_t k) {

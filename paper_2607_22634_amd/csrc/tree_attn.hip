@@ -574,13 +574,17 @@ __global__ __launch_bounds__(kAttnWaves * kWave) void tree_attn_bf16_kernel(Attn
 
 // Merge of the split partials: one wave per query row.  Lane s reads the
 // (m, l) pair of split s (at most 64 splits) and forms its weight
-// l exp2(m - M); the splits' normalised outputs are then read in groups of
-// kMergeUnroll with every load of a group issued before the first is used,
-// so a row costs two memory round trips rather than one per split.
+// l exp2(m - M); the splits' normalised outputs are read in groups of
+// kMergeUnroll.  The pairs and the first group of outputs are requested
+// together with the row's node count and context length, before any of
+// them is known (entries of splits the row does not have are read but
+// never used), so a row with up to kMergeUnroll splits costs one memory
+// round trip.
 constexpr int kMergeUnroll = 8;
 template <int D>
 __global__ __launch_bounds__(256) void tree_attn_merge_kernel(AttnArgs a) {
     constexpr int PER = D / kWave;  // output dims per lane
+    static_assert(PER == 1 || PER == 2, "head_dim 64 or 128");
     const int lane = lane_id();
     const int64_t r = (int64_t)blockIdx.x * (blockDim.x / kWave) + threadIdx.x / kWave;
     const int64_t rows = (int64_t)a.batch * a.hkv * a.G * a.n_max;
@@ -589,44 +593,55 @@ __global__ __launch_bounds__(256) void tree_attn_merge_kernel(AttnArgs a) {
     const int g = (int)((r / (a.G * a.n_max)) % a.hkv);
     const int b = (int)(r / ((int64_t)a.G * a.n_max * a.hkv));
     const int n = rho / a.G, hh = rho - n * a.G;
-    const int nn = clamp_nodes(a.n_nodes[b], a.n_max);
+    const int64_t rows_g = (int64_t)a.G * a.n_max;
+    const int64_t bg = (int64_t)b * a.hkv + g;
+    // split s of this row: ((b, g) * splits + s) * rows + rho
+    const uint16_t* po = a.part_o + (bg * a.splits * rows_g + rho) * D + lane * PER;
+    auto load_out = [&](int sp, float (&v)[PER]) {
+        if constexpr (PER == 1) {
+            v[0] = bf16_to_f(po[sp * rows_g * D]);
+        } else {
+            const uint32_t w2 = *reinterpret_cast<const uint32_t*>(po + sp * rows_g * D);
+            v[0] = bf16_to_f((uint16_t)(w2 & 0xffffu));
+            v[1] = bf16_to_f((uint16_t)(w2 >> 16));
+        }
+    };
+    // everything independent is requested at once
+    const int nn_raw = a.n_nodes[b];
+    const CtxSpan cs = ctx_span(a.ctx_off, b, a.ctx_slots);
+    float2 ml = make_float2(-INFINITY, 0.f);
+    if (lane < a.splits) ml = a.part_ml[(bg * rows_g + rho) * a.splits + lane];
+    float v0[kMergeUnroll][PER];
+#pragma unroll
+    for (int u = 0; u < kMergeUnroll; ++u) load_out(min(u, a.splits - 1), v0[u]);
+
+    const int nn = clamp_nodes(nn_raw, a.n_max);
+    const int keys = cs.ctx + nn;
+    const int nsplit = min(a.splits, (keys + a.split_len - 1) / a.split_len);
     uint16_t* op = a.out + (((int64_t)b * a.n_max + n) * a.hq + g * a.G + hh) * D + lane * PER;
     float acc[PER];
 #pragma unroll
     for (int e = 0; e < PER; ++e) acc[e] = 0.f;
     if (rho < a.G * nn) {
-        const int keys = ctx_span(a.ctx_off, b, a.ctx_slots).ctx + nn;
-        const int nsplit = min(a.splits, (keys + a.split_len - 1) / a.split_len);
-        // split s of this row: ((b, g) * splits + s) * rows + rho
-        const int64_t rows_g = (int64_t)a.G * a.n_max;
-        const int64_t pr = ((int64_t)b * a.hkv + g) * a.splits * rows_g + rho;
-        const uint16_t* po = a.part_o + pr * D + lane * PER;
-        float2 ml = make_float2(-INFINITY, 0.f);
-        if (lane < nsplit) ml = a.part_ml[(((int64_t)b * a.hkv + g) * rows_g + rho) * a.splits + lane];
+        if (lane >= nsplit) ml = make_float2(-INFINITY, 0.f);
         const float M = wave_max_f32_dpp(ml.x);
         const float wl = ml.x == -INFINITY ? 0.f : exp2f(ml.x - M) * ml.y;  // weight of split `lane`
         const float L = wave_sum_f32_dpp(wl);
-        for (int s0 = 0; s0 < nsplit; s0 += kMergeUnroll) {
+        auto add = [&](int sp, const float (&v)[PER]) {
+            const float w = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(wl), sp));
+#pragma unroll
+            for (int e = 0; e < PER; ++e) acc[e] += w * v[e];
+        };
+#pragma unroll
+        for (int u = 0; u < kMergeUnroll; ++u)
+            if (u < nsplit) add(u, v0[u]);
+        for (int s0 = kMergeUnroll; s0 < nsplit; s0 += kMergeUnroll) {
             float v[kMergeUnroll][PER];
 #pragma unroll
-            for (int u = 0; u < kMergeUnroll; ++u) {
-                const int s = min(s0 + u, nsplit - 1);
-                if constexpr (PER == 1) {
-                    v[u][0] = bf16_to_f(po[s * rows_g * D]);
-                } else {
-                    const uint32_t w2 = *reinterpret_cast<const uint32_t*>(po + s * rows_g * D);
-                    v[u][0] = bf16_to_f((uint16_t)(w2 & 0xffffu));
-                    v[u][1] = bf16_to_f((uint16_t)(w2 >> 16));
-                }
-            }
+            for (int u = 0; u < kMergeUnroll; ++u) load_out(min(s0 + u, nsplit - 1), v[u]);
 #pragma unroll
-            for (int u = 0; u < kMergeUnroll; ++u) {
-                if (s0 + u < nsplit) {
-                    const float w = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(wl), s0 + u));
-#pragma unroll
-                    for (int e = 0; e < PER; ++e) acc[e] += w * v[u][e];
-                }
-            }
+            for (int u = 0; u < kMergeUnroll; ++u)
+                if (s0 + u < nsplit) add(s0 + u, v[u]);
         }
         const float inv = L > 0.f ? 1.f / L : 0.f;
 #pragma unroll
@@ -635,7 +650,6 @@ __global__ __launch_bounds__(256) void tree_attn_merge_kernel(AttnArgs a) {
     if constexpr (PER == 1) {
         *op = f_to_bf16(acc[0]);
     } else {
-        static_assert(PER == 2, "head_dim 64 or 128");
         *reinterpret_cast<uint32_t*>(op) =
             (uint32_t)f_to_bf16(acc[0]) | ((uint32_t)f_to_bf16(acc[1]) << 16);
     }
