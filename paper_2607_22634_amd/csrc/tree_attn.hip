@@ -586,31 +586,33 @@ __global__ __launch_bounds__(256) void tree_attn_merge_kernel(AttnArgs a) {
     constexpr int PER = D / kWave;  // output dims per lane
     static_assert(PER == 1 || PER == 2, "head_dim 64 or 128");
     const int lane = lane_id();
-    const int64_t r = (int64_t)blockIdx.x * (blockDim.x / kWave) + threadIdx.x / kWave;
-    const int64_t rows = (int64_t)a.batch * a.hkv * a.G * a.n_max;
-    if (r >= rows) return;
-    const int rho = (int)(r % (a.G * a.n_max));
-    const int g = (int)((r / (a.G * a.n_max)) % a.hkv);
-    const int b = (int)(r / ((int64_t)a.G * a.n_max * a.hkv));
+    // grid: x covers the rows of one (sequence, KV head) four per block, y
+    // the (sequence, KV head) pairs
+    const int rows_g = a.G * a.n_max;
+    const int rho = (int)blockIdx.x * (blockDim.x / kWave) + (int)threadIdx.x / kWave;
+    if (rho >= rows_g) return;
+    const int bg = (int)blockIdx.y;
+    const int b = bg / a.hkv, g = bg - b * a.hkv;
     const int n = rho / a.G, hh = rho - n * a.G;
-    const int64_t rows_g = (int64_t)a.G * a.n_max;
-    const int64_t bg = (int64_t)b * a.hkv + g;
-    // split s of this row: ((b, g) * splits + s) * rows + rho
-    const uint16_t* po = a.part_o + (bg * a.splits * rows_g + rho) * D + lane * PER;
+    // split s of this row: ((b, g) * splits + s) * rows + rho; every
+    // offset within one (b, g) block of partials fits 32 bits
+    const uint16_t* po = a.part_o + ((int64_t)bg * a.splits * rows_g + rho) * D + lane * PER;
+    const uint32_t sstride = (uint32_t)rows_g * D;  // elements from one split to the next
     auto load_out = [&](int sp, float (&v)[PER]) {
+        const uint16_t* q = po + (uint32_t)sp * sstride;
         if constexpr (PER == 1) {
-            v[0] = bf16_to_f(po[sp * rows_g * D]);
+            v[0] = bf16_to_f(*q);
         } else {
-            const uint32_t w2 = *reinterpret_cast<const uint32_t*>(po + sp * rows_g * D);
-            v[0] = bf16_to_f((uint16_t)(w2 & 0xffffu));
-            v[1] = bf16_to_f((uint16_t)(w2 >> 16));
+            const uint32_t w2 = *reinterpret_cast<const uint32_t*>(q);
+            v[0] = bf16lo(w2);
+            v[1] = bf16hi(w2);
         }
     };
     // everything independent is requested at once
     const int nn_raw = a.n_nodes[b];
     const CtxSpan cs = ctx_span(a.ctx_off, b, a.ctx_slots);
     float2 ml = make_float2(-INFINITY, 0.f);
-    if (lane < a.splits) ml = a.part_ml[(bg * rows_g + rho) * a.splits + lane];
+    if (lane < a.splits) ml = a.part_ml[((int64_t)bg * rows_g + rho) * a.splits + lane];
     float v0[kMergeUnroll][PER];
 #pragma unroll
     for (int u = 0; u < kMergeUnroll; ++u) load_out(min(u, a.splits - 1), v0[u]);
@@ -812,6 +814,9 @@ presto_status launch_tree_attention(const presto_attn_desc* d, const void* q, co
         return check_launch("tree_attn_f32_kernel");
     }
     const AttnPlan p = attn_plan(d);
+    if (p.splits > 1 && (int64_t)d->batch * d->hkv > 65535)  // the merge's grid.y
+        return set_error(PRESTO_ERR_UNSUPPORTED, "tree attention: batch x KV heads %lld above 65535",
+                         (long long)d->batch * d->hkv);
     AttnArgs a;
     a.q = (const uint16_t*)q;
     a.kc = (const uint16_t*)k_cache;
@@ -848,8 +853,7 @@ presto_status launch_tree_attention(const presto_attn_desc* d, const void* q, co
         tree_attn_bf16_kernel<128><<<grid, block, 0, stream>>>(a);
     presto_status st = check_launch("tree_attn_bf16_kernel");
     if (st != PRESTO_OK || p.splits == 1) return st;
-    const int64_t merge_rows = (int64_t)d->batch * d->hkv * p.G * d->n_max;
-    const unsigned mgrid = (unsigned)((merge_rows + 3) / 4);
+    const dim3 mgrid((unsigned)((p.rows + 3) / 4), (unsigned)(d->batch * d->hkv));
     if (d->head_dim == 64)
         tree_attn_merge_kernel<64><<<mgrid, 256, 0, stream>>>(a);
     else
