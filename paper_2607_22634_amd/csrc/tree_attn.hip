@@ -222,7 +222,17 @@ __global__ __launch_bounds__(kAttnWaves * kWave) void tree_attn_bf16_kernel(Attn
     const int tid = threadIdx.x;
     const int wave = tid / kWave, lane = lane_id();
     const int l32 = lane & 31, h = lane >> 5;
-    const int row0 = rt * ROWS + wave * kRowsPerWave;  // first query row of this wave
+    // Row blocks: wave w takes block w, except that when fewer than
+    // kAttnWaves blocks hold live rows (A of them), the last one is shared by
+    // waves A-1 .. kAttnWaves-1, each taking every nshare-th key block, and
+    // their states are combined at the end: a 4-row tail block then costs a
+    // SIMD a fraction of a full one.
+    const int tile_live = min(max(live_rows - rt * ROWS, 0), ROWS);
+    const int A = (tile_live + kRowsPerWave - 1) / kRowsPerWave;
+    const int nshare = (A >= 1 && A < kAttnWaves) ? kAttnWaves - A + 1 : 1;
+    const bool shared = nshare > 1 && wave >= A - 1;
+    const int sidx = shared ? wave - (A - 1) : 0;
+    const int row0 = rt * ROWS + (shared ? A - 1 : wave) * kRowsPerWave;  // first query row of this wave
     const bool active = row0 < live_rows;
     const int rho = row0 + l32;  // this lane's query row
     const int qn = rho / a.G, qh = rho - qn * a.G;
@@ -491,6 +501,39 @@ __global__ __launch_bounds__(kAttnWaves * kWave) void tree_attn_bf16_kernel(Attn
         for (int j = 0; j < 8; ++j) Pp[j] = Pn[j];
         Sa = Sb;
     };
+    // P V of block q of ring buffer bv with the probabilities P
+    auto pv = [&](auto bvc, int q, const uint32_t (&P)[8]) {
+        constexpr int bv = decltype(bvc)::value;
+#pragma unroll
+        for (int st = 0; st < 2; ++st) {
+            const bf16x8 pb =
+                __builtin_bit_cast(bf16x8, make_uint4(P[4 * st], P[4 * st + 1], P[4 * st + 2], P[4 * st + 3]));
+#pragma unroll
+            for (int db = 0; db < DB; ++db) {
+                const uint32_t v0 = vaddr[db] + bv * AttnLds<D>::kTile + q * 32 * D * 2 + st * 16 * D * 2;
+                const short4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s4)(s_kv + v0));
+                const short4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s4)(s_kv + v0 + 8 * D * 2));
+                const uint2 ul = __builtin_bit_cast(uint2, lo), uh = __builtin_bit_cast(uint2, hi);
+                const bf16x8 va = __builtin_bit_cast(bf16x8, make_uint4(ul.x, ul.y, uh.x, uh.y));
+                o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pb, o[db], 0, 0, 0);
+            }
+        }
+    };
+    // a shared block's wave: block i (block q of ring buffer bv) on its own,
+    // scores, probabilities and P V in sequence (it takes every nshare-th
+    // block only)
+    auto shared_step = [&](auto bvc, int i, int q) {
+        floatx16 S = negm;
+        qk(bvc, q, S);
+        if (masked(i)) apply_mask(S, j0_of(i));
+        uint32_t P[8];
+        float ls = row_sum(exps(S, P));
+        const bool need = !(ls <= 256.f) || l_run + ls == 0.f;
+        floatx16 none = S;
+        if (__ballot(need)) exact(S, P, ls, need, none);
+        l_run += ls;
+        pv(bvc, q, P);
+    };
     // one tile: its two block steps, then the load of tile t+3 into the
     // buffer of tile t-1 (every wave finished it before the last barrier),
     // and the wait for tile t+2 before the barrier
@@ -499,9 +542,15 @@ __global__ __launch_bounds__(kAttnWaves * kWave) void tree_attn_bf16_kernel(Attn
         using BV = std::integral_constant<int, u>;
         using BK = std::integral_constant<int, (u + 1) % kRing>;
         load_tile(k_begin + (t + 3) * kKeyTile, (u + 3) % kRing);
-        if (active) {
+        if (active && !shared) {
             if (2 * t < nblocks) step(BV{}, BK{}, 2 * t, 0);
             if (2 * t + 1 < nblocks) step(BV{}, BK{}, 2 * t + 1, 1);
+        } else if (active) {
+#pragma unroll
+            for (int q = 0; q < kBlocksPerTile; ++q) {
+                const int i = 2 * t + q;
+                if (i < nblocks && i % nshare == sidx) shared_step(BV{}, i, q);
+            }
         }
         PRESTO_WAIT_VM(2 * LPT);
         __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): this wave's LDS reads are done
@@ -516,7 +565,7 @@ __global__ __launch_bounds__(kAttnWaves * kWave) void tree_attn_bf16_kernel(Attn
     PRESTO_WAIT_VM(2 * LPT);
     __syncthreads();
     using B0 = std::integral_constant<int, 0>;
-    if (active) {
+    if (active && !shared) {
         floatx16 S0 = negm;
         qk(B0{}, 0, S0);
         if (masked(0)) apply_mask(S0, j0_of(0));
@@ -533,6 +582,43 @@ __global__ __launch_bounds__(kAttnWaves * kWave) void tree_attn_bf16_kernel(Attn
     }
     PRESTO_WAIT_VM(0);  // no load into LDS outlives the workgroup
 #undef PRESTO_WAIT_VM
+
+    // ---- the shared block's states, combined pairwise through the (now
+    // idle) tile ring: per round the waves at odd multiples of `stride` write
+    // (m, l, O) and their partners fold them in
+    if (nshare > 1) {
+        constexpr int SLOT = kWave * (16 * DB + 2);  // floats per written state
+        float* s_state = reinterpret_cast<float*>(s_kv);
+        for (int stride = 1; stride < nshare; stride *= 2) {
+            __syncthreads();  // every wave's loads have landed; the ring is free
+            const bool writer = shared && (sidx % (2 * stride)) == stride;
+            const bool reader = shared && (sidx % (2 * stride)) == 0 && sidx + stride < nshare;
+            if (writer) {
+                float* st = s_state + (sidx / (2 * stride)) * SLOT + lane;
+                st[0] = m;
+                st[kWave] = l_run;
+#pragma unroll
+                for (int db = 0; db < DB; ++db)
+#pragma unroll
+                    for (int e = 0; e < 16; ++e) st[(2 + db * 16 + e) * kWave] = o[db][e];
+            }
+            __syncthreads();
+            if (reader) {
+                const float* st = s_state + (sidx / (2 * stride)) * SLOT + lane;
+                const float m2 = st[0], l2 = st[kWave];
+                const float M = l_run > 0.f ? (l2 > 0.f ? fmaxf(m, m2) : m) : m2;
+                const float a1 = l_run > 0.f ? __builtin_amdgcn_exp2f(m - M) : 0.f;
+                const float a2 = l2 > 0.f ? __builtin_amdgcn_exp2f(m2 - M) : 0.f;
+#pragma unroll
+                for (int db = 0; db < DB; ++db)
+#pragma unroll
+                    for (int e = 0; e < 16; ++e) o[db][e] = a1 * o[db][e] + a2 * st[(2 + db * 16 + e) * kWave];
+                l_run = a1 * l_run + a2 * l2;
+                m = M;
+            }
+        }
+        if (shared && sidx != 0) return;  // the combined state is wave A-1's
+    }
 
     // ---- epilogue: lane holds row l32, d = db*32 + 8(i/4) + 4h + i%4
     if (rho >= all_rows) return;
