@@ -50,7 +50,7 @@ struct TreeArgs {
     bool rho_in_lds;
     int32_t beam_width;  // beam search only
     // LDS byte offsets
-    int o_lp, o_ids, o_kord, o_krank, o_rec, o_ktab, o_beam, o_kbeam, o_rho;
+    int o_lp, o_ids, o_kord, o_krank, o_rec, o_pkey, o_ktab, o_beam, o_kbeam, o_rho;
     // literal Alg. 2 only: T (capacity budget + branch - 1) in LDS
     int o_tmeta, o_tS, o_tkey, o_tplace;
 };
@@ -431,22 +431,25 @@ __global__ __launch_bounds__(kWave) void tree_build_kernel(TreeArgs a) {
         }
     };
 
-    // Rank-path key (four 32-bit words, most significant first) of the child
-    // of committed node p with candidate rank r at depth d.
-    auto child_key = [&](int p, int r, int d, uint32_t (&kw)[4]) {
-        kw[0] = kw[1] = kw[2] = kw[3] = 0u;
-        int x = p, dx = d, rx = r;
-        while (dx > 0) {
-            const int wi = (dx - 1) / per_word, sh = 32 - ((dx - 1) % per_word + 1) * wbits;
-#pragma unroll
-            for (int q = 0; q < 4; ++q) kw[q] |= q == wi ? (uint32_t)(rx + 1) << sh : 0u;
-            if (x == 0) break;
-            const uint32_t m = s_rec[x].x;
-            rx = (m >> 10) & 15;
-            dx = (m >> 14) & 63;
-            x = m & 1023;
-        }
+    // Rank-path keys (four 32-bit words, most significant first): the key of
+    // a node is its parent's key with the digit rank + 1 at its depth.  They
+    // only break ties of S, so they are derived when a tie needs them: the
+    // parent chain of a tied entry is walked up to the nearest node whose key
+    // is known (the root, or a node whose key an earlier tie stored: every
+    // non-root key has a nonzero first word) and the parent's key is stored.
+    uint4* s_pkey = reinterpret_cast<uint4*>(lds + a.o_pkey);  // [N], 0 = not known yet
+    const uint32_t pw_magic = (65536u + per_word - 1) / per_word;  // t / per_word = t * magic >> 16 (t < 128)
+    auto add_digit = [&](uint4 key, int d, int r) {
+        const uint32_t t = (uint32_t)(d - 1);
+        const uint32_t wi = (t * pw_magic) >> 16;
+        const uint32_t v = (uint32_t)(r + 1) << (32 - (t - wi * per_word + 1) * wbits);
+        key.x |= wi == 0 ? v : 0u;
+        key.y |= wi == 1 ? v : 0u;
+        key.z |= wi == 2 ? v : 0u;
+        key.w |= wi == 3 ? v : 0u;
+        return key;
     };
+    for (int i = lane; i < N; i += kWave) s_pkey[i] = make_uint4(0u, 0u, 0u, 0u);
 
     if (lane == 0) s_rec[0] = make_uint2(0xffffffffu, __float_as_uint(0.f));
     uint32_t c_ord;
@@ -493,8 +496,21 @@ __global__ __launch_bounds__(kWave) void tree_build_kernel(TreeArgs a) {
             int bj = 0;
             for (int j = 0; j < A; ++j) {
                 if (fS[j] == M) {
-                    uint32_t kw[4];
-                    child_key(fM[j] & 1023, (fM[j] >> 10) & 15, (fM[j] >> 14) & 63, kw);
+                    const int p = fM[j] & 1023;
+                    uint4 acc = make_uint4(0u, 0u, 0u, 0u);
+                    int y = p;
+                    uint4 st = s_pkey[y];
+                    uint32_t m = s_rec[y].x;
+                    while (y != 0 && st.x == 0u) {
+                        acc = add_digit(acc, (m >> 14) & 63, (m >> 10) & 15);
+                        y = m & 1023;
+                        st = s_pkey[y];
+                        m = s_rec[y].x;
+                    }
+                    const uint4 kp = make_uint4(acc.x | st.x, acc.y | st.y, acc.z | st.z, acc.w | st.w);
+                    if (y != p) s_pkey[p] = kp;  // lanes storing the same node store the same key
+                    const uint4 kv = add_digit(kp, (fM[j] >> 14) & 63, (fM[j] >> 10) & 15);
+                    const uint32_t kw[4] = {kv.x, kv.y, kv.z, kv.w};
                     const bool less =
                         kw[0] != bk[0] ? kw[0] < bk[0]
                                        : (kw[1] != bk[1] ? kw[1] < bk[1]
@@ -882,7 +898,7 @@ static int align16(int x) { return (x + 15) & ~15; }
 
 struct TreeLayout {
     int total_no_rho, total_with_rho;
-    int o_lp, o_ids, o_kord, o_krank, o_rec, o_ktab, o_beam, o_kbeam, o_rho;
+    int o_lp, o_ids, o_kord, o_krank, o_rec, o_pkey, o_ktab, o_beam, o_kbeam, o_rho;
 };
 
 static TreeLayout tree_layout(int D, int k, int N, int Wb) {
@@ -896,6 +912,7 @@ static TreeLayout tree_layout(int D, int k, int N, int Wb) {
     L.o_beam = off; off = align16(off + 2 * Wb * (int)sizeof(BeamEntry));
     L.o_kbeam = off; off = align16(off + (Wb > 0 ? N * k : 0));  // beam search only
     L.o_rec = off; off = align16(off + N * 8);
+    L.o_pkey = off; off = align16(off + N * 16);
     L.total_no_rho = off;
     L.o_rho = off;
     L.total_with_rho = align16(off + D * k * k * k * 4);
@@ -1016,6 +1033,7 @@ presto_status launch_build_tree(const presto_tree_desc* desc, const int32_t* ids
     a.beam_width = beam ? desc->beam_width : 0;
     const TreeLayout L = tree_layout(a.D, a.k, a.N, a.beam_width);
     a.o_lp = L.o_lp; a.o_ids = L.o_ids; a.o_kord = L.o_kord; a.o_krank = L.o_krank; a.o_rec = L.o_rec;
+    a.o_pkey = L.o_pkey;
     a.o_ktab = L.o_ktab; a.o_beam = L.o_beam; a.o_kbeam = L.o_kbeam;
     a.o_rho = L.o_rho;
     a.rho_in_lds = log_rho != nullptr && L.total_with_rho <= kTreeLdsBudget;
