@@ -7,10 +7,11 @@
 // committed).  The frontier lives in registers spread over the 64 lanes (SL
 // slots per lane), each slot only (S, packed metadata): a pop is a per-lane
 // max, one DPP wave max and a ballot; the next sibling of a popped node is
-// one LDS read.  Rank-path keys are rebuilt from the parent records only
-// when several frontier entries share the best S; token ids, the output rows
-// and the ancestor bitmasks are produced after the search, in parallel over
-// the nodes.
+// one LDS read.  Rank-path keys are only derived when several frontier
+// entries share the best S (from the parent records, up to the nearest node
+// whose key an earlier tie stored); token ids, the output rows and the
+// ancestor bitmasks are produced after the search, in parallel over the
+// nodes.
 //
 // Frontier policy.  Committing nodes in pop order yields the B best prefixes
 // under the total order (S desc, rank path asc).  Instead of pushing all of

@@ -199,3 +199,25 @@ def test_tree_large_budgets_random(D, k, branch, B, mode):
             g, o = _gpu_and_oracle(ids, lp, rho, lam, root, D, k, B, branch=branch,
                                    beam_width=10 if mode == "beam10" else 0, alg2=mode == "alg2")
             _assert_same(g, o)
+
+
+@pytest.mark.parametrize("D,k,B", [(32, 3, 700), (32, 2, 1023), (20, 5, 400)])
+@pytest.mark.parametrize("mode", ["best_first", "beam10", "alg2"])
+def test_tree_deep_ties(D, k, B, mode):
+    """Whole tied subtrees: lambda = 0 and log q on a coarse grid with equal
+    candidates in most rows, so siblings with equal log q root score-identical
+    subtrees and most pops break a tie of S by rank-path keys, deep in the
+    tree and several times under the same ancestors."""
+    rng = np.random.default_rng([D, k, B, 31])
+    b = 8
+    lp = -np.round(rng.exponential(1.0, size=(b, D, k)) * 2) / 2
+    lp[:, :, 1] = lp[:, :, 0]  # the two best candidates of every row tie
+    lp = -np.sort(-lp, axis=2).astype(np.float32)
+    ids = np.stack([[rng.choice(5000, k, replace=False) for _ in range(D)] for _ in range(b)]).astype(np.int32)
+    root = rng.integers(0, 5000, size=b).astype(np.int32)
+    lam = np.zeros(D, np.float32)
+    g, o = _gpu_and_oracle(ids, lp, None, lam, root, D, k, B, beam_width=10 if mode == "beam10" else 0,
+                           alg2=mode == "alg2")
+    _assert_same(g, o)
+    ties = sum(int((np.diff(np.sort(row[np.isfinite(row)])) == 0).sum()) for row in o["score"][:, 1:])
+    assert ties > b * 10  # ties really occur
