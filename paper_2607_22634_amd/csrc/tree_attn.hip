@@ -121,9 +121,18 @@ __device__ __forceinline__ int xcd_task(int bid, int n_blocks) {
 __device__ __forceinline__ void lds_load16(const void* gptr, uint32_t lds) {
     asm volatile("global_load_lds_dwordx4 %0, off" ::"v"(gptr), "{m0}"(lds) : "memory");
 }
-// the same with a wave-uniform base and a per-lane 32-bit byte offset
+// the same with a wave-uniform base and a per-lane 32-bit byte offset (the
+// base and the LDS address are read from the first lane, so that they are
+// scalar operands whatever registers the caller computed them in)
 __device__ __forceinline__ void lds_load16(const void* base, uint32_t off, uint32_t lds) {
-    asm volatile("global_load_lds_dwordx4 %0, %1" ::"v"(off), "s"(base), "{m0}"(lds) : "memory");
+    const uint64_t b = (uint64_t)(uintptr_t)base;
+    // readfirstlane returns a signed int: both halves go through uint32_t so
+    // that the low half is zero-extended, not sign-extended, into the pointer
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)b);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)(b >> 32));
+    const uint64_t sb = ((uint64_t)hi << 32) | (uint64_t)lo;
+    const uint32_t m0v = (uint32_t)__builtin_amdgcn_readfirstlane(lds);
+    asm volatile("global_load_lds_dwordx4 %0, %1" ::"v"(off), "s"(sb), "{m0}"(m0v) : "memory");
 }
 
 template <int D>
