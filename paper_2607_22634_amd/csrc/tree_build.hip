@@ -140,6 +140,15 @@ __device__ __forceinline__ void stage_words(uint32_t* dst, const uint32_t* src, 
     }
 }
 
+// x with lane l replaced by v (v and l are read from the first lane, so they
+// are scalar operands whatever registers hold them).
+__device__ __forceinline__ uint32_t write_lane(uint32_t x, uint32_t v, int l) {
+    const uint32_t sv = (uint32_t)__builtin_amdgcn_readfirstlane(v);
+    const uint32_t sl = (uint32_t)__builtin_amdgcn_readfirstlane(l);
+    asm("v_writelane_b32 %0, %1, m0" : "+v"(x) : "s"(sv), "{m0}"(sl));
+    return x;
+}
+
 // Number of frontier slots per lane a pop works on (a compile-time tag).
 template <int A>
 struct SlotCount {
@@ -578,12 +587,29 @@ __global__ __launch_bounds__(kWave) void tree_build_kernel(TreeArgs a) {
         }
         const bool second = yS != 0u;
         const int ylane = fcount & (kWave - 1), yslot = fcount >> 6;
+        if constexpr (A <= 2) {
+            // one lane of one slot each: lane writes from scalar values (with
+            // a single slot in use both go to slot 0)
 #pragma unroll
-        for (int j = 0; j < A; ++j) {
-            const bool px = lane == w && j == eslot;
-            const bool py = second && lane == ylane && j == yslot;
-            fS[j] = px ? xS : (py ? yS : fS[j]);
-            fM[j] = px ? xM : (py ? yM : fM[j]);
+            for (int j = 0; j < A; ++j) {
+                if (A == 1 || j == eslot) {
+                    fS[j] = write_lane(fS[j], xS, w);
+                    fM[j] = write_lane(fM[j], xM, w);
+                }
+                if (second && (A == 1 || j == yslot)) {
+                    fS[j] = write_lane(fS[j], yS, ylane);
+                    fM[j] = write_lane(fM[j], yM, ylane);
+                }
+            }
+        } else {
+            // more slots: one select per slot instead of a branch per slot
+#pragma unroll
+            for (int j = 0; j < A; ++j) {
+                const bool px = lane == w && j == eslot;
+                const bool py = second && lane == ylane && j == yslot;
+                fS[j] = px ? xS : (py ? yS : fS[j]);
+                fM[j] = px ? xM : (py ? yM : fM[j]);
+            }
         }
         if (second) ++fcount;
         return true;
