@@ -54,6 +54,10 @@ struct TreeArgs {
     int o_lp, o_ids, o_kord, o_krank, o_rec, o_pkey, o_ktab, o_beam, o_kbeam, o_rho;
     // literal Alg. 2 only: T (capacity budget + branch - 1) in LDS
     int o_tmeta, o_tS, o_tkey, o_tplace;
+    // frontier sweeps only: lambda, the sorted best set, the pending
+    // prefixes and the parent positions
+    int o_lam, o_sw_t, o_sw_p, o_sw_par, o_sw_cnt, o_sw_np;
+    uint32_t mag_k, mag_k3;  // ceil(2^32 / k), ceil(2^32 / k^3) (k > 1): n / d = umulhi(n, mag) for n < 2^20
 };
 
 // Frontier metadata in one word: parent node (10 bits), candidate rank (4),
@@ -915,6 +919,509 @@ __global__ __launch_bounds__(kWave) void tree_alg2_kernel(TreeArgs a) {
     }
     if (lane == 0) a.n_nodes[b] = keep + 1;
 }
+
+// ---------------------------------------------------------------------------
+// Best-first tree by frontier sweeps.
+//
+// Every token score is <= 0, so S never increases along a path and an
+// ancestor precedes its descendants in the total order (S desc, rank path
+// asc): the nodes that best-first search commits, in pop order, are the
+// `budget` best non-root prefixes in that order (the closed form of Sec.
+// 4.2), sorted.  This kernel finds that set without popping one node at a
+// time.  One wavefront per sequence keeps in LDS
+//   T: the best (at most budget) prefixes materialised so far, sorted;
+//   P: pending prefixes, each the first child or the next sibling (in child
+//      order: S desc, rank asc, among the top-`branch` candidates) of a
+//      prefix that entered T, not materialised yet.
+// A sweep merges all of P into T (every entry's new place from counting
+// comparisons; entries pushed past the budget are dropped for good, since
+// T's last entry only ever improves) and then, for every prefix of P that
+// entered T, pushes its first child and its next sibling, keeping a push
+// while T is not full or when it precedes T's last entry.  A prefix of the
+// optimal tree is always pushed (its parent, or its previous sibling,
+// precedes it and so enters T when materialised) and never dropped (it
+// precedes every last entry T ever has), so T is the optimal tree once
+// nothing is pending.  A prefix is pushed at most once (by its parent, or by
+// its previous sibling), and a sweep pushes at most two prefixes per entry
+// that entered T, so P never holds more than 2 budget.  The number of
+// sweeps follows the depth of the tree (about 15 at depth 16), not the
+// budget.
+//
+// Every record carries its full rank-path key, its parent's S and the ranks
+// of its trigram context, so that a push reads no other record; a node's
+// parent is found after the search by a binary search of T for the
+// parent's (S, key).
+
+// A record: ord(S), rank-path key (k0 most significant), ord(S) of the
+// parent, and rank | depth << 4 | parent's rank << 10 | grandparent's rank
+// << 14.  In LDS two 16-byte words: (o, k0, k1, k2), (k3, po, meta, 0).
+struct SwRec {
+    uint32_t o, k0, k1, k2, k3, po, meta;
+};
+
+__device__ __forceinline__ SwRec sw_load(const uint4* base, int i) {
+    const uint4 x = base[2 * i], y = base[2 * i + 1];
+    return SwRec{x.x, x.y, x.z, x.w, y.x, y.y, y.z};
+}
+__device__ __forceinline__ void sw_store(uint4* base, int i, const SwRec& r) {
+    base[2 * i] = make_uint4(r.o, r.k0, r.k1, r.k2);
+    base[2 * i + 1] = make_uint4(r.k3, r.po, r.meta, 0u);
+}
+// The rank-path key of x is smaller than that of y.  Written with bitwise
+// operators throughout: short-circuit forms compile to divergent branches.
+__device__ __forceinline__ bool sw_key_less(const SwRec& x, const SwRec& y) {
+    const uint64_t xa = ((uint64_t)x.k0 << 32) | (uint64_t)x.k1;
+    const uint64_t ya = ((uint64_t)y.k0 << 32) | (uint64_t)y.k1;
+    const uint64_t xb = ((uint64_t)x.k2 << 32) | (uint64_t)x.k3;
+    const uint64_t yb = ((uint64_t)y.k2 << 32) | (uint64_t)y.k3;
+    return (xa < ya) | ((xa == ya) & (xb < yb));
+}
+// x precedes y in the total order (keys of distinct prefixes differ)
+__device__ __forceinline__ bool sw_before(const SwRec& x, const SwRec& y) {
+    return (x.o > y.o) | ((x.o == y.o) & sw_key_less(x, y));
+}
+__device__ __forceinline__ SwRec sw_readlane(const SwRec& r, int l) {
+    SwRec y;
+    y.o = (uint32_t)__builtin_amdgcn_readlane((int)r.o, l);
+    y.k0 = (uint32_t)__builtin_amdgcn_readlane((int)r.k0, l);
+    y.k1 = (uint32_t)__builtin_amdgcn_readlane((int)r.k1, l);
+    y.k2 = (uint32_t)__builtin_amdgcn_readlane((int)r.k2, l);
+    y.k3 = (uint32_t)__builtin_amdgcn_readlane((int)r.k3, l);
+    y.po = 0u;
+    y.meta = 0u;
+    return y;
+}
+__device__ __forceinline__ int lanes_below(uint64_t m) {
+    return (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+}
+
+constexpr int kSweepWaves = 4;  // one wave per SIMD
+
+// MT: slots per lane of T (budget <= 64 MT), MP: slots per lane of P
+// (2 budget <= 64 MP), KM: k <= KM, RHO as in tree_build_kernel.
+//
+// One workgroup of four waves per sequence.  Every wave holds all of T and
+// P in registers; the merge's comparisons are split over the waves (each
+// takes every fourth P entry in turn and its partial counts are summed
+// through LDS), the pushes are split into tasks (first children, next
+// siblings) per slot of P, and each task reserves its places in the next P
+// with one LDS atomic.  A sweep has two barriers: after the partial counts,
+// and after the stores and pushes.
+template <int MT, int MP, int KM, int RHO>
+__global__ __launch_bounds__(kSweepWaves * kWave) void tree_sweep_kernel(TreeArgs a) {
+    constexpr int NWV = kSweepWaves, NT = NWV * kWave;
+    extern __shared__ __align__(16) char lds[];
+    const int tid = threadIdx.x, lane = lane_id();
+    const int wv = __builtin_amdgcn_readfirstlane(tid / kWave);
+    const int b = blockIdx.x;
+    const int D = a.D, k = a.k, N = a.N, W = a.W, wbits = a.wbits, per_word = a.per_word;
+    const int NB = N - 1;             // non-root nodes of a full tree
+    const int cap_p = max(2 * NB, 1);  // P's capacity
+    float* s_lp = reinterpret_cast<float*>(lds + a.o_lp);
+    int32_t* s_ids = reinterpret_cast<int32_t*>(lds + a.o_ids);
+    float* s_lam = reinterpret_cast<float*>(lds + a.o_lam);
+    uint4* s_t = reinterpret_cast<uint4*>(lds + a.o_sw_t);          // [NB] records, sorted
+    uint4* s_p = reinterpret_cast<uint4*>(lds + a.o_sw_p);          // [cap_p] records
+    int32_t* s_par = reinterpret_cast<int32_t*>(lds + a.o_sw_par);  // [N] parent of node i
+    int32_t* s_cnt = reinterpret_cast<int32_t*>(lds + a.o_sw_cnt);  // [NWV][MT + MP][64] partial counts
+    int32_t* s_np = reinterpret_cast<int32_t*>(lds + a.o_sw_np);    // [2] pending counts, alternating
+    float* s_rho = reinterpret_cast<float*>(lds + a.o_rho);
+    const int rho_n = D * k * k * k;
+    const float* g_rho = RHO ? a.log_rho + (int64_t)b * rho_n : nullptr;
+
+    const int64_t tb = (int64_t)b * D * k;
+    if (wv == 0) {
+        uint32_t r_lp[8], r_ids[8], r_rho[16];  // D * k <= 512 words
+        load_words(r_lp, reinterpret_cast<const uint32_t*>(a.logprob + tb), D * k, 0, lane);
+        load_words(r_ids, reinterpret_cast<const uint32_t*>(a.ids + tb), D * k, 0, lane);
+        if constexpr (RHO == 1) load_words(r_rho, reinterpret_cast<const uint32_t*>(g_rho), rho_n, 0, lane);
+        const float lam = lane < D ? a.lambda[(int64_t)b * a.lambda_stride + lane] : 0.f;
+        store_words(reinterpret_cast<uint32_t*>(s_lp), r_lp, D * k, 0, lane);
+        store_words(reinterpret_cast<uint32_t*>(s_ids), r_ids, D * k, 0, lane);
+        if (lane < D) s_lam[lane] = lam;
+        if constexpr (RHO == 1) {
+            store_words(reinterpret_cast<uint32_t*>(s_rho), r_rho, rho_n, 0, lane);
+            if (rho_n > 16 * kWave)
+                stage_words(reinterpret_cast<uint32_t*>(s_rho) + 16 * kWave,
+                            reinterpret_cast<const uint32_t*>(g_rho) + 16 * kWave, rho_n - 16 * kWave,
+                            lane);
+        }
+    }
+    __syncthreads();
+    // Token scores fl(log q + fl(lambda * log rho)), NaN -> -inf, computed
+    // once per trigram context in place of the lattice (or of the log q
+    // table without one), so that scoring a node's children reads k values.
+    // A lattice read from global memory is scored on the fly instead.
+    if constexpr (RHO == 0) {
+        for (int i = tid; i < D * k; i += NT) {
+            const float v = s_lp[i];
+            s_lp[i] = (v == v) ? v : -INFINITY;
+        }
+    } else if constexpr (RHO == 1) {
+#pragma unroll 4
+        for (int i = tid; i < rho_n; i += NT) {
+            const int row = k == 1 ? i : (int)__umulhi((uint32_t)i, a.mag_k3);
+            const int r = k == 1 ? 0 : i - (int)__umulhi((uint32_t)i, a.mag_k) * k;
+            const float lq = s_lp[row * k + r];
+            const float t = s_lam[row] * s_rho[i];
+            const float v = lq + t;
+            s_rho[i] = (v == v) ? v : -INFINITY;
+        }
+    }
+    __syncthreads();
+
+    const uint32_t pw_magic = (65536u + per_word - 1) / per_word;  // t / per_word = t * magic >> 16 (t < 128)
+    // the key with the digit of depth d set to rank r + 1 (cleared first)
+    auto with_digit = [&](SwRec x, int d, int r) {
+        const uint32_t t = (uint32_t)(d - 1);
+        const uint32_t wi = (t * pw_magic) >> 16;
+        const uint32_t sh = 32u - (t - wi * (uint32_t)per_word + 1u) * (uint32_t)wbits;
+        const uint32_t m = ((1u << wbits) - 1u) << sh;
+        const uint32_t v = (uint32_t)(r + 1) << sh;
+        x.k0 = wi == 0 ? (x.k0 & ~m) | v : x.k0;
+        x.k1 = wi == 1 ? (x.k1 & ~m) | v : x.k1;
+        x.k2 = wi == 2 ? (x.k2 & ~m) | v : x.k2;
+        x.k3 = wi == 3 ? (x.k3 & ~m) | v : x.k3;
+        return x;
+    };
+
+    // The best child, in child order, of a node with score Sn whose children
+    // sit at drafter row `row` in trigram context (c2, c1): with `first`,
+    // the first child; otherwise the first one after the child (ao, ar) (its
+    // ord S and rank).  The top-`branch` by (token score desc, rank asc) are
+    // children.  Returns ord S of the child, 0 if there is none.
+    auto child = [&](int row, int c2, int c1, float Sn, bool first, uint32_t ao, int ar, int& r_out,
+                     float& S_out) -> uint32_t {
+        float s[KM];
+        if constexpr (RHO == 2) {
+            const float lam = s_lam[row];
+#pragma unroll
+            for (int r = 0; r < KM; ++r) {
+                const int rr = r < k ? r : k - 1;
+                const float lq = s_lp[row * k + rr];
+                const float lr = g_rho[((row * k + c2) * k + c1) * k + rr];
+                const float t = lam * lr;
+                const float v = lq + t;
+                s[r] = (v == v) ? v : -INFINITY;
+            }
+        } else {
+            const float* sc = RHO == 1 ? s_rho + ((row * k + c2) * k + c1) * k : s_lp + row * k;
+            if (KM == 4 && k == 4) {
+                const float4 v = *reinterpret_cast<const float4*>(sc);  // 16-byte aligned: offsets are multiples of 4 words
+                s[0] = v.x;
+                s[1] = v.y;
+                s[2] = v.z;
+                s[3] = v.w;
+            } else {
+#pragma unroll
+                for (int r = 0; r < KM; ++r) s[r] = sc[r < k ? r : k - 1];
+            }
+        }
+        uint32_t bo = 0u;
+        int br = 0;
+        float bS = 0.f;
+#pragma unroll
+        for (int r = 0; r < KM; ++r) {
+            if (r < k) {
+                bool sel = true;
+                if (a.branch < k) {
+                    int c = 0;
+#pragma unroll
+                    for (int j = 0; j < KM; ++j)
+                        c += ((j < k) & ((s[j] > s[r]) | ((s[j] == s[r]) & (j < r)))) ? 1 : 0;
+                    sel = c < a.branch;
+                }
+                const float Sc = Sn + s[r];
+                const uint32_t oc = ord32(Sc);
+                const bool after = first | (oc < ao) | ((oc == ao) & (r > ar));
+                const bool take = sel & after & (oc > bo);
+                bo = take ? oc : bo;
+                br = take ? r : br;
+                bS = take ? Sc : bS;
+            }
+        }
+        r_out = br;
+        S_out = bS;
+        return bo;
+    };
+
+    // P starts as the root's first child
+    if (tid == 0) {
+        int r;
+        float Sc;
+        const uint32_t oc = child(0, 0, 0, 0.f, true, 0u, 0, r, Sc);
+        SwRec c{oc, 0u, 0u, 0u, 0u, ord32(0.f), (uint32_t)r | (1u << 4)};
+        c = with_digit(c, 1, r);
+        sw_store(s_p, 0, c);
+        s_np[0] = oc != 0u ? 1 : 0;
+        s_np[1] = 0;
+    }
+    __syncthreads();
+
+    int nt = 0, cur = 0;
+    int np = min(s_np[0], cap_p);
+    while (np > 0) {
+        // P in slots (entry u * 64 + lane), T likewise (position v * 64 + lane)
+        SwRec pr[MP], tr[MT];
+        bool pv[MP], tv[MT];
+#pragma unroll
+        for (int u = 0; u < MP; ++u) {
+            pv[u] = u * kWave + lane < np;
+            pr[u] = SwRec{0u, 0u, 0u, 0u, 0u, 0u, 0u};
+            if (u * kWave < np) pr[u] = sw_load(s_p, min(u * kWave + lane, np - 1));
+        }
+#pragma unroll
+        for (int v = 0; v < MT; ++v) {
+            tv[v] = v * kWave + lane < nt;
+            tr[v] = SwRec{0u, 0u, 0u, 0u, 0u, 0u, 0u};
+            if (v * kWave < nt) tr[v] = sw_load(s_t, min(v * kWave + lane, nt - 1));
+        }
+        if (tid == 0) s_np[cur ^ 1] = 0;  // last read a sweep ago, before two barriers
+
+        // merged places: a T entry moves down by the P entries before it; a P
+        // entry lands after the T and P entries before it.  Each P entry in
+        // turn is read from its lane and compared with all entries at once,
+        // on S alone unless some S equals its S (then the keys decide); wave
+        // w takes the entries l = w (mod 4) of every slot.  AT, AP: the slots
+        // that hold entries this sweep.
+        int tc[MT], pc[MP];
+#pragma unroll
+        for (int v = 0; v < MT; ++v) tc[v] = 0;
+#pragma unroll
+        for (int u = 0; u < MP; ++u) pc[u] = 0;
+        auto count = [&](auto at, auto ap) {
+            constexpr int AT = decltype(at)::value, AP = decltype(ap)::value;
+#pragma unroll
+            for (int u = 0; u < AP; ++u) {
+                const int cnt = min(kWave, np - u * kWave);
+                for (int l = wv; l < cnt; l += NWV) {
+                    const uint32_t yo = (uint32_t)__builtin_amdgcn_readlane((int)pr[u].o, l);
+                    bool teq[AT], peq[AP];
+                    bool eq_any = false;
+                    int before = 0;
+#pragma unroll
+                    for (int v = 0; v < AT; ++v) {
+                        before += __popcll(__ballot(tv[v] & (tr[v].o > yo)));
+                        tc[v] += (tv[v] & (tr[v].o < yo)) ? 1 : 0;
+                        teq[v] = tv[v] & (tr[v].o == yo);
+                        eq_any |= teq[v];
+                    }
+#pragma unroll
+                    for (int q = 0; q < AP; ++q) {
+                        pc[q] += (pv[q] & (pr[q].o < yo)) ? 1 : 0;
+                        peq[q] = pv[q] & (pr[q].o == yo) & !((q == u) & (lane == l));
+                        eq_any |= peq[q];
+                    }
+                    if (__ballot(eq_any) != 0ull) {
+                        const SwRec y = sw_readlane(pr[u], l);
+#pragma unroll
+                        for (int v = 0; v < AT; ++v) {
+                            const bool g = sw_key_less(tr[v], y);
+                            before += __popcll(__ballot(teq[v] & g));
+                            tc[v] += (teq[v] & !g) ? 1 : 0;
+                        }
+#pragma unroll
+                        for (int q = 0; q < AP; ++q) pc[q] += (peq[q] & sw_key_less(y, pr[q])) ? 1 : 0;
+                    }
+                    pc[u] += lane == l ? before : 0;
+                }
+            }
+        };
+        auto count_p = [&](auto at) {
+            if (np <= kWave) count(at, SlotCount<1>{});
+            else if (MP <= 2 || np <= 2 * kWave) count(at, SlotCount<(MP < 2 ? MP : 2)>{});
+            else if (MP <= 4 || np <= 4 * kWave) count(at, SlotCount<(MP < 4 ? MP : 4)>{});
+            else count(at, SlotCount<MP>{});
+        };
+        if (nt <= kWave) count_p(SlotCount<1>{});
+        else if (MT <= 2 || nt <= 2 * kWave) count_p(SlotCount<(MT < 2 ? MT : 2)>{});
+        else count_p(SlotCount<MT>{});
+
+        // sum of the four waves' counts
+        int32_t* my_cnt = s_cnt + wv * (MT + MP) * kWave;
+#pragma unroll
+        for (int v = 0; v < MT; ++v)
+            if (v * kWave < nt) my_cnt[v * kWave + lane] = tc[v];
+#pragma unroll
+        for (int u = 0; u < MP; ++u)
+            if (u * kWave < np) my_cnt[(MT + u) * kWave + lane] = pc[u];
+        __syncthreads();
+#pragma unroll
+        for (int v = 0; v < MT; ++v) {
+            if (v * kWave < nt) {
+                int c = 0;
+#pragma unroll
+                for (int w = 0; w < NWV; ++w) c += s_cnt[(w * (MT + MP) + v) * kWave + lane];
+                tc[v] = c;
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < MP; ++u) {
+            if (u * kWave < np) {
+                int c = 0;
+#pragma unroll
+                for (int w = 0; w < NWV; ++w) c += s_cnt[(w * (MT + MP) + MT + u) * kWave + lane];
+                pc[u] = c;
+            }
+        }
+
+        // moved T entries and the P entries that made it go to their places
+        // (every wave read every record before the barrier); slot j of the
+        // two lists is stored by wave j mod 4
+#pragma unroll
+        for (int v = 0; v < MT; ++v) {
+            const int to = v * kWave + lane + tc[v];
+            if (v % NWV == wv && v * kWave < nt && (tv[v] & (tc[v] != 0) & (to < NB))) sw_store(s_t, to, tr[v]);
+        }
+#pragma unroll
+        for (int u = 0; u < MP; ++u)
+            if ((MT + u) % NWV == wv && u * kWave < np && (pv[u] & (pc[u] < NB))) sw_store(s_t, pc[u], pr[u]);
+        const int nt_new = min(NB, nt + np);
+        const bool full = nt_new == NB;
+        // T's last entry, from the registers
+        SwRec last = SwRec{0u, 0u, 0u, 0u, 0u, 0u, 0u};
+        if (full) {
+#pragma unroll
+            for (int v = 0; v < MT; ++v) {
+                if (v * kWave < nt) {
+                    const uint64_t m = __ballot(tv[v] & (v * kWave + lane + tc[v] == NB - 1));
+                    if (m) last = sw_readlane(tr[v], __ffsll((unsigned long long)m) - 1);
+                }
+            }
+#pragma unroll
+            for (int u = 0; u < MP; ++u) {
+                if (u * kWave < np) {
+                    const uint64_t m = __ballot(pv[u] & (pc[u] == NB - 1));
+                    if (m) last = sw_readlane(pr[u], __ffsll((unsigned long long)m) - 1);
+                }
+            }
+        }
+
+        // pushes of the P entries that entered T: task 2u (first children of
+        // slot u) and task 2u + 1 (next siblings) go to wave task mod 4; a
+        // task takes its places in the next P with one atomic
+        auto push = [&](bool h, const SwRec& c) {
+            const uint64_t m = __ballot(h);
+            if (m == 0ull) return;
+            int base = 0;
+            if (lane == 0) base = atomicAdd(&s_np[cur ^ 1], __popcll(m));
+            base = __builtin_amdgcn_readlane(base, 0);
+            const int at = base + lanes_below(m);
+            if (h & (at < cap_p)) sw_store(s_p, at, c);
+        };
+#pragma unroll
+        for (int u = 0; u < MP; ++u) {
+            if (u * kWave >= np) break;
+            const SwRec& w = pr[u];
+            const bool in = pv[u] & (pc[u] < NB);
+            const int d = (int)(w.meta >> 4) & 63, r = (int)(w.meta & 15);
+            const int rp = (int)(w.meta >> 10) & 15, rg = (int)(w.meta >> 14) & 15;
+            if ((2 * u) % NWV == wv) {
+                // first child (depth d + 1, drafter row d); rows clamped for
+                // lanes without a valid entry
+                const int drow = min(max(d, 0), D - 1);
+                int cr;
+                float cS;
+                const uint32_t co =
+                    child(drow, d >= 2 ? rp : 0, d >= 1 ? r : 0, unord32(w.o), true, 0u, 0, cr, cS);
+                SwRec ca{co, w.k0, w.k1, w.k2, w.k3, w.o,
+                         (uint32_t)cr | ((uint32_t)(d + 1) << 4) | ((uint32_t)r << 10) | ((uint32_t)rp << 14)};
+                ca = with_digit(ca, min(d + 1, D), cr);
+                push(in & (d < D) & (co != 0u) & (!full | sw_before(ca, last)), ca);
+            }
+            if ((2 * u + 1) % NWV == wv) {
+                // next sibling (depth d, drafter row d - 1, the parent's context)
+                const int srow = min(max(d - 1, 0), D - 1);
+                int sr;
+                float sS;
+                const uint32_t so = child(srow, d - 1 >= 2 ? rg : 0, d - 1 >= 1 ? rp : 0, unord32(w.po), false,
+                                          w.o, r, sr, sS);
+                SwRec cb{so, w.k0, w.k1, w.k2, w.k3, w.po,
+                         (uint32_t)sr | ((uint32_t)d << 4) | ((uint32_t)rp << 10) | ((uint32_t)rg << 14)};
+                cb = with_digit(cb, max(d, 1), sr);
+                push(in & (so != 0u) & (!full | sw_before(cb, last)), cb);
+            }
+        }
+        nt = nt_new;
+        __syncthreads();
+        cur ^= 1;
+        np = min(s_np[cur], cap_p);
+    }
+
+    // parents: node i >= 1 is T's position i - 1; the parent of a node of
+    // depth d > 1 is the T entry with the parent's (S, key), found by binary
+    // search (it precedes the node, so its position is smaller)
+    if (tid == 0) s_par[0] = -1;
+    const int top = nt > 0 ? 1 << (31 - __clz(nt)) : 0;
+    for (int p = tid; p < nt; p += NT) {
+        const SwRec x = sw_load(s_t, p);
+        const int d = (int)(x.meta >> 4) & 63;
+        int par = 0;
+        if (d > 1) {
+            SwRec tg = x;
+            tg.o = x.po;
+            const uint32_t t = (uint32_t)(d - 1);
+            const uint32_t wi = (t * pw_magic) >> 16;
+            const uint32_t sh = 32u - (t - wi * (uint32_t)per_word + 1u) * (uint32_t)wbits;
+            const uint32_t m = ~(((1u << wbits) - 1u) << sh);
+            tg.k0 &= wi == 0 ? m : ~0u;
+            tg.k1 &= wi == 1 ? m : ~0u;
+            tg.k2 &= wi == 2 ? m : ~0u;
+            tg.k3 &= wi == 3 ? m : ~0u;
+            int q = 0;
+            for (int step = top; step > 0; step >>= 1) {
+                const int c = q + step;
+                if (c <= nt && sw_before(sw_load(s_t, c - 1), tg)) q = c;
+            }
+            par = min(q + 1, p);
+        }
+        s_par[p + 1] = par;
+    }
+    __syncthreads();
+
+    // output rows and ancestor masks (the parent chain, at most D steps)
+    constexpr int SLW = MT + 1;  // W = ceil((budget + 1) / 64) <= MT + 1
+    const int64_t ob = (int64_t)b * N;
+    const int root_tok = __builtin_amdgcn_readfirstlane(a.root_token[b]);
+    for (int i = tid; i < N; i += NT) {
+        uint64_t words[SLW];
+#pragma unroll
+        for (int q = 0; q < SLW; ++q) words[q] = 0ull;
+        if (i == 0) {
+            a.parent[ob] = -1;
+            a.token[ob] = root_tok;
+            a.depth[ob] = 0;
+            a.rank[ob] = -1;
+            a.score[ob] = 0.f;
+            words[0] = 1ull;
+        } else if (i <= nt) {
+            const SwRec x = sw_load(s_t, i - 1);
+            const int d = (int)(x.meta >> 4) & 63, r = (int)(x.meta & 15);
+            a.parent[ob + i] = s_par[i];
+            a.token[ob + i] = s_ids[(d - 1) * k + r];
+            a.depth[ob + i] = d;
+            a.rank[ob + i] = r;
+            a.score[ob + i] = unord32(x.o);
+            int y = i;
+            for (int step = 0; step <= D && y > 0; ++step) {
+#pragma unroll
+                for (int q = 0; q < SLW; ++q) words[q] |= q == (y >> 6) ? 1ull << (y & 63) : 0ull;
+                y = s_par[y];
+            }
+            words[0] |= 1ull;
+        } else {
+            a.parent[ob + i] = -1;
+            a.token[ob + i] = -1;
+            a.depth[ob + i] = -1;
+            a.rank[ob + i] = -1;
+            a.score[ob + i] = -INFINITY;
+        }
+#pragma unroll
+        for (int q = 0; q < SLW; ++q)
+            if (q < W) a.anc[(ob + i) * W + q] = words[q];
+    }
+    if (tid == 0) a.n_nodes[b] = nt + 1;
+}
 }  // namespace presto
 
 namespace presto_host {
@@ -997,6 +1504,41 @@ static Alg2Layout alg2_layout(int D, int k, int branch, int budget) {
     return L;
 }
 
+// Frontier sweeps: candidate table, lambda, T, P (capacity 2 budget), the
+// parent positions, then the lattice.
+struct SweepLayout {
+    int total_no_rho, total_with_rho;
+    int o_lp, o_ids, o_lam, o_t, o_p, o_par, o_cnt, o_np, o_rho;
+};
+
+// slots per lane of T and P for a budget (the kernel's MT and MP)
+static int sweep_mt(int budget) { return budget <= 64 ? 1 : (budget <= 128 ? 2 : 4); }
+static int sweep_mp(int budget) { return 2 * sweep_mt(budget); }
+
+static SweepLayout sweep_layout(int D, int k, int N) {
+    SweepLayout L;
+    const int nb = N - 1;
+    int off = 0;
+    L.o_lp = off; off = align16(off + D * k * 4);
+    L.o_ids = off; off = align16(off + D * k * 4);
+    L.o_lam = off; off = align16(off + D * 4);
+    L.o_t = off; off = align16(off + nb * 32);
+    L.o_p = off; off = align16(off + (nb > 0 ? 2 * nb : 1) * 32);
+    L.o_par = off; off = align16(off + N * 4);
+    L.o_cnt = off; off = align16(off + kSweepWaves * (sweep_mt(nb) + sweep_mp(nb)) * kWave * 4);
+    L.o_np = off; off = align16(off + 2 * 4);
+    L.total_no_rho = off;
+    L.o_rho = off;
+    L.total_with_rho = align16(off + D * k * k * k * 4);
+    return L;
+}
+
+// Budgets the sweep kernel takes: above 256 its slots per lane would not
+// fit; at 32 and below popping one node at a time is faster (a sweep costs
+// about three pops, and a tree of depth 16 needs about 14 sweeps).
+static constexpr int kSweepMinBudget = 33;
+static constexpr int kSweepMaxBudget = 256;
+
 bool tree_build_fits(int D, int k, int branch, int N, int beam_width, bool alg2) {
     if (alg2) return alg2_layout(D, k, branch, N - 1).total_no_rho <= kTreeLdsBudget;
     return tree_layout(D, k, N, beam_width).total_no_rho <= kTreeLdsBudget;
@@ -1057,6 +1599,39 @@ presto_status launch_build_tree(const presto_tree_desc* desc, const int32_t* ids
         return check_launch("tree_alg2_kernel");
     }
     const bool beam = desc->mode == PRESTO_TREE_BEAM;
+    if (!beam && a.budget >= kSweepMinBudget && a.budget <= kSweepMaxBudget) {
+        const SweepLayout L = sweep_layout(a.D, a.k, a.N);
+        a.beam_width = 0;
+        a.o_lp = L.o_lp; a.o_ids = L.o_ids; a.o_lam = L.o_lam; a.o_rho = L.o_rho;
+        a.o_sw_t = L.o_t; a.o_sw_p = L.o_p; a.o_sw_par = L.o_par; a.o_sw_cnt = L.o_cnt; a.o_sw_np = L.o_np;
+        a.rho_in_lds = log_rho != nullptr && L.total_with_rho <= kTreeLdsBudget;
+        const uint64_t k3 = (uint64_t)a.k * a.k * a.k;
+        a.mag_k = (uint32_t)(((1ull << 32) + a.k - 1) / a.k);        // k > 1 only
+        a.mag_k3 = (uint32_t)(((1ull << 32) + k3 - 1) / k3);
+        const int lds = a.rho_in_lds ? L.total_with_rho : L.total_no_rho;
+        const int rho_mode = log_rho == nullptr ? 0 : (a.rho_in_lds ? 1 : 2);
+        presto_status st = PRESTO_OK;
+        auto go = [&](auto kernel) {
+            st = allow_lds(kernel, lds);
+            if (st == PRESTO_OK) kernel<<<desc->batch, kSweepWaves * kWave, lds, stream>>>(a);
+        };
+#define PRESTO_SWEEP3(T, P, K)                                    \
+    if (rho_mode == 0) go(tree_sweep_kernel<T, P, K, 0>);        \
+    else if (rho_mode == 1) go(tree_sweep_kernel<T, P, K, 1>);   \
+    else go(tree_sweep_kernel<T, P, K, 2>)
+#define PRESTO_SWEEP(T, P)                                        \
+    if (a.k <= 4) { PRESTO_SWEEP3(T, P, 4); }                     \
+    else if (a.k <= 8) { PRESTO_SWEEP3(T, P, 8); }                \
+    else { PRESTO_SWEEP3(T, P, 16); }
+        const int mt = sweep_mt(a.budget);
+        if (mt == 1) { PRESTO_SWEEP(1, 2) }
+        else if (mt == 2) { PRESTO_SWEEP(2, 4) }
+        else { PRESTO_SWEEP(4, 8) }
+#undef PRESTO_SWEEP
+#undef PRESTO_SWEEP3
+        if (st != PRESTO_OK) return st;
+        return check_launch("tree_sweep_kernel");
+    }
     a.beam_width = beam ? desc->beam_width : 0;
     const TreeLayout L = tree_layout(a.D, a.k, a.N, a.beam_width);
     a.o_lp = L.o_lp; a.o_ids = L.o_ids; a.o_kord = L.o_kord; a.o_krank = L.o_krank; a.o_rec = L.o_rec;

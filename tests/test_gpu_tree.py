@@ -201,7 +201,8 @@ def test_tree_large_budgets_random(D, k, branch, B, mode):
             _assert_same(g, o)
 
 
-@pytest.mark.parametrize("D,k,B", [(32, 3, 700), (32, 2, 1023), (20, 5, 400)])
+@pytest.mark.parametrize("D,k,B", [(32, 3, 700), (32, 2, 1023), (20, 5, 400), (32, 3, 200), (32, 2, 255),
+                                   (20, 5, 100), (24, 8, 64)])
 @pytest.mark.parametrize("mode", ["best_first", "beam10", "alg2"])
 def test_tree_deep_ties(D, k, B, mode):
     """Whole tied subtrees: lambda = 0 and log q on a coarse grid with equal
