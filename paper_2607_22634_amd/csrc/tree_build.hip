@@ -1003,10 +1003,10 @@ constexpr int kSweepWaves = 4;  // one wave per SIMD
 // One workgroup of four waves per sequence.  Every wave holds all of T and
 // P in registers; the merge's comparisons are split over the waves (each
 // takes every fourth P entry in turn and its partial counts are summed
-// through LDS), the pushes are split into tasks (first children, next
-// siblings) per slot of P, and each task reserves its places in the next P
-// with one LDS atomic.  A sweep has two barriers: after the partial counts,
-// and after the stores and pushes.
+// through LDS); the push candidates are scored before the merge, split into
+// tasks (first children, next siblings) per slot of P, and each task
+// reserves its places in the next P with one LDS atomic.  A sweep has two
+// barriers: after the partial counts, and after the stores and pushes.
 template <int MT, int MP, int KM, int RHO>
 __global__ __launch_bounds__(kSweepWaves * kWave) void tree_sweep_kernel(TreeArgs a) {
     constexpr int NWV = kSweepWaves, NT = NWV * kWave;
@@ -1176,7 +1176,62 @@ __global__ __launch_bounds__(kSweepWaves * kWave) void tree_sweep_kernel(TreeArg
             tr[v] = SwRec{0u, 0u, 0u, 0u, 0u, 0u, 0u};
             if (v * kWave < nt) tr[v] = sw_load(s_t, min(v * kWave + lane, nt - 1));
         }
+        // ord S of lanes without an entry: 0, below every score (ord32 of
+        // -inf is 0x007fffff), so that comparisons of S need no masks
+#pragma unroll
+        for (int u = 0; u < MP; ++u) pr[u].o = pv[u] ? pr[u].o : 0u;
+#pragma unroll
+        for (int v = 0; v < MT; ++v) tr[v].o = tv[v] ? tr[v].o : 0u;
         if (tid == 0) s_np[cur ^ 1] = 0;  // last read a sweep ago, before two barriers
+
+        // Push candidates: task 2u scores the first children of slot u, task
+        // 2u + 1 the next siblings.  With at most two slots per lane they are
+        // scored before the merge (whether an entry enters T is only known
+        // after it) on wave 3 - task mod 4, so that with one slot in use they
+        // overlap the counting of waves 0 and 1; with more slots, holding them
+        // across the merge would spill, and wave task mod 4 scores them after.
+        constexpr bool EARLY = MP <= 2;
+        auto owner = [&](int t) { return EARLY ? NWV - 1 - t % NWV : t % NWV; };
+        auto score = [&](int u, bool first, SwRec& c, bool& ok) {
+            const SwRec& w = pr[u];
+            const int d = (int)(w.meta >> 4) & 63, r = (int)(w.meta & 15);
+            const int rp = (int)(w.meta >> 10) & 15, rg = (int)(w.meta >> 14) & 15;
+            if (first) {
+                // first child (depth d + 1, drafter row d); rows clamped for
+                // lanes without a valid entry
+                const int drow = min(max(d, 0), D - 1);
+                int cr;
+                float cS;
+                const uint32_t co =
+                    child(drow, d >= 2 ? rp : 0, d >= 1 ? r : 0, unord32(w.o), true, 0u, 0, cr, cS);
+                c = SwRec{co, w.k0, w.k1, w.k2, w.k3, w.o,
+                          (uint32_t)cr | ((uint32_t)(d + 1) << 4) | ((uint32_t)r << 10) | ((uint32_t)rp << 14)};
+                c = with_digit(c, min(d + 1, D), cr);
+                ok = pv[u] & (d < D) & (co != 0u);
+            } else {
+                // next sibling (depth d, drafter row d - 1, the parent's context)
+                const int srow = min(max(d - 1, 0), D - 1);
+                int sr;
+                float sS;
+                const uint32_t so = child(srow, d - 1 >= 2 ? rg : 0, d - 1 >= 1 ? rp : 0, unord32(w.po), false,
+                                          w.o, r, sr, sS);
+                c = SwRec{so, w.k0, w.k1, w.k2, w.k3, w.po,
+                          (uint32_t)sr | ((uint32_t)d << 4) | ((uint32_t)rp << 10) | ((uint32_t)rg << 14)};
+                c = with_digit(c, max(d, 1), sr);
+                ok = pv[u] & (so != 0u);
+            }
+        };
+        constexpr int ME = EARLY ? MP : 1;
+        SwRec ca[ME], cb[ME];
+        bool oka[ME], okb[ME];
+#pragma unroll
+        for (int u = 0; u < ME; ++u) {
+            oka[u] = okb[u] = false;
+            ca[u] = cb[u] = SwRec{0u, 0u, 0u, 0u, 0u, 0u, 0u};
+            if (!EARLY || u * kWave >= np) continue;
+            if (owner(2 * u) == wv) score(u, true, ca[u], oka[u]);
+            if (owner(2 * u + 1) == wv) score(u, false, cb[u], okb[u]);
+        }
 
         // merged places: a T entry moves down by the P entries before it; a P
         // entry lands after the T and P entries before it.  Each P entry in
@@ -1189,41 +1244,56 @@ __global__ __launch_bounds__(kSweepWaves * kWave) void tree_sweep_kernel(TreeArg
         for (int v = 0; v < MT; ++v) tc[v] = 0;
 #pragma unroll
         for (int u = 0; u < MP; ++u) pc[u] = 0;
+        // Counts for the P entries at lanes l0 and l1 (l1 < 0: none) of slot
+        // u, written so that the two entries' instructions interleave.  Lane
+        // masks straight from the compares: T entries before y, T entries y
+        // precedes, P entries y precedes; equal S (rare) falls back to keys.
         auto count = [&](auto at, auto ap) {
             constexpr int AT = decltype(at)::value, AP = decltype(ap)::value;
+            auto tie_fix = [&](int u, int l, int& before) {
+                const SwRec y = sw_readlane(pr[u], l);
+                const uint32_t yo = y.o;
+#pragma unroll
+                for (int v = 0; v < AT; ++v) {
+                    const bool e = tr[v].o == yo;
+                    const bool g = sw_key_less(tr[v], y);
+                    before += __popcll(__ballot(e & g));
+                    tc[v] += (e & !g) ? 1 : 0;
+                }
+#pragma unroll
+                for (int q = 0; q < AP; ++q) {
+                    const bool e = (pr[q].o == yo) & !((q == u) & (lane == l));
+                    pc[q] += (e & sw_key_less(y, pr[q])) ? 1 : 0;
+                }
+            };
 #pragma unroll
             for (int u = 0; u < AP; ++u) {
                 const int cnt = min(kWave, np - u * kWave);
-                for (int l = wv; l < cnt; l += NWV) {
-                    const uint32_t yo = (uint32_t)__builtin_amdgcn_readlane((int)pr[u].o, l);
-                    bool teq[AT], peq[AP];
-                    bool eq_any = false;
-                    int before = 0;
+                for (int l0 = wv; l0 < cnt; l0 += 2 * NWV) {
+                    const int l1 = l0 + NWV < cnt ? l0 + NWV : l0;
+                    const bool two = l1 != l0;
+                    const uint32_t y0 = (uint32_t)__builtin_amdgcn_readlane((int)pr[u].o, l0);
+                    const uint32_t y1 = (uint32_t)__builtin_amdgcn_readlane((int)pr[u].o, l1);
+                    int b0 = 0, b1 = 0;
+                    uint64_t e0 = 0ull, e1 = 0ull;
 #pragma unroll
                     for (int v = 0; v < AT; ++v) {
-                        before += __popcll(__ballot(tv[v] & (tr[v].o > yo)));
-                        tc[v] += (tv[v] & (tr[v].o < yo)) ? 1 : 0;
-                        teq[v] = tv[v] & (tr[v].o == yo);
-                        eq_any |= teq[v];
+                        b0 += __popcll(__builtin_amdgcn_uicmp(tr[v].o, y0, 34));  // T before y: greater ord S
+                        b1 += __popcll(__builtin_amdgcn_uicmp(tr[v].o, y1, 34));
+                        tc[v] += (tr[v].o < y0 ? 1 : 0) + ((two & (tr[v].o < y1)) ? 1 : 0);
+                        e0 |= __builtin_amdgcn_uicmp(tr[v].o, y0, 32);
+                        e1 |= __builtin_amdgcn_uicmp(tr[v].o, y1, 32);
                     }
 #pragma unroll
                     for (int q = 0; q < AP; ++q) {
-                        pc[q] += (pv[q] & (pr[q].o < yo)) ? 1 : 0;
-                        peq[q] = pv[q] & (pr[q].o == yo) & !((q == u) & (lane == l));
-                        eq_any |= peq[q];
+                        pc[q] += (pr[q].o < y0 ? 1 : 0) + ((two & (pr[q].o < y1)) ? 1 : 0);
+                        const uint64_t self0 = q == u ? 1ull << l0 : 0ull, self1 = q == u ? 1ull << l1 : 0ull;
+                        e0 |= __builtin_amdgcn_uicmp(pr[q].o, y0, 32) & ~self0;
+                        e1 |= __builtin_amdgcn_uicmp(pr[q].o, y1, 32) & ~self1;
                     }
-                    if (__ballot(eq_any) != 0ull) {
-                        const SwRec y = sw_readlane(pr[u], l);
-#pragma unroll
-                        for (int v = 0; v < AT; ++v) {
-                            const bool g = sw_key_less(tr[v], y);
-                            before += __popcll(__ballot(teq[v] & g));
-                            tc[v] += (teq[v] & !g) ? 1 : 0;
-                        }
-#pragma unroll
-                        for (int q = 0; q < AP; ++q) pc[q] += (peq[q] & sw_key_less(y, pr[q])) ? 1 : 0;
-                    }
-                    pc[u] += lane == l ? before : 0;
+                    if (e0 != 0ull) tie_fix(u, l0, b0);
+                    if (two && e1 != 0ull) tie_fix(u, l1, b1);
+                    pc[u] += (lane == l0 ? b0 : 0) + ((two & (lane == l1)) ? b1 : 0);
                 }
             }
         };
@@ -1297,9 +1367,9 @@ __global__ __launch_bounds__(kSweepWaves * kWave) void tree_sweep_kernel(TreeArg
             }
         }
 
-        // pushes of the P entries that entered T: task 2u (first children of
-        // slot u) and task 2u + 1 (next siblings) go to wave task mod 4; a
-        // task takes its places in the next P with one atomic
+        // pushes of the P entries that entered T, while T is not full or when
+        // they precede its last entry; a task takes its places in the next P
+        // with one atomic
         auto push = [&](bool h, const SwRec& c) {
             const uint64_t m = __ballot(h);
             if (m == 0ull) return;
@@ -1312,34 +1382,18 @@ __global__ __launch_bounds__(kSweepWaves * kWave) void tree_sweep_kernel(TreeArg
 #pragma unroll
         for (int u = 0; u < MP; ++u) {
             if (u * kWave >= np) break;
-            const SwRec& w = pr[u];
             const bool in = pv[u] & (pc[u] < NB);
-            const int d = (int)(w.meta >> 4) & 63, r = (int)(w.meta & 15);
-            const int rp = (int)(w.meta >> 10) & 15, rg = (int)(w.meta >> 14) & 15;
-            if ((2 * u) % NWV == wv) {
-                // first child (depth d + 1, drafter row d); rows clamped for
-                // lanes without a valid entry
-                const int drow = min(max(d, 0), D - 1);
-                int cr;
-                float cS;
-                const uint32_t co =
-                    child(drow, d >= 2 ? rp : 0, d >= 1 ? r : 0, unord32(w.o), true, 0u, 0, cr, cS);
-                SwRec ca{co, w.k0, w.k1, w.k2, w.k3, w.o,
-                         (uint32_t)cr | ((uint32_t)(d + 1) << 4) | ((uint32_t)r << 10) | ((uint32_t)rp << 14)};
-                ca = with_digit(ca, min(d + 1, D), cr);
-                push(in & (d < D) & (co != 0u) & (!full | sw_before(ca, last)), ca);
+            if (owner(2 * u) == wv) {
+                SwRec c = ca[EARLY ? u : 0];
+                bool ok = oka[EARLY ? u : 0];
+                if (!EARLY) score(u, true, c, ok);
+                push(ok & in & (!full | sw_before(c, last)), c);
             }
-            if ((2 * u + 1) % NWV == wv) {
-                // next sibling (depth d, drafter row d - 1, the parent's context)
-                const int srow = min(max(d - 1, 0), D - 1);
-                int sr;
-                float sS;
-                const uint32_t so = child(srow, d - 1 >= 2 ? rg : 0, d - 1 >= 1 ? rp : 0, unord32(w.po), false,
-                                          w.o, r, sr, sS);
-                SwRec cb{so, w.k0, w.k1, w.k2, w.k3, w.po,
-                         (uint32_t)sr | ((uint32_t)d << 4) | ((uint32_t)rp << 10) | ((uint32_t)rg << 14)};
-                cb = with_digit(cb, max(d, 1), sr);
-                push(in & (so != 0u) & (!full | sw_before(cb, last)), cb);
+            if (owner(2 * u + 1) == wv) {
+                SwRec c = cb[EARLY ? u : 0];
+                bool ok = okb[EARLY ? u : 0];
+                if (!EARLY) score(u, false, c, ok);
+                push(ok & in & (!full | sw_before(c, last)), c);
             }
         }
         nt = nt_new;
