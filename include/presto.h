@@ -217,7 +217,9 @@ presto_status presto_ngram_gather(const void *table, int64_t capacity, float flo
  * PRESTO_TREE_BEST_FIRST (Sec. 4.2, Alg. 2 with commit on pop): the tree
  *   is exactly the `budget` best non-root prefixes of the candidate tree
  *   (the closed form of Sec. 4.2 via Eq. 3), or the whole candidate tree
- *   when it has fewer nodes.
+ *   when it has fewer nodes.  This relies on the input bounds below
+ *   (logprob <= 0, log_rho <= 0, lambda >= 0: every s <= 0, so S never
+ *   increases along a path); outside them the tree is unspecified.
  * PRESTO_TREE_BEST_FIRST_ALG2: Alg. 2 as printed: every pop adds all its
  *   children to T; stop once T holds `budget` non-root nodes; keep TopB(T).
  * PRESTO_TREE_BEAM (Sec. 4.2, Alg. 1, beam search with global retention):
