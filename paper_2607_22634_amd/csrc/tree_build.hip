@@ -954,7 +954,8 @@ __global__ __launch_bounds__(kWave) void tree_alg2_kernel(TreeArgs a) {
 
 // A record: ord(S), rank-path key (k0 most significant), ord(S) of the
 // parent, and rank | depth << 4 | parent's rank << 10 | grandparent's rank
-// << 14.  In LDS two 16-byte words: (o, k0, k1, k2), (k3, po, meta, 0).
+// << 14 | chain end << 18.  In LDS two 16-byte words: (o, k0, k1, k2),
+// (k3, po, meta, 0).
 struct SwRec {
     uint32_t o, k0, k1, k2, k3, po, meta;
 };
@@ -996,9 +997,17 @@ __device__ __forceinline__ int lanes_below(uint64_t m) {
 }
 
 constexpr int kSweepWaves = 4;  // one wave per SIMD
+// An entry that enters T pushes its next sibling and, when it ends a chain,
+// the chain of its first child, that child's first child, ... CL levels
+// deep; only the last of a chain pushes the next chain (every prefix is
+// still pushed once: a first child by its parent's chain).  A chain advances
+// a path of first children CL levels per sweep: with CL = 2 the sweeps at
+// depth 16 drop from about 15 to 8 at budget 64.
+constexpr uint32_t kChainEnd = 1u << 18;  // record meta: this entry pushes the next chain
 
 // MT: slots per lane of T (budget <= 64 MT), MP: slots per lane of P
-// (2 budget <= 64 MP), KM: k <= KM, RHO as in tree_build_kernel.
+// ((CL + 1) budget <= 64 MP), KM: k <= KM, RHO as in tree_build_kernel, CL:
+// chain length.
 //
 // One workgroup of four waves per sequence.  Every wave holds all of T and
 // P in registers; the merge's comparisons are split over the waves (each
@@ -1007,7 +1016,7 @@ constexpr int kSweepWaves = 4;  // one wave per SIMD
 // tasks (first children, next siblings) per slot of P, and each task
 // reserves its places in the next P with one LDS atomic.  A sweep has two
 // barriers: after the partial counts, and after the stores and pushes.
-template <int MT, int MP, int KM, int RHO>
+template <int MT, int MP, int KM, int RHO, int CL>
 __global__ __launch_bounds__(kSweepWaves * kWave) void tree_sweep_kernel(TreeArgs a) {
     constexpr int NWV = kSweepWaves, NT = NWV * kWave;
     extern __shared__ __align__(16) char lds[];
@@ -1016,7 +1025,7 @@ __global__ __launch_bounds__(kSweepWaves * kWave) void tree_sweep_kernel(TreeArg
     const int b = blockIdx.x;
     const int D = a.D, k = a.k, N = a.N, W = a.W, wbits = a.wbits, per_word = a.per_word;
     const int NB = N - 1;             // non-root nodes of a full tree
-    const int cap_p = max(2 * NB, 1);  // P's capacity
+    const int cap_p = (CL + 1) * NB;  // P's capacity
     float* s_lp = reinterpret_cast<float*>(lds + a.o_lp);
     int32_t* s_ids = reinterpret_cast<int32_t*>(lds + a.o_ids);
     float* s_lam = reinterpret_cast<float*>(lds + a.o_lam);
@@ -1117,43 +1126,66 @@ __global__ __launch_bounds__(kSweepWaves * kWave) void tree_sweep_kernel(TreeArg
                 for (int r = 0; r < KM; ++r) s[r] = sc[r < k ? r : k - 1];
             }
         }
-        uint32_t bo = 0u;
-        int br = 0;
-        float bS = 0.f;
+        // candidates kept by the branch filter (a mask), then one key per
+        // candidate, (ord S, 255 - rank), and a maximum over them as a tree
+        uint32_t selm = k >= 32 ? ~0u : (1u << k) - 1u;
+        if (a.branch < k) {
+            selm = 0u;
 #pragma unroll
-        for (int r = 0; r < KM; ++r) {
-            if (r < k) {
-                bool sel = true;
-                if (a.branch < k) {
-                    int c = 0;
+            for (int r = 0; r < KM; ++r) {
+                int c = 0;
 #pragma unroll
-                    for (int j = 0; j < KM; ++j)
-                        c += ((j < k) & ((s[j] > s[r]) | ((s[j] == s[r]) & (j < r)))) ? 1 : 0;
-                    sel = c < a.branch;
-                }
-                const float Sc = Sn + s[r];
-                const uint32_t oc = ord32(Sc);
-                const bool after = first | (oc < ao) | ((oc == ao) & (r > ar));
-                const bool take = sel & after & (oc > bo);
-                bo = take ? oc : bo;
-                br = take ? r : br;
-                bS = take ? Sc : bS;
+                for (int j = 0; j < KM; ++j)
+                    c += ((j < k) & ((s[j] > s[r]) | ((s[j] == s[r]) & (j < r)))) ? 1 : 0;
+                selm |= ((r < k) & (c < a.branch)) ? 1u << r : 0u;
             }
         }
-        r_out = br;
-        S_out = bS;
+        uint64_t key[KM];
+#pragma unroll
+        for (int r = 0; r < KM; ++r) {
+            const float Sc = Sn + s[r];
+            const uint32_t oc = ord32(Sc);
+            const bool after = first | (oc < ao) | ((oc == ao) & (r > ar));
+            key[r] = (((selm >> r) & 1u) & after) ? ((uint64_t)oc << 8) | (uint64_t)(255 - r) : 0ull;
+        }
+#pragma unroll
+        for (int w = 1; w < KM; w *= 2)
+#pragma unroll
+            for (int r = 0; r + w < KM; r += 2 * w) key[r] = key[r + w] > key[r] ? key[r + w] : key[r];
+        const uint32_t bo = (uint32_t)(key[0] >> 8);
+        r_out = 255 - (int)(key[0] & 255u);
+        S_out = unord32(bo);  // S is never -0.0 or NaN here, so this is the sum itself
         return bo;
     };
 
-    // P starts as the root's first child
+    // the first child of a record w (chain end flag `end`), or of the root
+    auto first_child = [&](const SwRec& w, bool root, bool end, SwRec& c) -> bool {
+        const int d = root ? 0 : (int)(w.meta >> 4) & 63, r = (int)(w.meta & 15);
+        const int rp = (int)(w.meta >> 10) & 15;
+        const int drow = min(max(d, 0), D - 1);  // clamped for lanes without a valid entry
+        int cr;
+        float cS;
+        const uint32_t co = child(drow, d >= 2 ? rp : 0, d >= 1 ? r : 0, root ? 0.f : unord32(w.o), true, 0u,
+                                  0, cr, cS);
+        c = SwRec{co, root ? 0u : w.k0, root ? 0u : w.k1, root ? 0u : w.k2, root ? 0u : w.k3,
+                  root ? ord32(0.f) : w.o,
+                  (uint32_t)cr | ((uint32_t)(d + 1) << 4) | ((uint32_t)r << 10) | ((uint32_t)rp << 14) |
+                      (end ? kChainEnd : 0u)};
+        c = with_digit(c, min(d + 1, D), cr);
+        return (d < D) & (co != 0u);
+    };
+
+    // P starts as the root's first chain
     if (tid == 0) {
-        int r;
-        float Sc;
-        const uint32_t oc = child(0, 0, 0, 0.f, true, 0u, 0, r, Sc);
-        SwRec c{oc, 0u, 0u, 0u, 0u, ord32(0.f), (uint32_t)r | (1u << 4)};
-        c = with_digit(c, 1, r);
-        sw_store(s_p, 0, c);
-        s_np[0] = oc != 0u ? 1 : 0;
+        SwRec par{0u, 0u, 0u, 0u, 0u, 0u, 0u};
+        int n = 0;
+        for (int i = 0; i < CL; ++i) {
+            SwRec c;
+            if (!first_child(par, i == 0, i == CL - 1, c)) break;
+            sw_store(s_p, n++, c);
+            par = c;
+        }
+        s_np[0] = n;
         s_np[1] = 0;
     }
     __syncthreads();
@@ -1184,53 +1216,49 @@ __global__ __launch_bounds__(kSweepWaves * kWave) void tree_sweep_kernel(TreeArg
         for (int v = 0; v < MT; ++v) tr[v].o = tv[v] ? tr[v].o : 0u;
         if (tid == 0) s_np[cur ^ 1] = 0;  // last read a sweep ago, before two barriers
 
-        // Push candidates: task 2u scores the first children of slot u, task
-        // 2u + 1 the next siblings.  With at most two slots per lane they are
-        // scored before the merge (whether an entry enters T is only known
-        // after it) on wave 3 - task mod 4, so that with one slot in use they
-        // overlap the counting of waves 0 and 1; with more slots, holding them
-        // across the merge would spill, and wave task mod 4 scores them after.
-        constexpr bool EARLY = MP <= 2;
-        auto owner = [&](int t) { return EARLY ? NWV - 1 - t % NWV : t % NWV; };
-        auto score = [&](int u, bool first, SwRec& c, bool& ok) {
-            const SwRec& w = pr[u];
-            const int d = (int)(w.meta >> 4) & 63, r = (int)(w.meta & 15);
-            const int rp = (int)(w.meta >> 10) & 15, rg = (int)(w.meta >> 14) & 15;
-            if (first) {
-                // first child (depth d + 1, drafter row d); rows clamped for
-                // lanes without a valid entry
-                const int drow = min(max(d, 0), D - 1);
-                int cr;
-                float cS;
-                const uint32_t co =
-                    child(drow, d >= 2 ? rp : 0, d >= 1 ? r : 0, unord32(w.o), true, 0u, 0, cr, cS);
-                c = SwRec{co, w.k0, w.k1, w.k2, w.k3, w.o,
-                          (uint32_t)cr | ((uint32_t)(d + 1) << 4) | ((uint32_t)r << 10) | ((uint32_t)rp << 14)};
-                c = with_digit(c, min(d + 1, D), cr);
-                ok = pv[u] & (d < D) & (co != 0u);
-            } else {
-                // next sibling (depth d, drafter row d - 1, the parent's context)
-                const int srow = min(max(d - 1, 0), D - 1);
-                int sr;
-                float sS;
-                const uint32_t so = child(srow, d - 1 >= 2 ? rg : 0, d - 1 >= 1 ? rp : 0, unord32(w.po), false,
-                                          w.o, r, sr, sS);
-                c = SwRec{so, w.k0, w.k1, w.k2, w.k3, w.po,
-                          (uint32_t)sr | ((uint32_t)d << 4) | ((uint32_t)rp << 10) | ((uint32_t)rg << 14)};
-                c = with_digit(c, max(d, 1), sr);
-                ok = pv[u] & (so != 0u);
+        // Push candidates: task 2u scores the first-child chains of slot u
+        // (of the entries that end a chain), task 2u + 1 the next siblings, on
+        // wave 3 - task mod 4.  With at most four slots per lane, slot 0's two
+        // tasks are scored before the merge (whether an entry enters T is only
+        // known after it), so that with one slot in use they overlap the
+        // counting of waves 0 and 1; every other task is scored after it.
+        constexpr bool EARLY = MP <= 4;
+        auto owner = [&](int t) { return NWV - 1 - t % NWV; };
+        auto score_chain = [&](const SwRec& w, bool valid, SwRec (&c)[CL], bool (&ok)[CL])
+                               __attribute__((always_inline)) {
+            SwRec par = w;
+            bool okp = valid & ((par.meta & kChainEnd) != 0u);
+#pragma unroll
+            for (int i = 0; i < CL; ++i) {
+                ok[i] = okp & first_child(par, false, i == CL - 1, c[i]);
+                par = c[i];
+                okp = ok[i];
             }
         };
-        constexpr int ME = EARLY ? MP : 1;
-        SwRec ca[ME], cb[ME];
-        bool oka[ME], okb[ME];
+        auto score_sibling = [&](const SwRec& w, bool valid, SwRec& c, bool& ok) __attribute__((always_inline)) {
+            // next sibling (depth d, drafter row d - 1, the parent's context)
+            const int d = (int)(w.meta >> 4) & 63, r = (int)(w.meta & 15);
+            const int rp = (int)(w.meta >> 10) & 15, rg = (int)(w.meta >> 14) & 15;
+            const int srow = min(max(d - 1, 0), D - 1);
+            int sr;
+            float sS;
+            const uint32_t so =
+                child(srow, d - 1 >= 2 ? rg : 0, d - 1 >= 1 ? rp : 0, unord32(w.po), false, w.o, r, sr, sS);
+            c = SwRec{so, w.k0, w.k1, w.k2, w.k3, w.po,
+                      (uint32_t)sr | ((uint32_t)d << 4) | ((uint32_t)rp << 10) | ((uint32_t)rg << 14) | kChainEnd};
+            c = with_digit(c, max(d, 1), sr);
+            ok = valid & (so != 0u);
+        };
+        SwRec ea[CL], eb = SwRec{0u, 0u, 0u, 0u, 0u, 0u, 0u};
+        bool oea[CL], oeb = false;
 #pragma unroll
-        for (int u = 0; u < ME; ++u) {
-            oka[u] = okb[u] = false;
-            ca[u] = cb[u] = SwRec{0u, 0u, 0u, 0u, 0u, 0u, 0u};
-            if (!EARLY || u * kWave >= np) continue;
-            if (owner(2 * u) == wv) score(u, true, ca[u], oka[u]);
-            if (owner(2 * u + 1) == wv) score(u, false, cb[u], okb[u]);
+        for (int i = 0; i < CL; ++i) {
+            oea[i] = false;
+            ea[i] = SwRec{0u, 0u, 0u, 0u, 0u, 0u, 0u};
+        }
+        if (EARLY) {
+            if (owner(0) == wv) score_chain(pr[0], pv[0], ea, oea);
+            if (owner(1) == wv) score_sibling(pr[0], pv[0], eb, oeb);
         }
 
         // merged places: a T entry moves down by the P entries before it; a P
@@ -1248,10 +1276,9 @@ __global__ __launch_bounds__(kSweepWaves * kWave) void tree_sweep_kernel(TreeArg
         // u, written so that the two entries' instructions interleave.  Lane
         // masks straight from the compares: T entries before y, T entries y
         // precedes, P entries y precedes; equal S (rare) falls back to keys.
-        auto count = [&](auto at, auto ap) {
+        auto count = [&](auto at, auto ap) __attribute__((always_inline)) {
             constexpr int AT = decltype(at)::value, AP = decltype(ap)::value;
-            auto tie_fix = [&](int u, int l, int& before) {
-                const SwRec y = sw_readlane(pr[u], l);
+            auto tie_fix = [&](const SwRec& y, int u, int l, int& before) __attribute__((always_inline)) {
                 const uint32_t yo = y.o;
 #pragma unroll
                 for (int v = 0; v < AT; ++v) {
@@ -1291,13 +1318,13 @@ __global__ __launch_bounds__(kSweepWaves * kWave) void tree_sweep_kernel(TreeArg
                         e0 |= __builtin_amdgcn_uicmp(pr[q].o, y0, 32) & ~self0;
                         e1 |= __builtin_amdgcn_uicmp(pr[q].o, y1, 32) & ~self1;
                     }
-                    if (e0 != 0ull) tie_fix(u, l0, b0);
-                    if (two && e1 != 0ull) tie_fix(u, l1, b1);
+                    if (e0 != 0ull) tie_fix(sw_readlane(pr[u], l0), u, l0, b0);
+                    if (two && e1 != 0ull) tie_fix(sw_readlane(pr[u], l1), u, l1, b1);
                     pc[u] += (lane == l0 ? b0 : 0) + ((two & (lane == l1)) ? b1 : 0);
                 }
             }
         };
-        auto count_p = [&](auto at) {
+        auto count_p = [&](auto at) __attribute__((always_inline)) {
             if (np <= kWave) count(at, SlotCount<1>{});
             else if (MP <= 2 || np <= 2 * kWave) count(at, SlotCount<(MP < 2 ? MP : 2)>{});
             else if (MP <= 4 || np <= 4 * kWave) count(at, SlotCount<(MP < 4 ? MP : 4)>{});
@@ -1370,30 +1397,53 @@ __global__ __launch_bounds__(kSweepWaves * kWave) void tree_sweep_kernel(TreeArg
         // pushes of the P entries that entered T, while T is not full or when
         // they precede its last entry; a task takes its places in the next P
         // with one atomic
-        auto push = [&](bool h, const SwRec& c) {
-            const uint64_t m = __ballot(h);
-            if (m == 0ull) return;
+        auto push = [&](auto& h, auto& c) __attribute__((always_inline)) {
+            constexpr int n = sizeof(h) / sizeof(h[0]);
+            uint64_t m[n];
+            int total = 0;
+#pragma unroll
+            for (int i = 0; i < n; ++i) {
+                m[i] = __ballot(h[i]);
+                total += __popcll(m[i]);
+            }
+            if (total == 0) return;
             int base = 0;
-            if (lane == 0) base = atomicAdd(&s_np[cur ^ 1], __popcll(m));
+            if (lane == 0) base = atomicAdd(&s_np[cur ^ 1], total);
             base = __builtin_amdgcn_readlane(base, 0);
-            const int at = base + lanes_below(m);
-            if (h & (at < cap_p)) sw_store(s_p, at, c);
+#pragma unroll
+            for (int i = 0; i < n; ++i) {
+                const int at = base + lanes_below(m[i]);
+                if (h[i] & (at < cap_p)) sw_store(s_p, at, c[i]);
+                base += __popcll(m[i]);
+            }
         };
 #pragma unroll
         for (int u = 0; u < MP; ++u) {
             if (u * kWave >= np) break;
             const bool in = pv[u] & (pc[u] < NB);
             if (owner(2 * u) == wv) {
-                SwRec c = ca[EARLY ? u : 0];
-                bool ok = oka[EARLY ? u : 0];
-                if (!EARLY) score(u, true, c, ok);
-                push(ok & in & (!full | sw_before(c, last)), c);
+                SwRec c[CL];
+                bool ok[CL];
+                if (EARLY && u == 0) {
+#pragma unroll
+                    for (int i = 0; i < CL; ++i) {
+                        c[i] = ea[i];
+                        ok[i] = oea[i];
+                    }
+                } else {
+                    score_chain(pr[u], pv[u], c, ok);
+                }
+                bool h[CL];
+#pragma unroll
+                for (int i = 0; i < CL; ++i) h[i] = ok[i] & in & (!full | sw_before(c[i], last));
+                push(h, c);
             }
             if (owner(2 * u + 1) == wv) {
-                SwRec c = cb[EARLY ? u : 0];
-                bool ok = okb[EARLY ? u : 0];
-                if (!EARLY) score(u, false, c, ok);
-                push(ok & in & (!full | sw_before(c, last)), c);
+                SwRec c[1] = {eb};
+                bool ok = oeb;
+                if (!(EARLY && u == 0)) score_sibling(pr[u], pv[u], c[0], ok);
+                bool h[1] = {(bool)(ok & in & (!full | sw_before(c[0], last)))};
+                push(h, c);
             }
         }
         nt = nt_new;
@@ -1567,7 +1617,10 @@ struct SweepLayout {
 
 // slots per lane of T and P for a budget (the kernel's MT and MP)
 static int sweep_mt(int budget) { return budget <= 64 ? 1 : (budget <= 128 ? 2 : 4); }
-static int sweep_mp(int budget) { return 2 * sweep_mt(budget); }
+// chains of two first children at budgets <= 64 (about half the sweeps at depth 16); at larger
+// budgets the trees are wider and chains added entries without removing sweeps
+static int sweep_chain(int budget) { return sweep_mt(budget) == 1 ? 2 : 1; }
+static int sweep_mp(int budget) { return (sweep_chain(budget) + 1) * sweep_mt(budget); }
 
 static SweepLayout sweep_layout(int D, int k, int N) {
     SweepLayout L;
@@ -1577,7 +1630,7 @@ static SweepLayout sweep_layout(int D, int k, int N) {
     L.o_ids = off; off = align16(off + D * k * 4);
     L.o_lam = off; off = align16(off + D * 4);
     L.o_t = off; off = align16(off + nb * 32);
-    L.o_p = off; off = align16(off + (nb > 0 ? 2 * nb : 1) * 32);
+    L.o_p = off; off = align16(off + (sweep_chain(nb) + 1) * nb * 32);
     L.o_par = off; off = align16(off + N * 4);
     L.o_cnt = off; off = align16(off + kSweepWaves * (sweep_mt(nb) + sweep_mp(nb)) * kWave * 4);
     L.o_np = off; off = align16(off + 2 * 4);
@@ -1669,18 +1722,18 @@ presto_status launch_build_tree(const presto_tree_desc* desc, const int32_t* ids
             st = allow_lds(kernel, lds);
             if (st == PRESTO_OK) kernel<<<desc->batch, kSweepWaves * kWave, lds, stream>>>(a);
         };
-#define PRESTO_SWEEP3(T, P, K)                                    \
-    if (rho_mode == 0) go(tree_sweep_kernel<T, P, K, 0>);        \
-    else if (rho_mode == 1) go(tree_sweep_kernel<T, P, K, 1>);   \
-    else go(tree_sweep_kernel<T, P, K, 2>)
-#define PRESTO_SWEEP(T, P)                                        \
-    if (a.k <= 4) { PRESTO_SWEEP3(T, P, 4); }                     \
-    else if (a.k <= 8) { PRESTO_SWEEP3(T, P, 8); }                \
-    else { PRESTO_SWEEP3(T, P, 16); }
+#define PRESTO_SWEEP3(T, P, K, C)                                    \
+    if (rho_mode == 0) go(tree_sweep_kernel<T, P, K, 0, C>);        \
+    else if (rho_mode == 1) go(tree_sweep_kernel<T, P, K, 1, C>);   \
+    else go(tree_sweep_kernel<T, P, K, 2, C>)
+#define PRESTO_SWEEP(T, P, C)                                        \
+    if (a.k <= 4) { PRESTO_SWEEP3(T, P, 4, C); }                     \
+    else if (a.k <= 8) { PRESTO_SWEEP3(T, P, 8, C); }                \
+    else { PRESTO_SWEEP3(T, P, 16, C); }
         const int mt = sweep_mt(a.budget);
-        if (mt == 1) { PRESTO_SWEEP(1, 2) }
-        else if (mt == 2) { PRESTO_SWEEP(2, 4) }
-        else { PRESTO_SWEEP(4, 8) }
+        if (mt == 1) { PRESTO_SWEEP(1, 3, 2) }
+        else if (mt == 2) { PRESTO_SWEEP(2, 4, 1) }
+        else { PRESTO_SWEEP(4, 8, 1) }
 #undef PRESTO_SWEEP
 #undef PRESTO_SWEEP3
         if (st != PRESTO_OK) return st;
