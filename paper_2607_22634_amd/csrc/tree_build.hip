@@ -1001,8 +1001,8 @@ constexpr int kSweepWaves = 4;  // one wave per SIMD
 // the chain of its first child, that child's first child, ... CL levels
 // deep; only the last of a chain pushes the next chain (every prefix is
 // still pushed once: a first child by its parent's chain).  A chain advances
-// a path of first children CL levels per sweep: with CL = 2 the sweeps at
-// depth 16 drop from about 15 to 8 at budget 64.
+// a path of first children CL levels per sweep: at budget 64 and depth 16
+// the sweeps drop from about 15 to 8 with CL = 2 and to 6 with CL = 3.
 constexpr uint32_t kChainEnd = 1u << 18;  // record meta: this entry pushes the next chain
 
 // MT: slots per lane of T (budget <= 64 MT), MP: slots per lane of P
@@ -1617,9 +1617,10 @@ struct SweepLayout {
 
 // slots per lane of T and P for a budget (the kernel's MT and MP)
 static int sweep_mt(int budget) { return budget <= 64 ? 1 : (budget <= 128 ? 2 : 4); }
-// chains of two first children at budgets <= 64 (about half the sweeps at depth 16); at larger
-// budgets the trees are wider and chains added entries without removing sweeps
-static int sweep_chain(int budget) { return sweep_mt(budget) == 1 ? 2 : 1; }
+// chains of three first children at budgets <= 64 (8 -> 6 sweeps at depth 16 against chains of
+// two, 15 with none); at larger budgets the trees are wider and chains added entries without
+// removing sweeps
+static int sweep_chain(int budget) { return sweep_mt(budget) == 1 ? 3 : 1; }
 static int sweep_mp(int budget) { return (sweep_chain(budget) + 1) * sweep_mt(budget); }
 
 static SweepLayout sweep_layout(int D, int k, int N) {
@@ -1731,7 +1732,7 @@ presto_status launch_build_tree(const presto_tree_desc* desc, const int32_t* ids
     else if (a.k <= 8) { PRESTO_SWEEP3(T, P, 8, C); }                \
     else { PRESTO_SWEEP3(T, P, 16, C); }
         const int mt = sweep_mt(a.budget);
-        if (mt == 1) { PRESTO_SWEEP(1, 3, 2) }
+        if (mt == 1) { PRESTO_SWEEP(1, 4, 3) }
         else if (mt == 2) { PRESTO_SWEEP(2, 4, 1) }
         else { PRESTO_SWEEP(4, 8, 1) }
 #undef PRESTO_SWEEP
