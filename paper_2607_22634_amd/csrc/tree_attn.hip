@@ -73,7 +73,7 @@ struct AttnArgs {
     uint16_t* part_o;
     float2* part_ml;
     int32_t batch, n_max, hq, hkv, G, W;
-    int32_t row_tiles, splits, split_len;
+    int32_t row_tiles, rows_per_tile, splits, split_len;  // rows_per_tile: a multiple of 32, <= 256
     int32_t n_tasks, n_blocks;
     int32_t compact;  // tasks dealt over the (sequence, split) pairs that hold keys
     float scale_log2;  // scale * log2(e)
@@ -236,12 +236,13 @@ __global__ __launch_bounds__(kAttnWaves * kWave) void tree_attn_bf16_kernel(Attn
     // waves A-1 .. kAttnWaves-1, each taking every nshare-th key block, and
     // their states are combined at the end: a 4-row tail block then costs a
     // SIMD a fraction of a full one.
-    const int tile_live = min(max(live_rows - rt * ROWS, 0), ROWS);
+    const int RT = a.rows_per_tile;
+    const int tile_live = min(max(live_rows - rt * RT, 0), RT);
     const int A = (tile_live + kRowsPerWave - 1) / kRowsPerWave;
     const int nshare = (A >= 1 && A < kAttnWaves) ? kAttnWaves - A + 1 : 1;
     const bool shared = nshare > 1 && wave >= A - 1;
     const int sidx = shared ? wave - (A - 1) : 0;
-    const int row0 = rt * ROWS + (shared ? A - 1 : wave) * kRowsPerWave;  // first query row of this wave
+    const int row0 = rt * RT + (shared ? A - 1 : wave) * kRowsPerWave;  // first query row of this wave
     const bool active = row0 < live_rows;
     const int rho = row0 + l32;  // this lane's query row
     const int qn = rho / a.G, qh = rho - qn * a.G;
@@ -268,9 +269,9 @@ __global__ __launch_bounds__(kAttnWaves * kWave) void tree_attn_bf16_kernel(Attn
     }
     // ancestor bitmask rows of the nodes this workgroup serves, when the
     // split reaches the tree keys (masks then read LDS, not global memory)
-    const int n_first = (rt * ROWS) / a.G;
+    const int n_first = (rt * RT) / a.G;
     if (k_end > ctx) {
-        const int n_last = min((rt * ROWS + ROWS - 1) / a.G, a.n_max - 1);
+        const int n_last = min((rt * RT + RT - 1) / a.G, a.n_max - 1);
         const int words = (n_last - n_first + 1) * a.W;
         const uint64_t* src = a.anc + ((int64_t)b * a.n_max + n_first) * a.W;
         for (int w = tid; w < words; w += NT) s_anc[w] = src[w];
@@ -880,6 +881,15 @@ static AttnPlan attn_plan(const presto_attn_desc* d) {
     }
     p.tasks = (int64_t)d->batch * p.splits * per_pair;  // in compact mode an upper bound
     p.blocks = (p.tasks + 7) / 8 * 8;
+    // When the whole grid fits one round (one workgroup per CU), the tiles
+    // are balanced: the same number of row tiles, each a multiple of 32 rows
+    // (a 32-row block never straddles two tiles).  260 rows then make tiles
+    // of 160 and 100 rows instead of 256 and 4: a workgroup of 256 rows runs
+    // two waves per SIMD through every key block (about 1 us per block), one
+    // of 160 rows one and a quarter (the idle waves share the fifth block's
+    // keys), and the 4-row tiles, nearly idle, disappear.
+    if (!p.compact && p.tasks <= 256 && p.row_tiles > 1)
+        p.rows_per_tile = kRowsPerWave * ((p.rows + kRowsPerWave * p.row_tiles - 1) / (kRowsPerWave * p.row_tiles));
     return p;
 }
 
@@ -935,6 +945,7 @@ presto_status launch_tree_attention(const presto_attn_desc* d, const void* q, co
     a.G = p.G;
     a.W = (d->n_max + 63) / 64;
     a.row_tiles = p.row_tiles;
+    a.rows_per_tile = p.rows_per_tile;
     a.splits = p.splits;
     a.split_len = p.split_len;
     a.n_tasks = (int32_t)p.tasks;
