@@ -928,24 +928,27 @@ __global__ __launch_bounds__(kWave) void tree_alg2_kernel(TreeArgs a) {
 // asc): the nodes that best-first search commits, in pop order, are the
 // `budget` best non-root prefixes in that order (the closed form of Sec.
 // 4.2), sorted.  This kernel finds that set without popping one node at a
-// time.  One wavefront per sequence keeps in LDS
+// time.  One workgroup per sequence keeps in LDS
 //   T: the best (at most budget) prefixes materialised so far, sorted;
-//   P: pending prefixes, each the first child or the next sibling (in child
-//      order: S desc, rank asc, among the top-`branch` candidates) of a
-//      prefix that entered T, not materialised yet.
+//   P: pending prefixes, each the next sibling (in child order: S desc,
+//      rank asc, among the top-`branch` candidates) or a member of the
+//      first-child chain (below) of a prefix that entered T, not
+//      materialised yet.
 // A sweep merges all of P into T (every entry's new place from counting
 // comparisons; entries pushed past the budget are dropped for good, since
 // T's last entry only ever improves) and then, for every prefix of P that
-// entered T, pushes its first child and its next sibling, keeping a push
-// while T is not full or when it precedes T's last entry.  A prefix of the
-// optimal tree is always pushed (its parent, or its previous sibling,
+// entered T, pushes its next sibling and, if it ends a chain, the chain of
+// its first child, that child's first child, ... (CL levels; only a chain's
+// last member pushes the next chain), keeping a push while T is not full or
+// when it precedes T's last entry.  A prefix of the optimal tree is always
+// pushed (its parent, or its previous sibling, or the head of its chain
 // precedes it and so enters T when materialised) and never dropped (it
 // precedes every last entry T ever has), so T is the optimal tree once
-// nothing is pending.  A prefix is pushed at most once (by its parent, or by
-// its previous sibling), and a sweep pushes at most two prefixes per entry
-// that entered T, so P never holds more than 2 budget.  The number of
-// sweeps follows the depth of the tree (about 15 at depth 16), not the
-// budget.
+// nothing is pending.  A prefix is pushed at most once, and a sweep pushes
+// at most CL + 1 prefixes per entry that entered T, so P never holds more
+// than (CL + 1) budget.  The number of sweeps follows the depth of the tree
+// and the chain length, not the budget (at depth 16 and budget 64: about 15
+// with CL = 1, 6 with CL = 3).
 //
 // Every record carries its full rank-path key, its parent's S and the ranks
 // of its trigram context, so that a push reads no other record; a node's
