@@ -56,7 +56,7 @@ struct TreeArgs {
     int o_tmeta, o_tS, o_tkey, o_tplace;
     // frontier sweeps only: lambda, the sorted best set, the pending
     // prefixes and the parent positions
-    int o_lam, o_sw_t, o_sw_p, o_sw_par, o_sw_cnt, o_sw_np;
+    int o_lam, o_sw_t, o_sw_p, o_sw_p2, o_sw_par, o_sw_cnt, o_sw_np;
     uint32_t mag_k, mag_k3;  // ceil(2^32 / k), ceil(2^32 / k^3) (k > 1): n / d = umulhi(n, mag) for n < 2^20
 };
 
@@ -1013,7 +1013,8 @@ constexpr uint32_t kChainEnd = 1u << 18;  // record meta: this entry pushes the 
 // chain length.
 //
 // One workgroup of four waves per sequence.  Every wave holds all of T and
-// P in registers; the merge's comparisons are split over the waves (each
+// P in registers (from 8 slots of T on, only P's ord S: its records stay in
+// LDS, in two buffers, one read and one written by a sweep); the merge's comparisons are split over the waves (each
 // takes every fourth P entry in turn and its partial counts are summed
 // through LDS); the push candidates are scored before the merge, split into
 // tasks (first children, next siblings) per slot of P, and each task
@@ -1033,7 +1034,9 @@ __global__ __launch_bounds__(kSweepWaves * kWave) void tree_sweep_kernel(TreeArg
     int32_t* s_ids = reinterpret_cast<int32_t*>(lds + a.o_ids);
     float* s_lam = reinterpret_cast<float*>(lds + a.o_lam);
     uint4* s_t = reinterpret_cast<uint4*>(lds + a.o_sw_t);          // [NB] records, sorted
-    uint4* s_p = reinterpret_cast<uint4*>(lds + a.o_sw_p);          // [cap_p] records
+    constexpr bool PL = MT >= 8;  // P's records in LDS only
+    uint4* s_pc = reinterpret_cast<uint4*>(lds + a.o_sw_p);         // [cap_p] records: P of this sweep
+    uint4* s_pn = PL ? reinterpret_cast<uint4*>(lds + a.o_sw_p2) : s_pc;  // the pushes
     int32_t* s_par = reinterpret_cast<int32_t*>(lds + a.o_sw_par);  // [N] parent of node i
     int32_t* s_cnt = reinterpret_cast<int32_t*>(lds + a.o_sw_cnt);  // [NWV][MT + MP][64] partial counts
     int32_t* s_np = reinterpret_cast<int32_t*>(lds + a.o_sw_np);    // [2] pending counts, alternating
@@ -1185,7 +1188,7 @@ __global__ __launch_bounds__(kSweepWaves * kWave) void tree_sweep_kernel(TreeArg
         for (int i = 0; i < CL; ++i) {
             SwRec c;
             if (!first_child(par, i == 0, i == CL - 1, c)) break;
-            sw_store(s_p, n++, c);
+            sw_store(s_pc, n++, c);
             par = c;
         }
         s_np[0] = n;
@@ -1197,14 +1200,31 @@ __global__ __launch_bounds__(kSweepWaves * kWave) void tree_sweep_kernel(TreeArg
     int np = min(s_np[0], cap_p);
     while (np > 0) {
         // P in slots (entry u * 64 + lane), T likewise (position v * 64 + lane)
-        SwRec pr[MP], tr[MT];
+        SwRec pr[PL ? 1 : MP], tr[MT];  // P's records (register mode)
+        uint32_t pS[MP];                // P's ord S
         bool pv[MP], tv[MT];
 #pragma unroll
         for (int u = 0; u < MP; ++u) {
             pv[u] = u * kWave + lane < np;
-            pr[u] = SwRec{0u, 0u, 0u, 0u, 0u, 0u, 0u};
-            if (u * kWave < np) pr[u] = sw_load(s_p, min(u * kWave + lane, np - 1));
+            pS[u] = 0u;
+            if constexpr (PL) {
+                if (u * kWave < np) pS[u] = reinterpret_cast<const uint32_t*>(s_pc)[8 * min(u * kWave + lane, np - 1)];
+            } else {
+                pr[u] = SwRec{0u, 0u, 0u, 0u, 0u, 0u, 0u};
+                if (u * kWave < np) pr[u] = sw_load(s_pc, min(u * kWave + lane, np - 1));
+                pS[u] = pr[u].o;
+            }
         }
+        // P entry u * 64 + lane as a whole record (from LDS when only its
+        // ord S is held)
+        auto prec = [&](int u) __attribute__((always_inline)) {
+            if constexpr (PL) return sw_load(s_pc, min(u * kWave + lane, np - 1));
+            else return pr[u];
+        };
+        auto prec_at = [&](int u, int l) __attribute__((always_inline)) {
+            if constexpr (PL) return sw_load(s_pc, u * kWave + l);
+            else return sw_readlane(pr[u], l);
+        };
 #pragma unroll
         for (int v = 0; v < MT; ++v) {
             tv[v] = v * kWave + lane < nt;
@@ -1214,7 +1234,7 @@ __global__ __launch_bounds__(kSweepWaves * kWave) void tree_sweep_kernel(TreeArg
         // ord S of lanes without an entry: 0, below every score (ord32 of
         // -inf is 0x007fffff), so that comparisons of S need no masks
 #pragma unroll
-        for (int u = 0; u < MP; ++u) pr[u].o = pv[u] ? pr[u].o : 0u;
+        for (int u = 0; u < MP; ++u) pS[u] = pv[u] ? pS[u] : 0u;
 #pragma unroll
         for (int v = 0; v < MT; ++v) tr[v].o = tv[v] ? tr[v].o : 0u;
         if (tid == 0) s_np[cur ^ 1] = 0;  // last read a sweep ago, before two barriers
@@ -1260,8 +1280,8 @@ __global__ __launch_bounds__(kSweepWaves * kWave) void tree_sweep_kernel(TreeArg
             ea[i] = SwRec{0u, 0u, 0u, 0u, 0u, 0u, 0u};
         }
         if (EARLY) {
-            if (owner(0) == wv) score_chain(pr[0], pv[0], ea, oea);
-            if (owner(1) == wv) score_sibling(pr[0], pv[0], eb, oeb);
+            if (owner(0) == wv) score_chain(prec(0), pv[0], ea, oea);
+            if (owner(1) == wv) score_sibling(prec(0), pv[0], eb, oeb);
         }
 
         // merged places: a T entry moves down by the P entries before it; a P
@@ -1292,8 +1312,8 @@ __global__ __launch_bounds__(kSweepWaves * kWave) void tree_sweep_kernel(TreeArg
                 }
 #pragma unroll
                 for (int q = 0; q < AP; ++q) {
-                    const bool e = (pr[q].o == yo) & !((q == u) & (lane == l));
-                    pc[q] += (e & sw_key_less(y, pr[q])) ? 1 : 0;
+                    const bool e = (pS[q] == yo) & !((q == u) & (lane == l));
+                    if (__ballot(e) != 0ull) pc[q] += (e & sw_key_less(y, prec(q))) ? 1 : 0;
                 }
             };
 #pragma unroll
@@ -1302,8 +1322,8 @@ __global__ __launch_bounds__(kSweepWaves * kWave) void tree_sweep_kernel(TreeArg
                 for (int l0 = wv; l0 < cnt; l0 += 2 * NWV) {
                     const int l1 = l0 + NWV < cnt ? l0 + NWV : l0;
                     const bool two = l1 != l0;
-                    const uint32_t y0 = (uint32_t)__builtin_amdgcn_readlane((int)pr[u].o, l0);
-                    const uint32_t y1 = (uint32_t)__builtin_amdgcn_readlane((int)pr[u].o, l1);
+                    const uint32_t y0 = (uint32_t)__builtin_amdgcn_readlane((int)pS[u], l0);
+                    const uint32_t y1 = (uint32_t)__builtin_amdgcn_readlane((int)pS[u], l1);
                     int b0 = 0, b1 = 0;
                     uint64_t e0 = 0ull, e1 = 0ull;
 #pragma unroll
@@ -1316,13 +1336,13 @@ __global__ __launch_bounds__(kSweepWaves * kWave) void tree_sweep_kernel(TreeArg
                     }
 #pragma unroll
                     for (int q = 0; q < AP; ++q) {
-                        pc[q] += (pr[q].o < y0 ? 1 : 0) + ((two & (pr[q].o < y1)) ? 1 : 0);
+                        pc[q] += (pS[q] < y0 ? 1 : 0) + ((two & (pS[q] < y1)) ? 1 : 0);
                         const uint64_t self0 = q == u ? 1ull << l0 : 0ull, self1 = q == u ? 1ull << l1 : 0ull;
-                        e0 |= __builtin_amdgcn_uicmp(pr[q].o, y0, 32) & ~self0;
-                        e1 |= __builtin_amdgcn_uicmp(pr[q].o, y1, 32) & ~self1;
+                        e0 |= __builtin_amdgcn_uicmp(pS[q], y0, 32) & ~self0;
+                        e1 |= __builtin_amdgcn_uicmp(pS[q], y1, 32) & ~self1;
                     }
-                    if (e0 != 0ull) tie_fix(sw_readlane(pr[u], l0), u, l0, b0);
-                    if (two && e1 != 0ull) tie_fix(sw_readlane(pr[u], l1), u, l1, b1);
+                    if (e0 != 0ull) tie_fix(prec_at(u, l0), u, l0, b0);
+                    if (two && e1 != 0ull) tie_fix(prec_at(u, l1), u, l1, b1);
                     pc[u] += (lane == l0 ? b0 : 0) + ((two & (lane == l1)) ? b1 : 0);
                 }
             }
@@ -1375,7 +1395,7 @@ __global__ __launch_bounds__(kSweepWaves * kWave) void tree_sweep_kernel(TreeArg
         }
 #pragma unroll
         for (int u = 0; u < MP; ++u)
-            if ((MT + u) % NWV == wv && u * kWave < np && (pv[u] & (pc[u] < NB))) sw_store(s_t, pc[u], pr[u]);
+            if ((MT + u) % NWV == wv && u * kWave < np && (pv[u] & (pc[u] < NB))) sw_store(s_t, pc[u], prec(u));
         const int nt_new = min(NB, nt + np);
         const bool full = nt_new == NB;
         // T's last entry, from the registers
@@ -1392,7 +1412,7 @@ __global__ __launch_bounds__(kSweepWaves * kWave) void tree_sweep_kernel(TreeArg
             for (int u = 0; u < MP; ++u) {
                 if (u * kWave < np) {
                     const uint64_t m = __ballot(pv[u] & (pc[u] == NB - 1));
-                    if (m) last = sw_readlane(pr[u], __ffsll((unsigned long long)m) - 1);
+                    if (m) last = prec_at(u, __ffsll((unsigned long long)m) - 1);
                 }
             }
         }
@@ -1416,7 +1436,7 @@ __global__ __launch_bounds__(kSweepWaves * kWave) void tree_sweep_kernel(TreeArg
 #pragma unroll
             for (int i = 0; i < n; ++i) {
                 const int at = base + lanes_below(m[i]);
-                if (h[i] & (at < cap_p)) sw_store(s_p, at, c[i]);
+                if (h[i] & (at < cap_p)) sw_store(s_pn, at, c[i]);
                 base += __popcll(m[i]);
             }
         };
@@ -1434,7 +1454,7 @@ __global__ __launch_bounds__(kSweepWaves * kWave) void tree_sweep_kernel(TreeArg
                         ok[i] = oea[i];
                     }
                 } else {
-                    score_chain(pr[u], pv[u], c, ok);
+                    score_chain(prec(u), pv[u], c, ok);
                 }
                 bool h[CL];
 #pragma unroll
@@ -1444,7 +1464,7 @@ __global__ __launch_bounds__(kSweepWaves * kWave) void tree_sweep_kernel(TreeArg
             if (owner(2 * u + 1) == wv) {
                 SwRec c[1] = {eb};
                 bool ok = oeb;
-                if (!(EARLY && u == 0)) score_sibling(pr[u], pv[u], c[0], ok);
+                if (!(EARLY && u == 0)) score_sibling(prec(u), pv[u], c[0], ok);
                 bool h[1] = {(bool)(ok & in & (!full | sw_before(c[0], last)))};
                 push(h, c);
             }
@@ -1453,6 +1473,11 @@ __global__ __launch_bounds__(kSweepWaves * kWave) void tree_sweep_kernel(TreeArg
         __syncthreads();
         cur ^= 1;
         np = min(s_np[cur], cap_p);
+        if (PL) {
+            uint4* t = s_pc;
+            s_pc = s_pn;
+            s_pn = t;
+        }
     }
 
     // parents: node i >= 1 is T's position i - 1; the parent of a node of
@@ -1615,11 +1640,11 @@ static Alg2Layout alg2_layout(int D, int k, int branch, int budget) {
 // parent positions, then the lattice.
 struct SweepLayout {
     int total_no_rho, total_with_rho;
-    int o_lp, o_ids, o_lam, o_t, o_p, o_par, o_cnt, o_np, o_rho;
+    int o_lp, o_ids, o_lam, o_t, o_p, o_p2, o_par, o_cnt, o_np, o_rho;
 };
 
 // slots per lane of T and P for a budget (the kernel's MT and MP)
-static int sweep_mt(int budget) { return budget <= 64 ? 1 : (budget <= 128 ? 2 : 4); }
+static int sweep_mt(int budget) { return budget <= 64 ? 1 : (budget <= 128 ? 2 : (budget <= 256 ? 4 : 8)); }
 // chains of three first children at budgets <= 64 (8 -> 6 sweeps at depth 16 against chains of
 // two, 15 with none); at larger budgets the trees are wider and chains added entries without
 // removing sweeps
@@ -1635,6 +1660,7 @@ static SweepLayout sweep_layout(int D, int k, int N) {
     L.o_lam = off; off = align16(off + D * 4);
     L.o_t = off; off = align16(off + nb * 32);
     L.o_p = off; off = align16(off + (sweep_chain(nb) + 1) * nb * 32);
+    L.o_p2 = off; off = align16(off + (sweep_mt(nb) >= 8 ? (sweep_chain(nb) + 1) * nb * 32 : 0));  // P's second buffer
     L.o_par = off; off = align16(off + N * 4);
     L.o_cnt = off; off = align16(off + kSweepWaves * (sweep_mt(nb) + sweep_mp(nb)) * kWave * 4);
     L.o_np = off; off = align16(off + 2 * 4);
@@ -1644,11 +1670,12 @@ static SweepLayout sweep_layout(int D, int k, int N) {
     return L;
 }
 
-// Budgets the sweep kernel takes: above 256 its slots per lane would not
-// fit; at 32 and below popping one node at a time is faster (a sweep costs
-// about three pops, and a tree of depth 16 needs about 14 sweeps).
+// Budgets the sweep kernel takes: above 512 the slots per lane would not
+// fit (T's records stay in registers); at 32 and below popping one node at
+// a time is faster (a sweep costs about three pops, and a tree of depth 16
+// needs about 14 sweeps).
 static constexpr int kSweepMinBudget = 33;
-static constexpr int kSweepMaxBudget = 256;
+static constexpr int kSweepMaxBudget = 512;
 
 bool tree_build_fits(int D, int k, int branch, int N, int beam_width, bool alg2) {
     if (alg2) return alg2_layout(D, k, branch, N - 1).total_no_rho <= kTreeLdsBudget;
@@ -1714,7 +1741,8 @@ presto_status launch_build_tree(const presto_tree_desc* desc, const int32_t* ids
         const SweepLayout L = sweep_layout(a.D, a.k, a.N);
         a.beam_width = 0;
         a.o_lp = L.o_lp; a.o_ids = L.o_ids; a.o_lam = L.o_lam; a.o_rho = L.o_rho;
-        a.o_sw_t = L.o_t; a.o_sw_p = L.o_p; a.o_sw_par = L.o_par; a.o_sw_cnt = L.o_cnt; a.o_sw_np = L.o_np;
+        a.o_sw_t = L.o_t; a.o_sw_p = L.o_p; a.o_sw_p2 = L.o_p2; a.o_sw_par = L.o_par; a.o_sw_cnt = L.o_cnt;
+        a.o_sw_np = L.o_np;
         a.rho_in_lds = log_rho != nullptr && L.total_with_rho <= kTreeLdsBudget;
         const uint64_t k3 = (uint64_t)a.k * a.k * a.k;
         a.mag_k = (uint32_t)(((1ull << 32) + a.k - 1) / a.k);        // k > 1 only
@@ -1737,7 +1765,8 @@ presto_status launch_build_tree(const presto_tree_desc* desc, const int32_t* ids
         const int mt = sweep_mt(a.budget);
         if (mt == 1) { PRESTO_SWEEP(1, 4, 3) }
         else if (mt == 2) { PRESTO_SWEEP(2, 4, 1) }
-        else { PRESTO_SWEEP(4, 8, 1) }
+        else if (mt == 4) { PRESTO_SWEEP(4, 8, 1) }
+        else { PRESTO_SWEEP(8, 16, 1) }
 #undef PRESTO_SWEEP
 #undef PRESTO_SWEEP3
         if (st != PRESTO_OK) return st;
