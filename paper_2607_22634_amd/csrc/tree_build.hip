@@ -1046,41 +1046,57 @@ __global__ __launch_bounds__(kSweepWaves * kWave) void tree_sweep_kernel(TreeArg
 
     const int64_t tb = (int64_t)b * D * k;
     if (wv == 0) {
-        uint32_t r_lp[8], r_ids[8], r_rho[16];  // D * k <= 512 words
+        uint32_t r_lp[8], r_ids[8];  // D * k <= 512 words
         load_words(r_lp, reinterpret_cast<const uint32_t*>(a.logprob + tb), D * k, 0, lane);
         load_words(r_ids, reinterpret_cast<const uint32_t*>(a.ids + tb), D * k, 0, lane);
-        if constexpr (RHO == 1) load_words(r_rho, reinterpret_cast<const uint32_t*>(g_rho), rho_n, 0, lane);
         const float lam = lane < D ? a.lambda[(int64_t)b * a.lambda_stride + lane] : 0.f;
         store_words(reinterpret_cast<uint32_t*>(s_lp), r_lp, D * k, 0, lane);
         store_words(reinterpret_cast<uint32_t*>(s_ids), r_ids, D * k, 0, lane);
         if (lane < D) s_lam[lane] = lam;
-        if constexpr (RHO == 1) {
-            store_words(reinterpret_cast<uint32_t*>(s_rho), r_rho, rho_n, 0, lane);
-            if (rho_n > 16 * kWave)
-                stage_words(reinterpret_cast<uint32_t*>(s_rho) + 16 * kWave,
-                            reinterpret_cast<const uint32_t*>(g_rho) + 16 * kWave, rho_n - 16 * kWave,
-                            lane);
-        }
     }
-    __syncthreads();
     // Token scores fl(log q + fl(lambda * log rho)), NaN -> -inf, computed
     // once per trigram context in place of the lattice (or of the log q
     // table without one), so that scoring a node's children reads k values.
+    // Every thread stages the lattice with 32 words in flight, the first
+    // batch requested before the barrier that publishes log q and lambda.
     // A lattice read from global memory is scored on the fly instead.
-    if constexpr (RHO == 0) {
-        for (int i = tid; i < D * k; i += NT) {
-            const float v = s_lp[i];
-            s_lp[i] = (v == v) ? v : -INFINITY;
+    if constexpr (RHO == 1) {
+        constexpr int U = 32;
+        const uint32_t* gr = reinterpret_cast<const uint32_t*>(g_rho);
+        for (int base = 0; base < rho_n; base += U * NT) {
+            float x[U];
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const int i = base + u * NT + tid;
+                x[u] = i < rho_n ? __uint_as_float(gr[i]) : 0.f;
+            }
+            if (base == 0) __syncthreads();
+            // every log q and lambda of the batch read before the first store
+            // (a store between them would order each read after it)
+            float lq[U], lm[U];
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const int i = min(base + u * NT + tid, rho_n - 1);
+                const int row = k == 1 ? i : (int)__umulhi((uint32_t)i, a.mag_k3);
+                const int r = k == 1 ? 0 : i - (int)__umulhi((uint32_t)i, a.mag_k) * k;
+                lq[u] = s_lp[row * k + r];
+                lm[u] = s_lam[row];
+            }
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const int i = base + u * NT + tid;
+                const float t = lm[u] * x[u];
+                const float v = lq[u] + t;
+                if (i < rho_n) s_rho[i] = (v == v) ? v : -INFINITY;
+            }
         }
-    } else if constexpr (RHO == 1) {
-#pragma unroll 4
-        for (int i = tid; i < rho_n; i += NT) {
-            const int row = k == 1 ? i : (int)__umulhi((uint32_t)i, a.mag_k3);
-            const int r = k == 1 ? 0 : i - (int)__umulhi((uint32_t)i, a.mag_k) * k;
-            const float lq = s_lp[row * k + r];
-            const float t = s_lam[row] * s_rho[i];
-            const float v = lq + t;
-            s_rho[i] = (v == v) ? v : -INFINITY;
+    } else {
+        __syncthreads();
+        if constexpr (RHO == 0) {
+            for (int i = tid; i < D * k; i += NT) {
+                const float v = s_lp[i];
+                s_lp[i] = (v == v) ? v : -INFINITY;
+            }
         }
     }
     __syncthreads();
