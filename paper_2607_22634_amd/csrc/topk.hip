@@ -127,6 +127,7 @@ __global__ __launch_bounds__(kTopkWavesPerBlock * kWave) void topk_partial_kerne
     __shared__ __align__(16) float cand_v[kTopkWavesPerBlock][kCandCap];
     __shared__ int32_t cand_i[kTopkWavesPerBlock][kGroupCap];
     __shared__ uint32_t cand_n[kTopkWavesPerBlock];
+    __shared__ uint32_t rank_keys[kTopkWavesPerBlock][kWave];  // valid bf16 keys, one per lane
 
     const int wave = threadIdx.x / kWave, lane = lane_id();
     const int64_t gw = (int64_t)blockIdx.x * kTopkWavesPerBlock + wave;
@@ -270,18 +271,50 @@ __global__ __launch_bounds__(kTopkWavesPerBlock * kWave) void topk_partial_kerne
         uint32_t x[C];
 #pragma unroll
         for (int c = 0; c < C; ++c) x[c] = (c == 0 || total > c * kWave) ? entry_key32(c * kWave + lane) : 0u;
-        uint32_t mine = 0u;
-        const int nc = (total + kWave - 1) / kWave;  // slots holding entries
-        for (int j = 0; j < k; ++j) {
-            uint32_t lmax = x[0];
+        // The valid keys (nonzero: at or above the bound) are usually about
+        // k.  Up to a wave of them are packed one per lane, and each finds its
+        // output place as its rank among them (keys are unique): one compare
+        // per valid key instead of k wave-wide maxima.
+        uint64_t bal[C];
+        int nv = 0;
 #pragma unroll
-            for (int c = 1; c < C; ++c) lmax = (c < nc && x[c] > lmax) ? x[c] : lmax;
-            const uint32_t m = wave_max_u32_dpp(lmax);
-            mine = lane == j ? m : mine;
-#pragma unroll
-            for (int c = 0; c < C; ++c) x[c] = x[c] == m ? 0u : x[c];
+        for (int c = 0; c < C; ++c) {
+            bal[c] = __ballot(x[c] != 0u);
+            nv += __popcll(bal[c]);
         }
-        if (lane < k) out[lane] = mine ? key64(mine) : 0ull;
+        if (nv <= kWave) {
+            int pos = 0;
+#pragma unroll
+            for (int c = 0; c < C; ++c) {
+                const int below = (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(bal[c] >> 32),
+                                                                 __builtin_amdgcn_mbcnt_lo((uint32_t)bal[c], 0u));
+                if (x[c] != 0u) rank_keys[wave][pos + below] = x[c];
+                pos += __popcll(bal[c]);
+            }
+            __builtin_amdgcn_wave_barrier();
+            const uint32_t my = lane < nv ? rank_keys[wave][lane] : 0u;
+            int rank = 0;
+            for (int j = 0; j < nv; ++j)
+                rank += (uint32_t)__builtin_amdgcn_readlane((int)my, j) > my ? 1 : 0;
+            if (lane < nv) {
+                if (rank < k) out[rank] = key64(my);
+            } else if (lane < k) {
+                out[lane] = 0ull;  // fewer than k valid entries
+            }
+        } else {
+            uint32_t mine = 0u;
+            const int nc = (total + kWave - 1) / kWave;  // slots holding entries
+            for (int j = 0; j < k; ++j) {
+                uint32_t lmax = x[0];
+#pragma unroll
+                for (int c = 1; c < C; ++c) lmax = (c < nc && x[c] > lmax) ? x[c] : lmax;
+                const uint32_t m = wave_max_u32_dpp(lmax);
+                mine = lane == j ? m : mine;
+#pragma unroll
+                for (int c = 0; c < C; ++c) x[c] = x[c] == m ? 0u : x[c];
+            }
+            if (lane < k) out[lane] = mine ? key64(mine) : 0ull;
+        }
     } else if (total <= kWave) {
         // one candidate per lane (keys are unique); k rounds of wave max,
         // retiring the lane that held it (0 past the last valid entry)
