@@ -207,3 +207,27 @@ def test_topk_fallback_count_on_ties():
     torch.cuda.synchronize()
     _compare(np.ascontiguousarray(store[:1]), "bf16", k, ids, lp, lse)
     assert P.topk_fallback_chunks(ws) == 0
+
+
+@pytest.mark.parametrize("k", [1, 5, 8, 10])
+def test_topk_tie_runs_around_a_wave_of_candidates(k):
+    """Runs of 63, 64 and 65 equal maxima in one chunk (in the first and in
+    a later chunk): up to 64 entries at or above the chunk's bound each
+    lane takes one and is placed by rank, above 64 the chunk takes the
+    wave-maximum selection; a run spread one per group over more groups
+    than the candidate list holds takes the exact pass.  The winners are
+    the run's lowest ids (value desc, id asc)."""
+    rng = np.random.default_rng([k, 64])
+    V = 151936
+    runs = [(0, 63), (0, 64), (0, 65), (4096 + 8, 64), (4096 + 8, 65), (2 * 4096 + 3, 64)]
+    x = np.clip(rng.standard_normal((len(runs) + 1, V)) * 2, -8, 8).astype(np.float32)
+    for r, (start, n) in enumerate(runs):
+        x[r, start:start + n] = 12.0
+    x[len(runs), 0:64 * 8:8] = 12.0  # one entry in each of 64 groups
+    store = sy.cast(x, "bf16")
+    ids, lp, lse = P.presto_topk(to_dev(store, "bf16"), k)
+    torch.cuda.synchronize()
+    _compare(store, "bf16", k, ids, lp, lse)
+    got = to_host(ids)
+    for r, (start, n) in enumerate(runs):
+        np.testing.assert_array_equal(got[r], np.arange(start, start + k))
