@@ -23,6 +23,8 @@
 // holds more than (committed + 1) entries.
 #include <math.h>
 
+#include <type_traits>
+
 #include "common.hpp"
 
 // Scores must round exactly as fl(log q + fl(lambda * log rho)) and
@@ -1057,39 +1059,54 @@ __global__ __launch_bounds__(kSweepWaves * kWave) void tree_sweep_kernel(TreeArg
     // Token scores fl(log q + fl(lambda * log rho)), NaN -> -inf, computed
     // once per trigram context in place of the lattice (or of the log q
     // table without one), so that scoring a node's children reads k values.
-    // Every thread stages the lattice with 32 words in flight, the first
-    // batch requested before the barrier that publishes log q and lambda.
-    // A lattice read from global memory is scored on the fly instead.
+    // Every thread stages the lattice with up to 32 words in flight, the
+    // first batch requested before the barrier that publishes log q and
+    // lambda.  A lattice of at most 8 words per thread takes a copy of the
+    // loop unrolled 8 times (its cold instruction fetch is part of every
+    // launch).  A lattice read from global memory is scored on the fly.
     if constexpr (RHO == 1) {
-        constexpr int U = 32;
         const uint32_t* gr = reinterpret_cast<const uint32_t*>(g_rho);
-        for (int base = 0; base < rho_n; base += U * NT) {
-            float x[U];
+        auto stage = [&](auto uc) __attribute__((always_inline)) {
+            constexpr int U = decltype(uc)::value;
+            for (int base = 0; base < rho_n; base += U * NT) {
+                // words of this batch per thread that exist for some thread
+                // (bounded in the small copy only: in the large one the
+                // bound's branches would split the batch's requests)
+                const int nu = U > 8 ? U : min(U, (rho_n - base + NT - 1) / NT);
+                float x[U];
 #pragma unroll
-            for (int u = 0; u < U; ++u) {
-                const int i = base + u * NT + tid;
-                x[u] = i < rho_n ? __uint_as_float(gr[i]) : 0.f;
-            }
-            if (base == 0) __syncthreads();
-            // every log q and lambda of the batch read before the first store
-            // (a store between them would order each read after it)
-            float lq[U], lm[U];
+                for (int u = 0; u < U; ++u) {
+                    const int i = base + u * NT + tid;
+                    x[u] = (u < nu && i < rho_n) ? __uint_as_float(gr[i]) : 0.f;
+                }
+                if (base == 0) __syncthreads();
+                // every log q and lambda of the batch read before the first
+                // store (a store between them would order each read after it)
+                float lq[U], lm[U];
 #pragma unroll
-            for (int u = 0; u < U; ++u) {
-                const int i = min(base + u * NT + tid, rho_n - 1);
-                const int row = k == 1 ? i : (int)__umulhi((uint32_t)i, a.mag_k3);
-                const int r = k == 1 ? 0 : i - (int)__umulhi((uint32_t)i, a.mag_k) * k;
-                lq[u] = s_lp[row * k + r];
-                lm[u] = s_lam[row];
-            }
+                for (int u = 0; u < U; ++u) {
+                    lq[u] = lm[u] = 0.f;
+                    if (u < nu) {
+                        const int i = min(base + u * NT + tid, rho_n - 1);
+                        const int row = k == 1 ? i : (int)__umulhi((uint32_t)i, a.mag_k3);
+                        const int r = k == 1 ? 0 : i - (int)__umulhi((uint32_t)i, a.mag_k) * k;
+                        lq[u] = s_lp[row * k + r];
+                        lm[u] = s_lam[row];
+                    }
+                }
 #pragma unroll
-            for (int u = 0; u < U; ++u) {
-                const int i = base + u * NT + tid;
-                const float t = lm[u] * x[u];
-                const float v = lq[u] + t;
-                if (i < rho_n) s_rho[i] = (v == v) ? v : -INFINITY;
+                for (int u = 0; u < U; ++u) {
+                    const int i = base + u * NT + tid;
+                    const float t = lm[u] * x[u];
+                    const float v = lq[u] + t;
+                    if (u < nu && i < rho_n) s_rho[i] = (v == v) ? v : -INFINITY;
+                }
             }
-        }
+        };
+        if (rho_n <= 8 * NT)
+            stage(std::integral_constant<int, 8>{});
+        else
+            stage(std::integral_constant<int, 32>{});
     } else {
         __syncthreads();
         if constexpr (RHO == 0) {
