@@ -9,8 +9,10 @@
 // on its orderable bits for k > 8) is a lower bound on the chunk's k-th value, so only the
 // 16-byte groups whose maximum reaches it can hold a top-k entry (at least
 // k of them, normally about k); they are appended to a per-wave LDS list of
-// up to 256 values, their entries at or above the bound are keyed (one or
-// up to four per lane) and the k best taken by k rounds of wave max.  A
+// up to 256 values and their entries at or above the bound are keyed.  With
+// bf16 values, up to 64 such entries take one lane each and are placed in
+// the output by their rank among them; otherwise (and for fp32) the k best
+// are taken by k rounds of wave max over up to four keys per lane.  A
 // chunk with more candidate groups than the list holds (massive ties) falls
 // back to k rounds of exact wave-wide selection over the chunk re-read from
 // memory, and marks its partial so that the merge can count such chunks.
