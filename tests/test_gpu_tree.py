@@ -69,7 +69,7 @@ def _random_batch(seed, b, D, k, quant):
 @pytest.mark.parametrize("D,k,branch,B", [(1, 1, 1, 1), (3, 2, 2, 4), (4, 3, 2, 40), (5, 3, 3, 200),
                                           (6, 2, 1, 9), (16, 8, 8, 256), (32, 4, 3, 128),
                                           (8, 16, 16, 255), (2, 16, 5, 63), (12, 5, 5, 130),
-                                          (10, 4, 4, 511)])
+                                          (10, 4, 4, 511), (20, 5, 5, 300), (7, 5, 5, 100)])
 @pytest.mark.parametrize("quant", [False, True])
 def test_tree_matches_oracle_random(D, k, branch, B, quant):
     ids, lp, R, root = _random_batch([D, k, B, int(quant)], 24, D, k, quant)
