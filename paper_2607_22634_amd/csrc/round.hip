@@ -76,7 +76,10 @@ __global__ void select_slots_kernel(int32_t batch, int32_t n_max, int32_t depth,
 }
 
 // One lane per (composite row, mask word).  Composite row r = n * (1 + S) + j:
-// node n (j = 0) or its slot j (1 .. S).  Column c = m * (1 + S) + jj.
+// node n (j = 0) or its slot j (1 .. S).  Column c = m * (1 + S) + jj.  The
+// node columns of a word (jj = 0) are consecutive nodes m0 .. m1, so their
+// bits are one field of node n's ancestor row, spread out (1 + S) apart; the
+// slot columns a slot row sees are one range, its own block.
 __global__ void flatten_slots_kernel(int32_t batch, int32_t n_max, int32_t S,
                                      const int32_t* __restrict__ depth,
                                      const uint64_t* __restrict__ anc,
@@ -102,14 +105,24 @@ __global__ void flatten_slots_kernel(int32_t batch, int32_t n_max, int32_t S,
     }
     uint64_t bits = 0;
     if (live) {
-        const uint64_t* arow = anc + ((int64_t)b * n_max + n) * W;
-        const int c_end = min(64, R - 64 * w);
-        for (int t = 0; t < c_end; ++t) {
-            const int c = 64 * w + t;
-            const int m = c / blk, jj = c - m * blk;
-            const bool on = jj == 0 ? (m < nn && ((arow[m >> 6] >> (m & 63)) & 1ull))
-                                    : (j > 0 && m == n);
-            bits |= (uint64_t)on << t;
+        const int c0 = 64 * w, c1 = min(c0 + 64, R);  // columns [c0, c1)
+        // node columns m * blk in [c0, c1) with m < nn: at most 32 (blk >= 2)
+        const int m0 = (c0 + blk - 1) / blk;
+        const int m1 = min((c1 - 1) / blk, nn - 1);
+        if (m0 <= m1) {
+            const uint64_t* arow = anc + ((int64_t)b * n_max + n) * W;
+            const int wa = m0 >> 6, sh = m0 & 63;
+            uint64_t f = arow[wa] >> sh;
+            if (sh != 0 && wa + 1 < W) f |= arow[wa + 1] << (64 - sh);
+            for (int q = 0; q <= m1 - m0; ++q) bits |= ((f >> q) & 1ull) << ((m0 + q) * blk - c0);
+        }
+        // a slot row sees its whole block: columns n * blk + 1 .. n * blk + S
+        if (j > 0) {
+            const int s0 = max(n * blk + 1, c0), s1 = min(n * blk + S + 1, c1);  // [s0, s1)
+            if (s0 < s1) {
+                const int len = s1 - s0;
+                bits |= (len == 64 ? ~0ull : (1ull << len) - 1ull) << (s0 - c0);
+            }
         }
     }
     anc_out[((int64_t)b * R + r) * WO + w] = bits;

@@ -173,7 +173,7 @@ def test_topk_rows_bad_index_is_flagged():
     np.testing.assert_array_equal(to_host(ids)[[0, 2, 4]], rid)
 
 
-@pytest.mark.parametrize("cfg,slots", [(1, 3), (2, 1), (2, 14), (3, 4), (4, 2), (5, 3)])
+@pytest.mark.parametrize("cfg,slots", [(1, 3), (2, 1), (2, 14), (3, 4), (4, 2), (5, 3), (1, 64), (2, 64), (2, 63)])
 def test_flatten_slots_matches_oracle(cfg, slots):
     w, th, _ = _accept_for(cfg)
     root_pos = np.random.default_rng(cfg).integers(0, 9000, w.batch).astype(np.int32)
